@@ -1,0 +1,225 @@
+"""CPU oracle for the Deep Parity Bottleneck -- TEST INFRASTRUCTURE ONLY.
+
+A plain, slow, fp64 implementation of what the paper defines (§2.1 parity
+decoder, §2.2 parity encoder, App. A.4 seed matrix).  It is written in C
+(`dpb_oracle.c`, built with gcc) and wrapped here with ctypes.  It shares no
+code with the HIP library, and only the tests, the smoke check and the
+benchmark's CPU-baseline leg may import it.
+
+Functions whose parity against the paper cannot be pinned (they rest on a
+reading of a point the paper leaves open) say "parity unpinned" below.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "dpb_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc -O2 -fopenmp into oracle/liboracle.so."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp"
+        cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", _SRC, "-o", tmp, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    lib = ctypes.CDLL(build())
+    u32, i32, i64, u64, dbl = ctypes.c_uint32, ctypes.c_int, ctypes.c_int64, ctypes.c_uint64, ctypes.c_double
+    P = ctypes.c_void_p
+    sig = {
+        "oracle_gf_mul": (u32, [u32, u32, i32, u32]),
+        "oracle_gf_pow": (u32, [u32, u64, i32, u32]),
+        "oracle_gf_inv": (u32, [u32, i32, u32]),
+        "oracle_gf_trace": (u32, [u32, i32, u32]),
+        "oracle_gf_order": (u32, [u32, i32, u32]),
+        "oracle_poly_irreducible": (i32, [u64]),
+        "oracle_pick_poly": (u32, [i32]),
+        "oracle_primitive_element": (u32, [i32, u32]),
+        "oracle_ceil_log2": (i32, [i32]),
+        "oracle_masks": (i32, [i32, i32, P]),
+        "oracle_phi": (dbl, [i32, P, i64, i32]),
+        "oracle_generators": (i32, [i32, P, P, u64, P]),
+        "oracle_hierarchy": (i32, [i32, i32, i32, i32, i32, i32, P, P, P]),
+        "oracle_encode": (i32, [i32, P, i32, P, P, P, P, P, i64, P, P, P, P]),
+        "oracle_decode": (None, [i32, P, i32, P, P, i64, P]),
+        "oracle_decode_bwd": (None, [i32, P, i32, P, P, i64, P, P]),
+        "oracle_walsh_spectrum": (i32, [i32, P, i32, P]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _ptr(a: np.ndarray):
+    assert a.flags["C_CONTIGUOUS"]
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+# ---------------------------------------------------------------- field
+
+def gf_mul(a: int, b: int, t: int, poly: int) -> int:
+    return int(_load().oracle_gf_mul(a, b, t, poly))
+
+
+def gf_pow(a: int, e: int, t: int, poly: int) -> int:
+    return int(_load().oracle_gf_pow(a, e, t, poly))
+
+
+def gf_inv(a: int, t: int, poly: int) -> int:
+    """xi^{-1} = xi^{2^t-2}, 0 -> 0 (App. A.4, inverse-by-exponentiation eq.)."""
+    return int(_load().oracle_gf_inv(a, t, poly))
+
+
+def gf_trace(y: int, t: int, poly: int) -> int:
+    """Absolute trace (App. A.2)."""
+    return int(_load().oracle_gf_trace(y, t, poly))
+
+
+def gf_order(a: int, t: int, poly: int) -> int:
+    return int(_load().oracle_gf_order(a, t, poly))
+
+
+def poly_irreducible(f: int) -> bool:
+    return bool(_load().oracle_poly_irreducible(f))
+
+
+def pick_poly(t: int) -> int:
+    """Modulus p(z) of degree t: fewest terms, then smallest value.
+
+    Reproduces the paper's two choices (App. A.4); other degrees are a
+    reading of the paper (parity unpinned for t not in {10, 11}).
+    """
+    return int(_load().oracle_pick_poly(t))
+
+
+def primitive_element(t: int, poly: int) -> int:
+    return int(_load().oracle_primitive_element(t, poly))
+
+
+def ceil_log2(d: int) -> int:
+    return int(_load().oracle_ceil_log2(d))
+
+
+# ---------------------------------------------------------------- dictionary
+
+def masks(d: int, r: int) -> np.ndarray:
+    """Packed rows of the seed matrix M (App. A.4, parity-mask-row eq.).
+
+    d = 2^t follows the paper exactly.  d not a power of two and r > 2t are
+    readings (parity unpinned against the paper).
+    """
+    out = np.zeros(d, dtype=np.uint32)
+    t = _load().oracle_masks(d, r, _ptr(out))
+    if t < 0:
+        raise ValueError(f"oracle_masks: unsupported d={d}, r={r}")
+    return out
+
+
+def phi(d: int, m: np.ndarray, i: int) -> np.ndarray:
+    """Direction phi_i (§2.1 Eqs. 1-2) as an fp64 vector, one entry at a time."""
+    lib = _load()
+    return np.array([lib.oracle_phi(d, _ptr(m), int(i), k) for k in range(d)], dtype=np.float64)
+
+
+def generators(nbits: Sequence[int], delta: Sequence[int], seed: int = 0) -> list[np.ndarray]:
+    """Per-level generator sets (§2.2; sampling rule is a reading, parity unpinned)."""
+    L = len(nbits)
+    nb = np.asarray(nbits, dtype=np.int32)
+    dl = np.asarray(delta, dtype=np.int32)
+    total = int(dl[1:].sum()) if L > 1 else 0
+    out = np.zeros(max(total, 1), dtype=np.uint32)
+    rc = _load().oracle_generators(L, _ptr(nb), _ptr(dl), seed & (2**64 - 1), _ptr(out))
+    if rc < 0:
+        raise ValueError("oracle_generators: level too small for its branching")
+    res, off = [np.zeros(0, dtype=np.uint32)], 0
+    for l in range(1, L):
+        res.append(out[off:off + dl[l]].copy())
+        off += int(dl[l])
+    return res
+
+
+def hierarchy(d: int, n: int, levels: int, branching: int, beam: int, k: int):
+    """Config terms -> (n_l, Delta_l, K_l) (reading of App. G Table 6; parity unpinned)."""
+    nb = np.zeros(levels, dtype=np.int32)
+    dl = np.zeros(levels, dtype=np.int32)
+    ac = np.zeros(levels, dtype=np.int32)
+    if _load().oracle_hierarchy(d, n, levels, branching, beam, k, _ptr(nb), _ptr(dl), _ptr(ac)) < 0:
+        raise ValueError("oracle_hierarchy: bad arguments")
+    return nb.tolist(), dl.tolist(), ac.tolist()
+
+
+# ---------------------------------------------------------------- the path
+
+def encode(d: int, m: np.ndarray, nbits, active, delta, gens: list[np.ndarray], x: np.ndarray):
+    """Beam-search encoder (§2.2).  x: [T, d] (any float dtype; used as fp64).
+
+    Returns idx [T, k_tot] int32, coef [T, k_tot] fp64, and the boundary and
+    order margins [T, L] used to exempt near-ties when comparing with a
+    finite-precision implementation.
+    """
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    T = x.shape[0]
+    assert x.shape[1] == d
+    L = len(nbits)
+    nb = np.asarray(nbits, dtype=np.int32)
+    ac = np.asarray(active, dtype=np.int32)
+    dl = np.asarray(delta, dtype=np.int32)
+    g = np.concatenate([np.asarray(gg, dtype=np.uint32) for gg in gens[1:]]) if L > 1 else np.zeros(1, np.uint32)
+    g = np.ascontiguousarray(g if g.size else np.zeros(1, np.uint32), dtype=np.uint32)
+    k_tot = int(ac.sum())
+    idx = np.zeros((T, k_tot), dtype=np.int32)
+    coef = np.zeros((T, k_tot), dtype=np.float64)
+    margin = np.zeros((T, L), dtype=np.float64)
+    order = np.zeros((T, L), dtype=np.float64)
+    rc = _load().oracle_encode(d, _ptr(m), L, _ptr(nb), _ptr(ac), _ptr(dl), _ptr(g), _ptr(x), T,
+                               _ptr(idx), _ptr(coef), _ptr(margin), _ptr(order))
+    if rc < 0:
+        raise ValueError("oracle_encode: bad arguments")
+    return idx, coef, margin, order
+
+
+def decode(d: int, m: np.ndarray, idx: np.ndarray, coef: np.ndarray) -> np.ndarray:
+    """x_hat = sum_i a_i phi_i (§2.1), fp64.  idx < 0 slots are padding."""
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    coef = np.ascontiguousarray(coef, dtype=np.float64)
+    T, k = idx.shape
+    y = np.zeros((T, d), dtype=np.float64)
+    _load().oracle_decode(d, _ptr(m), k, _ptr(idx), _ptr(coef), T, _ptr(y))
+    return y
+
+
+def decode_bwd(d: int, m: np.ndarray, idx: np.ndarray, g: np.ndarray):
+    """grad_coef = Phi_S^T g and grad_x = Phi_S grad_coef, fp64."""
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    g = np.ascontiguousarray(g, dtype=np.float64)
+    T, k = idx.shape
+    gc = np.zeros((T, k), dtype=np.float64)
+    gx = np.zeros((T, d), dtype=np.float64)
+    _load().oracle_decode_bwd(d, _ptr(m), k, _ptr(idx), _ptr(g), T, _ptr(gc), _ptr(gx))
+    return gc, gx
+
+
+def walsh_spectrum(d: int, m: np.ndarray, r: int) -> np.ndarray:
+    """S(u) = sum_iota (-1)^{popcount(M_iota & u)}, all u < 2^r, via one FWHT."""
+    S = np.zeros(1 << r, dtype=np.int64)
+    if _load().oracle_walsh_spectrum(d, _ptr(m), r, _ptr(S)) < 0:
+        raise ValueError("oracle_walsh_spectrum: r out of range")
+    return S

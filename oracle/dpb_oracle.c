@@ -1,0 +1,494 @@
+/*
+ * Deep Parity Bottleneck (DPB) -- CPU ORACLE.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is a plain, slow, fp64 implementation of
+ * what the paper "Scaling Interpretable Transformers with Parity Bottleneck
+ * Layers" defines, written so that each step can be checked against the paper
+ * by eye.  It shares no code, header, table or constant generator with the
+ * HIP library; only tests, the smoke check and the benchmark's CPU-baseline leg
+ * may load it.  The product path never calls it.
+ *
+ * Readings taken where the paper is silent (each also listed in the design doc):
+ *   R1  indices are 0-based: phi_i = e_i for 0 <= i < d  (Eq. 2 writes i <= d).
+ *   R2  bit p of an index (LSB = 0) pairs with column p of M; columns 0..t-1
+ *       hold coord(xi), columns t..2t-1 hold coord(xi^-1)  (App. A.4).
+ *   R3  the modulus p(z) is the irreducible polynomial of degree t with the
+ *       fewest terms, ties broken by the smaller integer value; this gives the
+ *       paper's z^10+z^3+1 and z^11+z^2+1 (App. A.4, irreducible-polys eq.).
+ *   R4  d not a power of two: t = ceil(log2 d); coordinate 0 is the field
+ *       element 0 and coordinate iota >= 1 is alpha^(iota-1), alpha the
+ *       numerically smallest primitive element.
+ *   R5  more index bits than 2t: column 2t+q of row iota is Tr(z^q xi_iota^3).
+ *   R6  generators of level l are distinct values in [2^n_{l-1}, 2^n_l) drawn
+ *       by rejection from SplitMix64 (Steele, Lea, Flood 2014), state
+ *       seed ^ (l * 0x9E3779B97F4A7C15), low n_l bits of each draw (§2.2).
+ *   R7  candidates reached through several (parent, generator) pairs are one
+ *       candidate; if fewer than K_l exist the code is padded with (-1, 0).
+ *   R8  AbsTopK key: |score| descending, then index ascending; coefficient is
+ *       the signed score; level-0 coefficient is x_iota itself (Eq. 2).
+ *   R9  every level is emitted, level-major, so k_tot = sum_l K_l.
+ *   R10 selection scores are the raw scores (EMA standardization with mean 0,
+ *       std 1, i.e. its initial state; §2.2 "Score Standardization").
+ *   R11 backward: grad_coef = Phi_S^T g, grad_x = Phi_S grad_coef.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------ */
+/* Finite field F_{2^t} in the polynomial basis (App. A.2).            */
+/* An element is a t-bit vector (xi_0..xi_{t-1}) read as               */
+/* xi_0 + xi_1 z + ... + xi_{t-1} z^{t-1}.  `poly` holds all t+1        */
+/* coefficients of p(z), including the z^t term.                       */
+/* ------------------------------------------------------------------ */
+
+/* Product of two field elements: carry-less polynomial product reduced
+ * modulo p(z).  Written as the schoolbook sum  a * sum_i b_i z^i  where
+ * each a z^i is formed by repeated multiplication by z and reduction. */
+uint32_t oracle_gf_mul(uint32_t a, uint32_t b, int t, uint32_t poly)
+{
+    uint32_t acc = 0;
+    uint32_t a_zi = a; /* a * z^i mod p, for i = 0, 1, ... */
+    for (int i = 0; i < t; ++i) {
+        if ((b >> i) & 1u) acc ^= a_zi;
+        a_zi <<= 1;
+        if ((a_zi >> t) & 1u) a_zi ^= poly; /* subtract (= add) p(z) */
+    }
+    return acc;
+}
+
+uint32_t oracle_gf_pow(uint32_t a, uint64_t e, int t, uint32_t poly)
+{
+    uint32_t result = 1;
+    uint32_t base = a;
+    while (e) {
+        if (e & 1u) result = oracle_gf_mul(result, base, t, poly);
+        base = oracle_gf_mul(base, base, t, poly);
+        e >>= 1;
+    }
+    return result;
+}
+
+/* Inverse by exponentiation xi^{-1} = xi^{2^t - 2}, with 0^{-1} = 0
+ * (App. A.3 convention; App. A.4 inverse-by-exponentiation eq.). */
+uint32_t oracle_gf_inv(uint32_t a, int t, uint32_t poly)
+{
+    if (a == 0) return 0;
+    return oracle_gf_pow(a, ((uint64_t)1 << t) - 2, t, poly);
+}
+
+/* Absolute trace Tr(y) = y + y^2 + y^4 + ... + y^{2^{t-1}} (App. A.2,
+ * absolute-trace eq.).  The sum is a field element equal to 0 or 1. */
+uint32_t oracle_gf_trace(uint32_t y, int t, uint32_t poly)
+{
+    uint32_t sum = 0;
+    uint32_t term = y;
+    for (int j = 0; j < t; ++j) {
+        sum ^= term;
+        term = oracle_gf_mul(term, term, t, poly);
+    }
+    return sum;
+}
+
+/* ---- binary polynomials (for choosing p(z)) ---- */
+static int bpoly_degree(uint64_t a)
+{
+    int deg = -1;
+    while (a) { ++deg; a >>= 1; }
+    return deg;
+}
+
+static uint64_t bpoly_mod(uint64_t a, uint64_t b)
+{
+    int db = bpoly_degree(b);
+    int da = bpoly_degree(a);
+    while (a && da >= db) {
+        a ^= b << (da - db);
+        da = bpoly_degree(a);
+    }
+    return a;
+}
+
+/* Irreducible iff no binary polynomial of degree 1..floor(t/2) divides it. */
+int oracle_poly_irreducible(uint64_t f)
+{
+    int t = bpoly_degree(f);
+    if (t < 1) return 0;
+    for (int deg = 1; deg <= t / 2; ++deg) {
+        for (uint64_t g = (uint64_t)1 << deg; g < ((uint64_t)1 << (deg + 1)); ++g) {
+            if (bpoly_mod(f, g) == 0) return 0;
+        }
+    }
+    return 1;
+}
+
+static int popcount64(uint64_t v)
+{
+    int c = 0;
+    while (v) { c += (int)(v & 1u); v >>= 1; }
+    return c;
+}
+
+/* Reading R3: fewest terms first, then smallest value. */
+uint32_t oracle_pick_poly(int t)
+{
+    if (t < 1 || t > 16) return 0;
+    for (int weight = 2; weight <= t + 1; ++weight) {
+        for (uint64_t f = ((uint64_t)1 << t) | 1u; f < ((uint64_t)1 << (t + 1)); f += 2) {
+            if (popcount64(f) != weight) continue;
+            if (oracle_poly_irreducible(f)) return (uint32_t)f;
+        }
+    }
+    return 0;
+}
+
+/* Multiplicative order of a nonzero element, by walking its powers. */
+uint32_t oracle_gf_order(uint32_t a, int t, uint32_t poly)
+{
+    if (a == 0) return 0;
+    uint32_t x = a;
+    uint32_t k = 1;
+    while (x != 1) {
+        x = oracle_gf_mul(x, a, t, poly);
+        ++k;
+        if (k > ((uint32_t)1 << t)) return 0;
+    }
+    return k;
+}
+
+/* Reading R4: numerically smallest element of order 2^t - 1. */
+uint32_t oracle_primitive_element(int t, uint32_t poly)
+{
+    uint32_t full = ((uint32_t)1 << t) - 1;
+    for (uint32_t a = 1; a <= full; ++a) {
+        if (oracle_gf_order(a, t, poly) == full) return a;
+    }
+    return 0;
+}
+
+int oracle_ceil_log2(int d)
+{
+    int t = 0;
+    while ((1 << t) < d) ++t;
+    return t;
+}
+
+/* ------------------------------------------------------------------ */
+/* Seed matrix M, one packed row word per coordinate (App. A.4,        */
+/* parity-mask-row eq.): row iota = (coord xi_iota, coord xi_iota^-1),  */
+/* plus reading R5 columns when r > 2t.  Returns t, or -1 on bad args. */
+/* ------------------------------------------------------------------ */
+int oracle_masks(int d, int r, uint32_t* masks)
+{
+    if (d < 2) return -1;
+    int t = oracle_ceil_log2(d);
+    if (2 * t > 31 || r > 31 || r > 3 * t) return -1;
+    uint32_t poly = oracle_pick_poly(t);
+    int power_of_two = (d == (1 << t));
+    uint32_t alpha = power_of_two ? 0 : oracle_primitive_element(t, poly);
+    uint32_t alpha_pow = 1; /* alpha^(iota-1) */
+    for (int iota = 0; iota < d; ++iota) {
+        uint32_t xi;
+        if (power_of_two) {
+            xi = (uint32_t)iota; /* coordinates = bits of iota */
+        } else if (iota == 0) {
+            xi = 0;
+        } else {
+            xi = alpha_pow;
+            alpha_pow = oracle_gf_mul(alpha_pow, alpha, t, poly);
+        }
+        uint32_t inv = oracle_gf_inv(xi, t, poly);
+        uint32_t row = xi | (inv << t);
+        if (r > 2 * t) {
+            uint32_t cube = oracle_gf_mul(oracle_gf_mul(xi, xi, t, poly), xi, t, poly);
+            uint32_t zq = 1; /* z^q */
+            for (int q = 0; q < r - 2 * t; ++q) {
+                uint32_t bit = oracle_gf_trace(oracle_gf_mul(zq, cube, t, poly), t, poly);
+                row |= bit << (2 * t + q);
+                zq = oracle_gf_mul(zq, 2u, t, poly);
+            }
+        }
+        masks[iota] = row;
+    }
+    return t;
+}
+
+/* ------------------------------------------------------------------ */
+/* Hashed direction entry (§2.1 Eq. 1 with App. A.4 packed-parity eq.) */
+/* and the dictionary with basis override (§2.1 Eq. 2).                */
+/* ------------------------------------------------------------------ */
+static int parity32(uint32_t v)
+{
+    return __builtin_parity(v); /* popcount(v) mod 2 */
+}
+
+double oracle_phi(int d, const uint32_t* masks, int64_t i, int iota)
+{
+    if (i < d) return (i == iota) ? 1.0 : 0.0;
+    int bit = parity32(masks[iota] & (uint32_t)i); /* (M bits(i))_iota */
+    double mag = 1.0 / sqrt((double)d);
+    return bit ? -mag : mag; /* R maps 0 -> +1, 1 -> -1 */
+}
+
+/* ------------------------------------------------------------------ */
+/* Generators (§2.2, reading R6).                                      */
+/* ------------------------------------------------------------------ */
+static uint64_t splitmix64_next(uint64_t* state)
+{
+    uint64_t z = (*state += 0x9E3779B97F4A7C15ull);
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+/* gens receives sum_{l>=1} delta[l] words, level by level. */
+int oracle_generators(int levels, const int* nbits, const int* delta, uint64_t seed, uint32_t* gens)
+{
+    int out = 0;
+    for (int l = 1; l < levels; ++l) {
+        uint64_t lo = (uint64_t)1 << nbits[l - 1];
+        uint64_t hi = (uint64_t)1 << nbits[l];
+        if ((uint64_t)delta[l] > hi - lo) return -1;
+        uint64_t state = seed ^ ((uint64_t)l * 0x9E3779B97F4A7C15ull);
+        int have = 0;
+        while (have < delta[l]) {
+            uint64_t g = splitmix64_next(&state) & (hi - 1);
+            if (g < lo) continue;
+            int dup = 0;
+            for (int j = 0; j < have; ++j) if (gens[out + j] == (uint32_t)g) dup = 1;
+            if (dup) continue;
+            gens[out + have] = (uint32_t)g;
+            ++have;
+        }
+        out += delta[l];
+    }
+    return out;
+}
+
+/* Configuration terms (d, n, L levels, branching b, beam B, k) to the
+ * per-level table (n_l, Delta_l, K_l) of App. G Table 6.  L counts level 0;
+ * n_0 = ceil(log2 d), n_{L-1} = n, evenly spaced in between (floor);
+ * Delta_l = b; K_l = B below the last level and k on the last level. */
+int oracle_hierarchy(int d, int n, int levels, int branching, int beam, int k,
+                     int* nbits, int* delta, int* active)
+{
+    if (levels < 1 || d < 2) return -1;
+    int n0 = oracle_ceil_log2(d);
+    for (int l = 0; l < levels; ++l) {
+        nbits[l] = (levels == 1) ? n0 : n0 + (l * (n - n0)) / (levels - 1);
+        delta[l] = (l == 0) ? 0 : branching;
+        active[l] = (l == levels - 1) ? k : beam;
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* Encoder: top-down beam search (§2.2).                               */
+/* ------------------------------------------------------------------ */
+typedef struct {
+    double score; /* signed */
+    int64_t index;
+} cand_t;
+
+/* AbsTopK order (reading R8): larger |score| first, then smaller index. */
+static int cand_cmp(const void* pa, const void* pb)
+{
+    const cand_t* a = (const cand_t*)pa;
+    const cand_t* b = (const cand_t*)pb;
+    double fa = fabs(a->score), fb = fabs(b->score);
+    if (fa > fb) return -1;
+    if (fa < fb) return 1;
+    if (a->index < b->index) return -1;
+    if (a->index > b->index) return 1;
+    return 0;
+}
+
+static int idx_cmp(const void* pa, const void* pb)
+{
+    int64_t a = *(const int64_t*)pa, b = *(const int64_t*)pb;
+    return (a > b) - (a < b);
+}
+
+/* <phi_c, x> as a dense dot product with phi_c built from its definition. */
+static double dense_score(int d, const uint32_t* masks, int64_t c, const double* x)
+{
+    double s = 0.0;
+    for (int iota = 0; iota < d; ++iota) s += oracle_phi(d, masks, c, iota) * x[iota];
+    return s;
+}
+
+/* Records the selection margins used to decide which GPU/oracle
+ * differences come from near-ties:  boundary = (|s|_(K) - |s|_(K+1)) / |s|_(K)
+ * (infinite without a (K+1)-th candidate) and order = smallest relative gap
+ * between consecutive selected scores (infinite for K <= 1). */
+static void margins_of(const cand_t* sorted, int n, int K, double* boundary, double* order)
+{
+    *boundary = INFINITY;
+    *order = INFINITY;
+    int take = K < n ? K : n;
+    if (n > K && K > 0) {
+        double a = fabs(sorted[K - 1].score), b = fabs(sorted[K].score);
+        *boundary = (a > 0.0) ? (a - b) / a : 0.0;
+    }
+    for (int i = 0; i + 1 < take; ++i) {
+        double a = fabs(sorted[i].score), b = fabs(sorted[i + 1].score);
+        double m = (a > 0.0) ? (a - b) / a : 0.0;
+        if (m < *order) *order = m;
+    }
+}
+
+/*
+ * x: [T, d] fp64.  idx/coef: [T, k_tot] level-major.  margin/order_margin:
+ * [T, levels] (may be NULL).  gens: level-by-level generator words.
+ * Returns 0, or -1 on bad arguments.
+ */
+int oracle_encode(int d, const uint32_t* masks, int levels, const int* nbits, const int* active,
+                  const int* delta, const uint32_t* gens, const double* x, int64_t T,
+                  int32_t* idx, double* coef, double* margin, double* order_margin)
+{
+    int k_tot = 0;
+    int max_cand = d;
+    for (int l = 0; l < levels; ++l) {
+        k_tot += active[l];
+        if (l > 0 && active[l - 1] * delta[l] > max_cand) max_cand = active[l - 1] * delta[l];
+    }
+    if (active[0] > d) return -1;
+
+#pragma omp parallel
+    {
+        cand_t* cand = (cand_t*)malloc(sizeof(cand_t) * (size_t)max_cand);
+        int64_t* ids = (int64_t*)malloc(sizeof(int64_t) * (size_t)max_cand);
+        int64_t* parents = (int64_t*)malloc(sizeof(int64_t) * (size_t)(max_cand + 1));
+#pragma omp for schedule(dynamic, 16)
+        for (int64_t tok = 0; tok < T; ++tok) {
+            const double* xt = x + tok * d;
+            int32_t* out_idx = idx + tok * k_tot;
+            double* out_coef = coef + tok * k_tot;
+            int slot = 0;
+            int n_parents = 0;
+
+            /* Level 0: basis features, score = x_iota (a coordinate read). */
+            for (int iota = 0; iota < d; ++iota) {
+                cand[iota].score = xt[iota];
+                cand[iota].index = iota;
+            }
+            qsort(cand, (size_t)d, sizeof(cand_t), cand_cmp);
+            if (margin) margins_of(cand, d, active[0], &margin[tok * levels], &order_margin[tok * levels]);
+            for (int i = 0; i < active[0]; ++i) {
+                out_idx[slot] = (int32_t)cand[i].index;
+                out_coef[slot] = cand[i].score;
+                parents[n_parents++] = cand[i].index;
+                ++slot;
+            }
+
+            /* Levels l >= 1: children p XOR g_j of the active parents. */
+            const uint32_t* g = gens;
+            for (int l = 1; l < levels; ++l) {
+                int n_ids = 0;
+                for (int p = 0; p < n_parents; ++p)
+                    for (int j = 0; j < delta[l]; ++j) ids[n_ids++] = parents[p] ^ (int64_t)g[j];
+                qsort(ids, (size_t)n_ids, sizeof(int64_t), idx_cmp);
+                int n_cand = 0;
+                for (int i = 0; i < n_ids; ++i) {
+                    if (i > 0 && ids[i] == ids[i - 1]) continue; /* reading R7 */
+                    cand[n_cand].index = ids[i];
+                    cand[n_cand].score = dense_score(d, masks, ids[i], xt);
+                    ++n_cand;
+                }
+                qsort(cand, (size_t)n_cand, sizeof(cand_t), cand_cmp);
+                if (margin)
+                    margins_of(cand, n_cand, active[l], &margin[tok * levels + l],
+                               &order_margin[tok * levels + l]);
+                n_parents = 0;
+                for (int i = 0; i < active[l]; ++i) {
+                    if (i < n_cand) {
+                        out_idx[slot] = (int32_t)cand[i].index;
+                        out_coef[slot] = cand[i].score;
+                        parents[n_parents++] = cand[i].index;
+                    } else {
+                        out_idx[slot] = -1;
+                        out_coef[slot] = 0.0;
+                    }
+                    ++slot;
+                }
+                g += delta[l];
+            }
+        }
+        free(cand);
+        free(ids);
+        free(parents);
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* Decoder  x_hat = sum_{i in S} a_i phi_i  (§2.1) and its backward.   */
+/* Slots with index < 0 are padding and contribute nothing.            */
+/* ------------------------------------------------------------------ */
+void oracle_decode(int d, const uint32_t* masks, int k_tot, const int32_t* idx, const double* coef,
+                   int64_t T, double* y)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t tok = 0; tok < T; ++tok) {
+        double* yt = y + tok * d;
+        for (int iota = 0; iota < d; ++iota) yt[iota] = 0.0;
+        for (int s = 0; s < k_tot; ++s) {
+            int64_t i = idx[tok * k_tot + s];
+            if (i < 0) continue;
+            double a = coef[tok * k_tot + s];
+            for (int iota = 0; iota < d; ++iota) yt[iota] += a * oracle_phi(d, masks, i, iota);
+        }
+    }
+}
+
+/* grad_coef[s] = <phi_{idx_s}, g>;  grad_x = sum_s grad_coef[s] phi_{idx_s}. */
+void oracle_decode_bwd(int d, const uint32_t* masks, int k_tot, const int32_t* idx, const double* g,
+                       int64_t T, double* grad_coef, double* grad_x)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t tok = 0; tok < T; ++tok) {
+        const double* gt = g + tok * d;
+        double* gc = grad_coef + tok * k_tot;
+        double* gx = grad_x + tok * d;
+        for (int iota = 0; iota < d; ++iota) gx[iota] = 0.0;
+        for (int s = 0; s < k_tot; ++s) {
+            int64_t i = idx[tok * k_tot + s];
+            gc[s] = 0.0;
+            if (i < 0) continue;
+            double acc = 0.0;
+            for (int iota = 0; iota < d; ++iota) acc += oracle_phi(d, masks, i, iota) * gt[iota];
+            gc[s] = acc;
+        }
+        for (int s = 0; s < k_tot; ++s) {
+            int64_t i = idx[tok * k_tot + s];
+            if (i < 0) continue;
+            for (int iota = 0; iota < d; ++iota) gx[iota] += gc[s] * oracle_phi(d, masks, i, iota);
+        }
+    }
+}
+
+/* ------------------------------------------------------------------ */
+/* Coherence spectrum S(u) = sum_iota (-1)^{popcount(M_iota & u)} for   */
+/* every u in [0, 2^r):  the Walsh-Hadamard transform of the histogram  */
+/* of row masks (restricted to r bits).  For u = i XOR j of two hashed  */
+/* indices, <phi_i, phi_j> = S(u) / d (App. A.1 hamming-correlation eq.,*/
+/* with the linearity of parity, §2.1 Eq. 4).                          */
+/* ------------------------------------------------------------------ */
+int oracle_walsh_spectrum(int d, const uint32_t* masks, int r, int64_t* S)
+{
+    if (r < 1 || r > 26) return -1;
+    int64_t n = (int64_t)1 << r;
+    for (int64_t u = 0; u < n; ++u) S[u] = 0;
+    for (int iota = 0; iota < d; ++iota) S[masks[iota] & (uint32_t)(n - 1)] += 1;
+    for (int64_t h = 1; h < n; h <<= 1) {
+        for (int64_t base = 0; base < n; base += 2 * h) {
+            for (int64_t u = base; u < base + h; ++u) {
+                int64_t a = S[u], b = S[u + h];
+                S[u] = a + b;
+                S[u + h] = a - b;
+            }
+        }
+    }
+    return 0;
+}
