@@ -1,0 +1,339 @@
+// C ABI of libdpb.so: argument validation, plan lifetime, launches.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <new>
+
+#include "../../include/dpb.h"
+#include "dpb_internal.hpp"
+
+using dpb::DevPlan;
+using dpb::Hierarchy;
+
+namespace {
+
+int pow2_at_least(int v)
+{
+    int p = 1;
+    while (p < v) p <<= 1;
+    return p;
+}
+
+int table_status(int rc) { return rc; }
+
+// Builds the host tables and the DevPlan layout of a validated hierarchy.
+dpb_status fill_plan(dpb_plan* plan, const Hierarchy& h, const uint32_t* gens, uint64_t seed)
+{
+    plan->h = h;
+    int rc = dpb::build_masks(h.d, h.level_bits[h.levels - 1], &plan->masks_h);
+    if (rc) return (dpb_status)table_status(rc);
+    if (gens) {
+        rc = dpb::check_generators(h, gens);
+        if (rc) return (dpb_status)rc;
+        size_t total = 0;
+        for (int l = 1; l < h.levels; ++l) total += h.branching[l];
+        plan->gens_h.assign(gens, gens + total);
+    } else {
+        rc = dpb::draw_generators(h, seed, &plan->gens_h);
+        if (rc) return (dpb_status)rc;
+    }
+
+    DevPlan& P = plan->dev;
+    P.d = h.d;
+    P.dp = (h.d + dpb::kChunk - 1) / dpb::kChunk * dpb::kChunk;
+    P.nchunk = P.dp / dpb::kChunk;
+    P.levels = h.levels;
+    P.rsd = (float)(1.0 / std::sqrt((double)h.d));
+    P.k_tot = 0;
+    P.kmax = 0;
+    int goff = 0;
+    int64_t gamma_off = 0;
+    for (int l = 0; l < dpb::kMaxLevels; ++l) {
+        const bool live = l < h.levels;
+        P.level_bits[l] = live ? h.level_bits[l] : 0;
+        P.delta[l] = live && l ? h.branching[l] : 0;
+        P.active[l] = live ? h.active[l] : 0;
+        P.slot_base[l] = P.k_tot;
+        P.k_tot += P.active[l];
+        if (P.active[l] > P.kmax) P.kmax = P.active[l];
+        P.mblocks[l] = (P.delta[l] + 15) / 16;
+        P.cpad[l] = l && live ? pow2_at_least(h.active[l - 1] * h.branching[l]) : 0;
+        P.gens_off[l] = goff;
+        goff += P.delta[l];
+        P.gamma_off[l] = gamma_off;
+        gamma_off += (int64_t)P.mblocks[l] * P.nchunk * 64;
+    }
+    return DPB_OK;
+}
+
+// Child sign patterns gamma_j = R(M g_j) (§2.2 child-scoring equation) laid
+// out as MFMA A fragments: lane L of fragment (mb, c) holds generator row
+// 16*mb + L%16 at coordinates 32c + 8*(L/16) + e, e = 0..7, as bf16 +-1.
+void build_gamma_fragments(const dpb_plan* plan, std::vector<uint16_t>* out)
+{
+    const DevPlan& P = plan->dev;
+    int64_t total = 0;
+    for (int l = 1; l < P.levels; ++l) total += (int64_t)P.mblocks[l] * P.nchunk * 64 * 8;
+    out->assign((size_t)total, 0);
+    for (int l = 1; l < P.levels; ++l) {
+        const uint32_t* g = plan->gens_h.data() + P.gens_off[l];
+        for (int mb = 0; mb < P.mblocks[l]; ++mb)
+            for (int c = 0; c < P.nchunk; ++c)
+                for (int lane = 0; lane < 64; ++lane) {
+                    const int j = 16 * mb + (lane & 15);
+                    uint16_t* dst = out->data() + (P.gamma_off[l] + ((int64_t)mb * P.nchunk + c) * 64 + lane) * 8;
+                    for (int e = 0; e < 8; ++e) {
+                        const int iota = 32 * c + 8 * (lane >> 4) + e;
+                        uint16_t v = 0;
+                        if (j < P.delta[l] && iota < P.d)
+                            v = (__builtin_popcount(plan->masks_h[iota] & g[j]) & 1) ? 0xBF80 : 0x3F80;
+                        dst[e] = v;
+                    }
+                }
+    }
+}
+
+dpb_status upload(dpb_plan* plan)
+{
+    DevPlan& P = plan->dev;
+    std::vector<uint16_t> gamma;
+    build_gamma_fragments(plan, &gamma);
+    std::vector<uint32_t> masks_p(P.dp, 0);
+    std::copy(plan->masks_h.begin(), plan->masks_h.end(), masks_p.begin());
+
+    auto align = [](size_t v) { return (v + 255) & ~(size_t)255; };
+    const size_t masks_bytes = align(masks_p.size() * 4);
+    const size_t gens_bytes = align(std::max<size_t>(plan->gens_h.size(), 1) * 4);
+    const size_t gamma_bytes = align(std::max<size_t>(gamma.size(), 8) * 2);
+    if (hipGetDevice(&plan->device) != hipSuccess) {
+        (void)hipGetLastError();
+        return DPB_EHIP;
+    }
+    void* mem = nullptr;
+    if (hipMalloc(&mem, masks_bytes + gens_bytes + gamma_bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        return DPB_ENOMEM;
+    }
+    plan->dev_alloc = mem;
+    char* base = (char*)mem;
+    P.masks = (const uint32_t*)base;
+    P.gens = (const uint32_t*)(base + masks_bytes);
+    P.gamma = (const uint4*)(base + masks_bytes + gens_bytes);
+    hipError_t e = hipMemcpy(base, masks_p.data(), masks_p.size() * 4, hipMemcpyHostToDevice);
+    if (e == hipSuccess && !plan->gens_h.empty())
+        e = hipMemcpy(base + masks_bytes, plan->gens_h.data(), plan->gens_h.size() * 4, hipMemcpyHostToDevice);
+    if (e == hipSuccess && !gamma.empty())
+        e = hipMemcpy(base + masks_bytes + gens_bytes, gamma.data(), gamma.size() * 2, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return DPB_EHIP;
+    }
+    return DPB_OK;
+}
+
+dpb_status create(dpb_plan** out, const Hierarchy& h, const uint32_t* gens, uint64_t seed)
+{
+    if (!out) return DPB_EINVAL;
+    *out = nullptr;
+    int rc = dpb::validate_hierarchy(h);
+    if (rc) return (dpb_status)rc;
+    dpb_plan* plan = new (std::nothrow) dpb_plan();
+    if (!plan) return DPB_ENOMEM;
+    dpb_status s = fill_plan(plan, h, gens, seed);
+    if (s == DPB_OK && !dpb::plan_fits(plan->dev)) s = DPB_EUNSUPPORTED;
+    if (s == DPB_OK) s = upload(plan);
+    if (s != DPB_OK) {
+        dpb_plan_destroy(plan);
+        return s;
+    }
+    *out = plan;
+    return DPB_OK;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+dpb_status check_call(const dpb_plan* plan, int64_t T)
+{
+    if (!plan || !plan->dev_alloc || T < 0) return DPB_EINVAL;
+    if (T > ((int64_t)1 << 40)) return DPB_EUNSUPPORTED;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return DPB_EHIP;
+    }
+    return dev == plan->device ? DPB_OK : DPB_EINVAL;
+}
+
+bool dtype_ok(dpb_dtype t) { return t == DPB_F32 || t == DPB_BF16; }
+
+dpb_status launched(hipError_t e)
+{
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return DPB_EHIP;
+    }
+    return DPB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dpb_status_string(dpb_status s)
+{
+    switch (s) {
+    case DPB_OK: return "DPB_OK";
+    case DPB_EINVAL: return "DPB_EINVAL: invalid argument";
+    case DPB_EUNSUPPORTED: return "DPB_EUNSUPPORTED: configuration not supported by this build";
+    case DPB_EHIP: return "DPB_EHIP: HIP runtime or launch failure";
+    case DPB_ENOMEM: return "DPB_ENOMEM: allocation failed";
+    }
+    return "DPB: unknown status";
+}
+
+dpb_status dpb_hierarchy(int d, int n_bits, int levels, int branching, int beam, int k, int* level_bits,
+                         int* branching_out, int* active_out)
+{
+    if (!level_bits || !branching_out || !active_out) return DPB_EINVAL;
+    Hierarchy h;
+    int rc = dpb::hierarchy_from_terms(d, n_bits, levels, branching, beam, k, &h);
+    if (rc) return (dpb_status)rc;
+    for (int l = 0; l < levels; ++l) {
+        level_bits[l] = h.level_bits[l];
+        branching_out[l] = h.branching[l];
+        active_out[l] = h.active[l];
+    }
+    return DPB_OK;
+}
+
+dpb_status dpb_build_tables(int d, int levels, const int* level_bits, const int* branching, uint64_t seed,
+                            uint32_t* masks_out, uint32_t* gens_out)
+{
+    if (!level_bits || !branching || levels < 1 || levels > DPB_MAX_LEVELS || !masks_out) return DPB_EINVAL;
+    Hierarchy h;
+    h.d = d;
+    h.levels = levels;
+    for (int l = 0; l < levels; ++l) {
+        h.level_bits[l] = level_bits[l];
+        h.branching[l] = l ? branching[l] : 0;
+        h.active[l] = 1;
+    }
+    if (d < 2) return DPB_EINVAL;
+    for (int l = 1; l < levels; ++l) {
+        if (h.level_bits[l] <= h.level_bits[l - 1] || h.branching[l] < 1) return DPB_EINVAL;
+        if ((uint64_t)h.branching[l] > ((uint64_t)1 << h.level_bits[l]) - ((uint64_t)1 << h.level_bits[l - 1]))
+            return DPB_EINVAL;
+    }
+    if (h.level_bits[0] < dpb::field_degree(d) || h.level_bits[levels - 1] > 31) return DPB_EINVAL;
+    std::vector<uint32_t> m, g;
+    int rc = dpb::build_masks(d, h.level_bits[levels - 1], &m);
+    if (rc) return (dpb_status)rc;
+    std::memcpy(masks_out, m.data(), m.size() * 4);
+    if (levels > 1) {
+        if (!gens_out) return DPB_EINVAL;
+        dpb::draw_generators(h, seed, &g);
+        std::memcpy(gens_out, g.data(), g.size() * 4);
+    }
+    return DPB_OK;
+}
+
+dpb_status dpb_plan_create(dpb_plan** out, int d, int n_bits, int levels, int branching, int beam, int k,
+                           uint64_t seed)
+{
+    if (!out) return DPB_EINVAL;
+    *out = nullptr;
+    Hierarchy h;
+    int rc = dpb::hierarchy_from_terms(d, n_bits, levels, branching, beam, k, &h);
+    if (rc) return (dpb_status)rc;
+    return create(out, h, nullptr, seed);
+}
+
+dpb_status dpb_plan_create_ex(dpb_plan** out, int d, int levels, const int* level_bits, const int* branching,
+                              const int* active, const uint32_t* generators, uint64_t seed)
+{
+    if (!out) return DPB_EINVAL;
+    *out = nullptr;
+    if (!level_bits || !active || (levels > 1 && !branching) || levels < 1 || levels > DPB_MAX_LEVELS)
+        return DPB_EINVAL;
+    Hierarchy h;
+    h.d = d;
+    h.levels = levels;
+    for (int l = 0; l < levels; ++l) {
+        h.level_bits[l] = level_bits[l];
+        h.branching[l] = l ? branching[l] : 0;
+        h.active[l] = active[l];
+    }
+    return create(out, h, generators, seed);
+}
+
+void dpb_plan_destroy(dpb_plan* plan)
+{
+    if (!plan) return;
+    if (plan->dev_alloc) {
+        int cur = -1;
+        (void)hipGetDevice(&cur);
+        if (cur != plan->device) (void)hipSetDevice(plan->device);
+        (void)hipFree(plan->dev_alloc);
+        if (cur != plan->device && cur >= 0) (void)hipSetDevice(cur);
+        (void)hipGetLastError();
+    }
+    delete plan;
+}
+
+int dpb_plan_code_width(const dpb_plan* plan) { return plan ? plan->dev.k_tot : 0; }
+
+dpb_status dpb_plan_describe(const dpb_plan* plan, int* d, int* levels, int* level_bits, int* branching,
+                             int* active, uint32_t* masks, uint32_t* gens)
+{
+    if (!plan) return DPB_EINVAL;
+    const Hierarchy& h = plan->h;
+    if (d) *d = h.d;
+    if (levels) *levels = h.levels;
+    for (int l = 0; l < h.levels; ++l) {
+        if (level_bits) level_bits[l] = h.level_bits[l];
+        if (branching) branching[l] = h.branching[l];
+        if (active) active[l] = h.active[l];
+    }
+    if (masks) std::memcpy(masks, plan->masks_h.data(), plan->masks_h.size() * 4);
+    if (gens && !plan->gens_h.empty()) std::memcpy(gens, plan->gens_h.data(), plan->gens_h.size() * 4);
+    return DPB_OK;
+}
+
+dpb_status dpb_encode(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T, int32_t* idx,
+                      float* coef, void* stream)
+{
+    dpb_status s = check_call(plan, T);
+    if (s) return s;
+    if (!dtype_ok(x_dtype)) return DPB_EINVAL;
+    if (T == 0) return DPB_OK;
+    if (!x || !idx || !coef || !aligned16(x) || !aligned16(idx) || !aligned16(coef)) return DPB_EINVAL;
+    return launched(dpb::launch_encode(plan->dev, x, x_dtype == DPB_BF16, T, idx, coef, (hipStream_t)stream));
+}
+
+dpb_status dpb_decode(const dpb_plan* plan, const int32_t* idx, const float* coef, int64_t T, void* y,
+                      dpb_dtype y_dtype, void* stream)
+{
+    dpb_status s = check_call(plan, T);
+    if (s) return s;
+    if (!dtype_ok(y_dtype)) return DPB_EINVAL;
+    if (T == 0) return DPB_OK;
+    if (!idx || !coef || !y || !aligned16(idx) || !aligned16(coef) || !aligned16(y)) return DPB_EINVAL;
+    return launched(dpb::launch_decode(plan->dev, idx, coef, T, y, y_dtype == DPB_BF16, (hipStream_t)stream));
+}
+
+dpb_status dpb_decode_bwd(const dpb_plan* plan, const int32_t* idx, const void* grad_y, dpb_dtype g_dtype,
+                          int64_t T, float* grad_coef, void* grad_x, dpb_dtype gx_dtype, void* stream)
+{
+    dpb_status s = check_call(plan, T);
+    if (s) return s;
+    if (!dtype_ok(g_dtype) || !dtype_ok(gx_dtype)) return DPB_EINVAL;
+    if (T == 0) return DPB_OK;
+    if (!idx || !grad_y || !grad_coef || !grad_x || !aligned16(idx) || !aligned16(grad_y) ||
+        !aligned16(grad_coef) || !aligned16(grad_x))
+        return DPB_EINVAL;
+    return launched(dpb::launch_decode_bwd(plan->dev, idx, grad_y, g_dtype == DPB_BF16, T, grad_coef, grad_x,
+                                           gx_dtype == DPB_BF16, (hipStream_t)stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,105 @@
+"""CPU tests of the C ABI: exports, host tables against the oracle, argument checks.
+
+No compute call runs here (no GPU): error paths that the host detects before
+any launch, and the host-only table construction, are what these cover.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_20652_amd import binding, inputs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(binding.lib_path):
+        from paper_2607_20652_amd import build
+        build.build()
+    return binding.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    header = open(os.path.join(ROOT, "include", "dpb.h")).read()
+    declared = set(re.findall(r"\b(dpb_[a-z_]+)\s*\(", header))
+    assert {"dpb_encode", "dpb_decode", "dpb_decode_bwd", "dpb_plan_create"} <= declared
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+@pytest.mark.parametrize("name", list(inputs.WORKLOADS))
+def test_hierarchy_matches_oracle(lib, name):
+    w = inputs.workload(name)
+    got = binding.hierarchy(w.d, w.n, w.levels, w.branching, w.beam, w.k)
+    want = oracle.hierarchy(w.d, w.n, w.levels, w.branching, w.beam, w.k)
+    assert got == tuple(want) or list(got) == list(want)
+
+
+@pytest.mark.parametrize("name", list(inputs.WORKLOADS))
+@pytest.mark.parametrize("seed", [0, 12345])
+def test_tables_match_oracle_bit_exactly(lib, name, seed):
+    w = inputs.workload(name)
+    nb, br, _ = oracle.hierarchy(w.d, w.n, w.levels, w.branching, w.beam, w.k)
+    m, g = binding.build_tables(w.d, nb, br, seed)
+    assert np.array_equal(np.array(m, np.uint32), oracle.masks(w.d, w.n))
+    og = oracle.generators(nb, br, seed)
+    assert np.array_equal(np.array(g, np.uint32), np.concatenate(og[1:]))
+
+
+@pytest.mark.parametrize("d,n", [(2, 2), (3, 4), (64, 12), (100, 14), (256, 16), (1000, 20), (2048, 22), (4096, 30)])
+def test_masks_match_oracle_other_widths(lib, d, n):
+    t = oracle.ceil_log2(d)
+    m, _ = binding.build_tables(d, [t, n], [0, 1], 0)
+    assert np.array_equal(np.array(m, np.uint32), oracle.masks(d, n))
+
+
+def _create(lib, *args):
+    h = ctypes.c_void_p()
+    st = lib.dpb_plan_create(ctypes.byref(h), *args)
+    if st == 0:
+        lib.dpb_plan_destroy(h)
+    return st
+
+
+@pytest.mark.parametrize("args,status", [
+    ((1, 12, 3, 16, 4, 8, 0), -1),        # d < 2
+    ((64, 12, 0, 16, 4, 8, 0), -1),       # no levels
+    ((64, 12, 9, 16, 4, 8, 0), -1),       # too many levels
+    ((64, 31, 3, 16, 4, 8, 0), -1),       # index wider than 30 bits
+    ((64, 12, 3, 16, 65, 8, 0), -1),      # K_0 > d
+    ((64, 12, 3, 16, 4, 65, 0), -1),      # K_2 > K_1 * Delta_2
+    ((64, 12, 3, 0, 4, 8, 0), -1),        # no children
+    ((64, 7, 3, 16, 4, 8, 0), -1),        # level bits not increasing
+    ((64, 12, 3, 500, 4, 8, 0), -1),      # more generators than level 1 holds (448)
+    ((8192, 26, 2, 16, 4, 8, 0), -2),     # wider than this build supports
+])
+def test_plan_create_rejects_bad_arguments_before_touching_the_gpu(lib, args, status):
+    assert _create(lib, *args) == status
+
+
+def test_compute_calls_reject_null_plan(lib):
+    P = ctypes.c_void_p
+    assert lib.dpb_encode(None, P(16), 0, 4, P(16), P(16), None) == -1
+    assert lib.dpb_decode(None, P(16), P(16), 4, P(16), 0, None) == -1
+    assert lib.dpb_decode_bwd(None, P(16), P(16), 0, 4, P(16), P(16), 0, None) == -1
+    assert lib.dpb_plan_code_width(None) == 0
+    lib.dpb_plan_destroy(None)
+
+
+def test_create_ex_rejects_bad_generators(lib):
+    h = ctypes.c_void_p()
+    lb, br, ac = binding._ints([6, 9]), binding._ints([0, 2]), binding._ints([4, 4])
+    dup = (ctypes.c_uint32 * 2)(100, 100)
+    assert lib.dpb_plan_create_ex(ctypes.byref(h), 64, 2, lb, br, ac, dup, 0) == -1
+    low = (ctypes.c_uint32 * 2)(63, 100)       # 63 lies in level 0
+    assert lib.dpb_plan_create_ex(ctypes.byref(h), 64, 2, lb, br, ac, low, 0) == -1
+
+
+def test_status_strings(lib):
+    for s in (0, -1, -2, -3, -4):
+        assert lib.dpb_status_string(s).startswith(b"DPB_")

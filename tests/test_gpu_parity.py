@@ -1,0 +1,300 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Every input is seeded (paper_2607_20652_amd.inputs); decode and backward are
+fed the oracle's own codes so that near-tie exemptions of the encoder never
+leak into their checks.  Full-size workloads run on the GPU in the launch
+configuration the benchmark times; the oracle checks a sample of rows.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_20652_amd import binding as dpb
+from paper_2607_20652_amd import inputs
+from parity_util import TOL_BF16, TOL_F32, compare_dense, compare_encode
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    dpb.load()
+
+
+_PLANS = {}
+_FULL = {}
+
+
+def full_activations(name):
+    if name not in _FULL:
+        _FULL[name] = inputs.activations(name)
+    return _FULL[name]
+
+
+def plan_for(name, seed=0):
+    key = (name, seed)
+    if key not in _PLANS:
+        w = inputs.workload(name)
+        _PLANS[key] = dpb.Plan(w.d, w.n, w.levels, w.branching, w.beam, w.k, seed)
+    return _PLANS[key]
+
+
+def oracle_setup(name, seed=0):
+    w = inputs.workload(name)
+    nb, dl, K = oracle.hierarchy(w.d, w.n, w.levels, w.branching, w.beam, w.k)
+    return w, nb, dl, K, oracle.masks(w.d, w.n), oracle.generators(nb, dl, seed)
+
+
+def sample_rows(T, n, seed=0):
+    if T <= n:
+        return np.arange(T)
+    rng = np.random.default_rng(seed)
+    mid = rng.choice(np.arange(64, T - 64), size=n - 128, replace=False)
+    return np.unique(np.concatenate([np.arange(64), mid, np.arange(T - 64, T)]))
+
+
+# ---------------------------------------------------------------- encode
+
+@pytest.mark.parametrize("name,T", [("tiny", 256), ("tiny", 37), ("gpt2", 1000), ("wide", 333),
+                                    ("very_wide", 150)])
+def test_encode_matches_oracle(name, T):
+    say(f"[encode] {name} T={T}")
+    plan = plan_for(name)
+    w, nb, dl, K, m, gens = oracle_setup(name)
+    x = inputs.activations(name, T)
+    idx, coef = dpb.encode(plan, x.to(DEV))
+    torch.cuda.synchronize()
+    oi, oc, om, oo = oracle.encode(w.d, m, nb, K, dl, gens, x.double().numpy())
+    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32)
+    say(f"  {st}")
+    assert st["exempt_tokens"] <= max(2, 0.02 * T)
+
+
+@pytest.mark.parametrize("name,rows", [("gpt2", 384), ("wide", 256), ("very_wide", 160)])
+def test_encode_full_size_sampled(name, rows):
+    w = inputs.workload(name)
+    say(f"[encode full] {name} T={w.tokens}")
+    plan = plan_for(name)
+    _, nb, dl, K, m, gens = oracle_setup(name)
+    x = full_activations(name)
+    idx, coef = dpb.encode(plan, x.to(DEV))
+    torch.cuda.synchronize()
+    r = sample_rows(w.tokens, rows, seed=w.index)
+    oi, oc, om, oo = oracle.encode(w.d, m, nb, K, dl, gens, x[r].double().numpy())
+    st = compare_encode(K, idx.cpu().numpy()[r], coef.cpu().numpy()[r], oi, oc, om, oo, TOL_F32)
+    say(f"  {st}")
+    assert st["exempt_tokens"] <= max(2, 0.02 * len(r))
+    # every emitted index is unique within its token and lies in its level
+    ih = idx.cpu().numpy()
+    s = np.sort(ih, axis=1)
+    assert not np.any((s[:, 1:] == s[:, :-1]) & (s[:, 1:] >= 0))
+    slot = 0
+    for l, k in enumerate(K):
+        lo = 0 if l == 0 else 1 << nb[l - 1]
+        hi = w.d if l == 0 else 1 << nb[l]
+        blk = ih[:, slot:slot + k]
+        assert ((blk >= lo) & (blk < hi)).all()
+        slot += k
+
+
+def test_encode_exhaustive_generators_tiny():
+    """Full generator sets: every parent reaches its whole next level, so the
+    search prunes nothing and repeats each child once per parent (heavy dedup)."""
+    say("[encode exhaustive] d=64 n=(6,8,10)")
+    d, nb, K = 64, [6, 8, 10], [4, 4, 8]
+    full = [np.arange(1 << nb[l - 1], 1 << nb[l], dtype=np.uint32) for l in (1, 2)]
+    dl = [0, len(full[0]), len(full[1])]
+    plan = dpb.Plan(d, level_bits=nb, branchings=dl, active=K, generators=np.concatenate(full).tolist())
+    x = inputs.activations("tiny", 200)
+    idx, coef = dpb.encode(plan, x.to(DEV))
+    torch.cuda.synchronize()
+    m = oracle.masks(d, nb[-1])
+    oi, oc, om, oo = oracle.encode(d, m, nb, K, dl, [np.zeros(0, np.uint32)] + full, x.double().numpy())
+    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32)
+    say(f"  {st}")
+
+
+def test_encode_dyadic_ties_tiny():
+    """Integer activations: hashed scores are multiples of 1/8 and tie often;
+    fp32 sums are exact, so selection must match exactly with index tie-breaks."""
+    say("[encode dyadic] tiny")
+    plan = plan_for("tiny")
+    w, nb, dl, K, m, gens = oracle_setup("tiny")
+    x = inputs.dyadic(w.d, 256)
+    idx, coef = dpb.encode(plan, x.to(DEV))
+    torch.cuda.synchronize()
+    oi, oc, _, _ = oracle.encode(w.d, m, nb, K, dl, gens, x.double().numpy())
+    assert np.array_equal(idx.cpu().numpy(), oi)
+    assert np.array_equal(coef.cpu().numpy().astype(np.float64), oc)
+
+
+def test_encode_deterministic_and_empty():
+    say("[encode determinism] gpt2")
+    plan = plan_for("gpt2")
+    x = inputs.activations("gpt2", 2048).to(DEV)
+    a = dpb.encode(plan, x)
+    b = dpb.encode(plan, x)
+    torch.cuda.synchronize()
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+    e = dpb.encode(plan, x[:0])
+    assert e[0].shape == (0, plan.k_tot)
+
+
+# ---------------------------------------------------------------- decode
+
+def _oracle_codes(name, T):
+    w, nb, dl, K, m, gens = oracle_setup(name)
+    x = inputs.activations(name, T)
+    oi, oc, _, _ = oracle.encode(w.d, m, nb, K, dl, gens, x.double().numpy())
+    return w, m, oi, oc.astype(np.float32)
+
+
+@pytest.mark.parametrize("name,T", [("tiny", 256), ("gpt2", 777), ("wide", 300), ("very_wide", 130)])
+@pytest.mark.parametrize("out", ["f32", "bf16"])
+def test_decode_matches_oracle(name, T, out):
+    say(f"[decode] {name} T={T} out={out}")
+    plan = plan_for(name)
+    w, m, oi, oc = _oracle_codes(name, T)
+    dt = torch.float32 if out == "f32" else torch.bfloat16
+    y = dpb.decode(plan, torch.from_numpy(oi).to(DEV), torch.from_numpy(oc).to(DEV), dt)
+    torch.cuda.synchronize()
+    ref = oracle.decode(w.d, m, oi, oc.astype(np.float64))
+    err = compare_dense(y.float().cpu().numpy(), ref, TOL_F32 if out == "f32" else TOL_BF16)
+    say(f"  max rel err {err:.3g}")
+
+
+@pytest.mark.parametrize("name", ["tiny", "wide", "very_wide"])
+def test_decode_arbitrary_codes(name):
+    """Any valid code, not only encoder output: indices anywhere in the
+    dictionary, repeated indices, basis slots and padding."""
+    say(f"[decode arbitrary] {name}")
+    plan = plan_for(name)
+    w = inputs.workload(name)
+    m = oracle.masks(w.d, w.n)
+    T, k = 97, plan.k_tot
+    rng = np.random.default_rng(11)
+    idx = rng.integers(0, 1 << w.n, size=(T, k)).astype(np.int32)
+    idx[:, :3] = rng.integers(0, w.d, size=(T, 3))
+    idx[:, 5] = idx[:, 6]
+    idx[::3, -2:] = -1
+    coef = rng.standard_normal((T, k)).astype(np.float32)
+    y = dpb.decode(plan, torch.from_numpy(idx).to(DEV), torch.from_numpy(coef).to(DEV))
+    torch.cuda.synchronize()
+    ref = oracle.decode(w.d, m, idx, coef.astype(np.float64))
+    compare_dense(y.cpu().numpy(), ref, TOL_F32)
+
+
+def test_decode_dyadic_bit_exact_and_one_hot():
+    say("[decode exact] tiny")
+    plan = plan_for("tiny")
+    w = inputs.workload("tiny")
+    m = oracle.masks(w.d, w.n)
+    rng = np.random.default_rng(3)
+    T, k = 64, plan.k_tot
+    idx = rng.integers(0, 1 << w.n, size=(T, k)).astype(np.int32)
+    coef = rng.integers(-8, 9, size=(T, k)).astype(np.float32)
+    y = dpb.decode(plan, torch.from_numpy(idx).to(DEV), torch.from_numpy(coef).to(DEV))
+    torch.cuda.synchronize()
+    ref = oracle.decode(w.d, m, idx, coef.astype(np.float64))
+    assert np.array_equal(y.cpu().numpy().astype(np.float64), ref)
+    # one-hot codes of hashed features return exactly +-fp32(1/sqrt d)
+    for name in ("tiny", "wide"):
+        p = plan_for(name)
+        ww = inputs.workload(name)
+        oh = np.full((4, p.k_tot), -1, np.int32)
+        oh[:, 0] = [ww.d, ww.d + 1, (1 << ww.n) - 1, 12345 % (1 << ww.n) + ww.d]
+        c = np.zeros((4, p.k_tot), np.float32)
+        c[:, 0] = 1
+        yy = dpb.decode(p, torch.from_numpy(oh).to(DEV), torch.from_numpy(c).to(DEV)).cpu().numpy()
+        v = np.float32(1.0 / math.sqrt(ww.d))
+        assert set(np.unique(yy).tolist()) == {float(v), float(-v)}
+
+
+@pytest.mark.parametrize("name", ["gpt2", "wide", "very_wide"])
+def test_decode_full_size_sampled(name):
+    w = inputs.workload(name)
+    say(f"[decode full] {name} T={w.tokens}")
+    plan = plan_for(name)
+    x = full_activations(name).to(DEV)
+    idx, coef = dpb.encode(plan, x)
+    y = dpb.decode(plan, idx, coef, torch.bfloat16)
+    torch.cuda.synchronize()
+    r = sample_rows(w.tokens, 256, seed=w.index + 1)
+    m = oracle.masks(w.d, w.n)
+    ih, ch = idx.cpu().numpy()[r], coef.cpu().numpy()[r].astype(np.float64)
+    compare_dense(y.float().cpu().numpy()[r], oracle.decode(w.d, m, ih, ch), TOL_BF16)
+
+
+# ---------------------------------------------------------------- backward
+
+@pytest.mark.parametrize("name,T", [("tiny", 256), ("gpt2", 500), ("train", 300), ("very_wide", 120)])
+def test_decode_bwd_matches_oracle(name, T):
+    say(f"[bwd] {name} T={T}")
+    plan = plan_for(name)
+    w, m, oi, _ = _oracle_codes(name, T)
+    g = inputs.upstream_grad(name, T)
+    gc, gx = dpb.decode_bwd(plan, torch.from_numpy(oi).to(DEV), g.to(DEV))
+    torch.cuda.synchronize()
+    rgc, rgx = oracle.decode_bwd(w.d, m, oi, g.double().numpy())
+    tol = TOL_F32 if w.dtype == "f32" else TOL_BF16
+    e1 = compare_dense(gc.cpu().numpy(), rgc, TOL_F32)
+    e2 = compare_dense(gx.float().cpu().numpy(), rgx, tol)
+    say(f"  grad_coef err {e1:.3g}  grad_x err {e2:.3g}")
+
+
+def test_decode_bwd_full_size_sampled_train():
+    w = inputs.workload("train")
+    say(f"[bwd full] train T={w.tokens}")
+    plan = plan_for("train")
+    x = full_activations("train").to(DEV)
+    g = inputs.upstream_grad("train").to(DEV)
+    idx, coef = dpb.encode(plan, x)
+    gc, gx = dpb.decode_bwd(plan, idx, g)
+    torch.cuda.synchronize()
+    r = sample_rows(w.tokens, 256, seed=9)
+    m = oracle.masks(w.d, w.n)
+    rgc, rgx = oracle.decode_bwd(w.d, m, idx.cpu().numpy()[r], g.cpu()[r].double().numpy())
+    compare_dense(gc.cpu().numpy()[r], rgc, TOL_F32)
+    compare_dense(gx.float().cpu().numpy()[r], rgx, TOL_BF16)
+
+
+def test_decode_bwd_adjoint_identity():
+    """<decode(idx, a), g> == <a, grad_coef(idx, g)> (fp32 sums, fp64 compare)."""
+    say("[bwd adjoint] wide")
+    plan = plan_for("wide")
+    w = inputs.workload("wide")
+    rng = np.random.default_rng(5)
+    T = 64
+    idx = torch.from_numpy(rng.integers(0, 1 << w.n, size=(T, plan.k_tot)).astype(np.int32)).to(DEV)
+    a = torch.from_numpy(rng.standard_normal((T, plan.k_tot)).astype(np.float32)).to(DEV)
+    g = torch.from_numpy(rng.standard_normal((T, w.d)).astype(np.float32)).to(DEV)
+    y = dpb.decode(plan, idx, a)
+    gc, gx = dpb.decode_bwd(plan, idx, g, torch.float32)
+    lhs = (y.double() * g.double()).sum(1)
+    rhs = (a.double() * gc.double()).sum(1)
+    assert torch.allclose(lhs, rhs, rtol=1e-4, atol=1e-4)
+    assert torch.allclose(gx, dpb.decode(plan, idx, gc), rtol=0, atol=0)
+
+
+def test_boundary_errors_on_gpu():
+    say("[errors] gpu")
+    plan = plan_for("tiny")
+    x = torch.zeros((8, 64), device=DEV)
+    with pytest.raises(TypeError):
+        dpb.encode(plan, x.half())
+    xb = torch.zeros(8 * 64 + 1, device=DEV)[1:].view(8, 64)   # 4-byte offset: misaligned
+    with pytest.raises(dpb.DPBError):
+        dpb.encode(plan, xb)
