@@ -1,0 +1,229 @@
+"""DPB benchmark on one MI355X: encode + decode + decode-backward per step.
+
+    python bench.py [--steps K] [--warmup W] [--workload train]
+
+A step is one pass of the whole path over one batch: encode x -> (idx, coef),
+decode -> y, and decode-backward of an upstream gradient g -> (grad_coef,
+grad_x).  Inputs are seeded synthetic activations resident in HBM before the
+timed region; three input sets rotate so that their total (>600 MB at the
+default workload) exceeds the 256 MB Infinity Cache.
+
+Prints ONE JSON line.  `roofline` describes the kernel with the largest average
+launch time, timed with HIP events on the stream the kernels run on;
+`cpu_baseline` times the CPU oracle on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2607_20652_amd import binding as dpb  # noqa: E402
+from paper_2607_20652_amd import inputs  # noqa: E402
+
+METRIC = "DPB fwd+bwd tokens/sec at d=768,N=2^20,k=64; % of HBM/VALU roofline"
+HBM_PEAK_GBS = 8000.0
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2607_20652_amd", "csrc", f) for f in ("kernels.hip", "dpb_internal.hpp")]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+
+
+def kernel_source_digest() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        h.update(open(p, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes_per_token(w, k_tot: int) -> dict:
+    """HBM bytes each kernel must move per token (inputs read once, outputs written once)."""
+    xb = 2 if w.dtype == "bf16" else 4
+    return {
+        "encode": w.d * xb + k_tot * 8,                    # read x, write (idx, coef)
+        "decode": k_tot * 8 + w.d * xb,                    # read (idx, coef), write y
+        "decode_bwd": k_tot * 4 + w.d * xb + k_tot * 4 + w.d * xb,  # read idx, g; write grad_coef, grad_x
+    }
+
+
+def load_traffic(kernel: str, tokens: int):
+    """Measured HBM bytes per launch from the committed rocprofv3 counter runs,
+    if they were taken on the current kernel sources; else None."""
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_digest") != kernel_source_digest():
+        return None
+    k = rec.get("kernels", {}).get(kernel)
+    if not k or k.get("tokens") != tokens:
+        return None
+    return k.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(name: str, target_s: float = 12.0) -> dict:
+    """The oracle (fp64 C, OpenMP over tokens) on a bounded sample of the workload."""
+    import oracle
+
+    w = inputs.workload(name)
+    nb, dl, K = oracle.hierarchy(w.d, w.n, w.levels, w.branching, w.beam, w.k)
+    m = oracle.masks(w.d, w.n)
+    gens = oracle.generators(nb, dl, 0)
+
+    def run(T):
+        x = inputs.activations(name, T).double().numpy()
+        g = inputs.upstream_grad(name, T).double().numpy()
+        t = time.perf_counter()
+        idx, coef, _, _ = oracle.encode(w.d, m, nb, K, dl, gens, x)
+        oracle.decode(w.d, m, idx, coef)
+        oracle.decode_bwd(w.d, m, idx, g)
+        return time.perf_counter() - t
+
+    probe = 256
+    t_probe = run(probe)
+    T = int(min(w.tokens, max(probe, probe * target_s / max(t_probe, 1e-3))))
+    t = run(T)
+    return {
+        "value": T / t,
+        "unit": "tokens/s",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": f"first {T} of {w.tokens} tokens of '{name}' (encode+decode+decode_bwd), {t:.1f} s",
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="train")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--only", choices=["encode", "decode", "decode_bwd"], default=None,
+                    help="time a single kernel (for counter runs)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs on one GPU only; the DPB shards by tokens with no "
+              "communication, so a multi-GPU figure is N times the one-GPU value (not measured).",
+              file=sys.stderr)
+        return 2
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU", file=sys.stderr)
+        return 2
+    if not os.path.exists(dpb.lib_path):
+        from paper_2607_20652_amd import build
+        build.build()
+
+    w = inputs.workload(args.workload)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    plan = dpb.Plan(w.d, w.n, w.levels, w.branching, w.beam, w.k, 0)
+    T, k = w.tokens, plan.k_tot
+    act = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+
+    # three rotating input sets, resident in HBM before timing
+    x0, g0 = inputs.activations(args.workload), inputs.upstream_grad(args.workload)
+    sets = []
+    for r in range(3):
+        sets.append((torch.roll(x0, shifts=r * 7919, dims=0).to(dev).contiguous(),
+                     torch.roll(g0, shifts=r * 7919, dims=0).to(dev).contiguous()))
+    idx = torch.empty((T, k), dtype=torch.int32, device=dev)
+    coef = torch.empty((T, k), dtype=torch.float32, device=dev)
+    y = torch.empty((T, w.d), dtype=act, device=dev)
+    gc = torch.empty((T, k), dtype=torch.float32, device=dev)
+    gx = torch.empty((T, w.d), dtype=act, device=dev)
+
+    names = ["encode", "decode", "decode_bwd"]
+    run = {n: (args.only is None or args.only == n) for n in names}
+
+    def step(i, ev=None):
+        x, g = sets[i % 3]
+        if ev is not None:
+            ev[0].record()
+        if run["encode"]:
+            dpb.encode(plan, x, idx, coef)
+        if ev is not None:
+            ev[1].record()
+        if run["decode"]:
+            dpb.decode(plan, idx, coef, act, y)
+        if ev is not None:
+            ev[2].record()
+        if run["decode_bwd"]:
+            dpb.decode_bwd(plan, idx, g, act, gc, gx)
+        if ev is not None:
+            ev[3].record()
+
+    if args.only in ("decode", "decode_bwd"):
+        dpb.encode(plan, sets[0][0], idx, coef)  # codes for the kernels under test
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(args.steps):
+        step(i, evs[i])
+    end.record()
+    torch.cuda.synchronize()
+    ms_total = start.elapsed_time(end)
+    ms_step = ms_total / args.steps
+    per_kernel_ms = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(args.steps)]))
+                     for j, n in enumerate(names)}
+
+    bpt = algorithmic_bytes_per_token(w, k)
+    timed = [n for n in names if run[n]]
+    dom = max(timed, key=lambda n: per_kernel_ms[n])
+    achieved = bpt[dom] * T / (per_kernel_ms[dom] * 1e-3) / 1e9
+    traffic = load_traffic(dom, T)
+    roofline = {
+        "kernel": dom,
+        "bound": "hbm",
+        "achieved": round(achieved, 2),
+        "peak": HBM_PEAK_GBS,
+        "unit": "GB/s",
+        "frac": round(achieved / HBM_PEAK_GBS, 4),
+        "traffic": traffic,
+        "algorithmic_bytes_per_launch": bpt[dom] * T,
+        "avg_launch_ms": round(per_kernel_ms[dom], 4),
+        "per_kernel_ms": {n: round(v, 4) for n, v in per_kernel_ms.items() if run[n]},
+    }
+
+    out = {
+        "metric": METRIC,
+        "value": T / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{w.name}: DPB d={w.d}, N=2^{w.n} ({w.levels} levels x {w.branching}-way), "
+                        f"beam {w.beam}, k={w.k}, {T} tokens {w.dtype}; encode+decode+decode_bwd per step",
+            "tokens_per_step": T, "d": w.d, "n_bits": w.n, "levels": w.levels, "branching": w.branching,
+            "beam": w.beam, "k": w.k, "k_tot": k, "only": args.only,
+        },
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline and args.only is None:
+        out["cpu_baseline"] = cpu_baseline(args.workload)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -59,6 +59,7 @@ def _load():
         "oracle_decode": (None, [i32, P, i32, P, P, i64, P]),
         "oracle_decode_bwd": (None, [i32, P, i32, P, P, i64, P, P]),
         "oracle_walsh_spectrum": (i32, [i32, P, i32, P]),
+        "oracle_num_threads": (i32, []),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -215,6 +216,11 @@ def decode_bwd(d: int, m: np.ndarray, idx: np.ndarray, g: np.ndarray):
     gx = np.zeros((T, d), dtype=np.float64)
     _load().oracle_decode_bwd(d, _ptr(m), k, _ptr(idx), _ptr(g), T, _ptr(gc), _ptr(gx))
     return gc, gx
+
+
+def num_threads() -> int:
+    """OpenMP threads the oracle's token loops run on."""
+    return int(_load().oracle_num_threads())
 
 
 def walsh_spectrum(d: int, m: np.ndarray, r: int) -> np.ndarray:

@@ -492,3 +492,10 @@ int oracle_walsh_spectrum(int d, const uint32_t* masks, int r, int64_t* S)
     }
     return 0;
 }
+
+/* Threads the OpenMP loops above use (reported next to timings). */
+#include <omp.h>
+int oracle_num_threads(void)
+{
+    return omp_get_max_threads();
+}
