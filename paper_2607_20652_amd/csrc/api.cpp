@@ -64,7 +64,92 @@ dpb_status fill_plan(dpb_plan* plan, const Hierarchy& h, const uint32_t* gens, u
         P.gamma_off[l] = gamma_off;
         gamma_off += (int64_t)P.mblocks[l] * P.nchunk * 64;
     }
+
+    // code kernels: parent columns per token, padded branching, nibble groups
+    const int L = h.levels;
+    int maxcpt = 1;
+    int64_t gt_off = 0;
+    for (int l = 0; l < dpb::kMaxLevels; ++l) {
+        const bool live = l >= 1 && l < L;
+        P.cpt[l] = live ? pow2_at_least(h.active[l - 1]) : 0;
+        P.dpad[l] = live ? (h.branching[l] + 15) / 16 * 16 : 0;
+        if (P.cpt[l] > maxcpt) maxcpt = P.cpt[l];
+        P.gamma_t_off[l] = gt_off;
+        if (live) gt_off += (int64_t)(P.dp / 16) * (P.dpad[l] / 16) * 64;
+    }
+    P.wave_tokens = maxcpt >= 16 ? 1 : 16 / maxcpt;
+    P.leaf_columns = (L >= 2 && P.cpt[L - 1] >= 4 && P.cpt[L - 1] <= 16 && h.active[L - 1] >= 2 * h.active[L - 2] &&
+                      P.dpad[L - 1] <= 64)
+                         ? 1
+                         : 0;
+    P.nt_groups = (h.level_bits[L - 1] + 3) / 4;
     return DPB_OK;
+}
+
+inline uint32_t row_parity(uint32_t m, uint32_t p) { return (uint32_t)__builtin_popcount(m & p) & 1u; }
+
+inline uint16_t pm_one(uint32_t neg) { return neg ? 0xBF80 : 0x3F80; }  // bf16 -1 / +1
+
+// Sign-bitmap words of index (v << 4g): bit b of word w is the sign at coordinate 32w + b.
+void build_nibble_tables(const dpb_plan* plan, std::vector<uint32_t>* out)
+{
+    const DevPlan& P = plan->dev;
+    out->assign((size_t)P.nt_groups * 16 * P.nchunk, 0);
+    for (int g = 0; g < P.nt_groups; ++g)
+        for (uint32_t v = 0; v < 16; ++v)
+            for (int w = 0; w < P.nchunk; ++w) {
+                uint32_t word = 0;
+                for (int b = 0; b < 32; ++b) {
+                    const int iota = 32 * w + b;
+                    if (iota < P.d) word |= row_parity(plan->masks_h[iota], v << (4 * g)) << b;
+                }
+                (*out)[((size_t)g * 16 + v) * P.nchunk + w] = word;
+            }
+}
+
+// Scoring A fragments in the paired coordinate order (see DevPlan::gamma_pair).
+void build_gamma_pair(const dpb_plan* plan, std::vector<uint16_t>* out)
+{
+    const DevPlan& P = plan->dev;
+    int64_t total = 0;
+    for (int l = 1; l < P.levels; ++l) total += (int64_t)P.mblocks[l] * P.nchunk * 64 * 8;
+    out->assign((size_t)total, 0);
+    for (int l = 1; l < P.levels; ++l) {
+        const uint32_t* g = plan->gens_h.data() + P.gens_off[l];
+        for (int mb = 0; mb < P.mblocks[l]; ++mb)
+            for (int c = 0; c < P.nchunk; ++c)
+                for (int lane = 0; lane < 64; ++lane) {
+                    const int j = 16 * mb + (lane & 15), kq = lane >> 4;
+                    uint16_t* dst = out->data() + (P.gamma_off[l] + ((int64_t)mb * P.nchunk + c) * 64 + lane) * 8;
+                    for (int e = 0; e < 8; ++e) {
+                        const int iota = 32 * c + kq + 4 * (e >> 1) + 16 * (e & 1);
+                        dst[e] = (j < P.delta[l] && iota < P.d) ? pm_one(row_parity(plan->masks_h[iota], g[j])) : 0;
+                    }
+                }
+    }
+}
+
+// Column-decode B fragments (see DevPlan::gamma_t).
+void build_gamma_t(const dpb_plan* plan, std::vector<uint16_t>* out)
+{
+    const DevPlan& P = plan->dev;
+    int64_t total = 0;
+    for (int l = 1; l < P.levels; ++l) total += (int64_t)(P.dp / 16) * (P.dpad[l] / 16) * 64 * 4;
+    out->assign((size_t)total, 0);
+    for (int l = 1; l < P.levels; ++l) {
+        const uint32_t* g = plan->gens_h.data() + P.gens_off[l];
+        const int nkb = P.dpad[l] / 16;
+        for (int cb = 0; cb < P.dp / 16; ++cb)
+            for (int kb = 0; kb < nkb; ++kb)
+                for (int lane = 0; lane < 64; ++lane) {
+                    uint16_t* dst = out->data() + (P.gamma_t_off[l] + ((int64_t)cb * nkb + kb) * 64 + lane) * 4;
+                    const int iota = 16 * cb + (lane & 15);
+                    for (int i = 0; i < 4; ++i) {
+                        const int j = 16 * kb + 4 * (lane >> 4) + i;
+                        dst[i] = (j < P.delta[l] && iota < P.d) ? pm_one(row_parity(plan->masks_h[iota], g[j])) : 0;
+                    }
+                }
+    }
 }
 
 // Child sign patterns gamma_j = R(M g_j) (§2.2 child-scoring equation) laid
@@ -97,38 +182,58 @@ void build_gamma_fragments(const dpb_plan* plan, std::vector<uint16_t>* out)
 dpb_status upload(dpb_plan* plan)
 {
     DevPlan& P = plan->dev;
-    std::vector<uint16_t> gamma;
+    std::vector<uint16_t> gamma, gamma_pair, gamma_t;
+    std::vector<uint32_t> nt;
     build_gamma_fragments(plan, &gamma);
+    build_gamma_pair(plan, &gamma_pair);
+    build_gamma_t(plan, &gamma_t);
+    build_nibble_tables(plan, &nt);
     std::vector<uint32_t> masks_p(P.dp, 0);
     std::copy(plan->masks_h.begin(), plan->masks_h.end(), masks_p.begin());
 
-    auto align = [](size_t v) { return (v + 255) & ~(size_t)255; };
-    const size_t masks_bytes = align(masks_p.size() * 4);
-    const size_t gens_bytes = align(std::max<size_t>(plan->gens_h.size(), 1) * 4);
-    const size_t gamma_bytes = align(std::max<size_t>(gamma.size(), 8) * 2);
+    // one device allocation, 256-byte aligned sub-buffers
+    struct Part {
+        const void* src;
+        size_t bytes;
+        size_t off;
+    };
+    Part parts[] = {
+        {masks_p.data(), masks_p.size() * 4, 0},
+        {plan->gens_h.data(), plan->gens_h.size() * 4, 0},
+        {gamma.data(), gamma.size() * 2, 0},
+        {gamma_pair.data(), gamma_pair.size() * 2, 0},
+        {gamma_t.data(), gamma_t.size() * 2, 0},
+        {nt.data(), nt.size() * 4, 0},
+    };
+    size_t total = 0;
+    for (Part& p : parts) {
+        p.off = total;
+        total += (std::max<size_t>(p.bytes, 16) + 255) & ~(size_t)255;
+    }
     if (hipGetDevice(&plan->device) != hipSuccess) {
         (void)hipGetLastError();
         return DPB_EHIP;
     }
     void* mem = nullptr;
-    if (hipMalloc(&mem, masks_bytes + gens_bytes + gamma_bytes) != hipSuccess) {
+    if (hipMalloc(&mem, total) != hipSuccess) {
         (void)hipGetLastError();
         return DPB_ENOMEM;
     }
     plan->dev_alloc = mem;
     char* base = (char*)mem;
-    P.masks = (const uint32_t*)base;
-    P.gens = (const uint32_t*)(base + masks_bytes);
-    P.gamma = (const uint4*)(base + masks_bytes + gens_bytes);
-    hipError_t e = hipMemcpy(base, masks_p.data(), masks_p.size() * 4, hipMemcpyHostToDevice);
-    if (e == hipSuccess && !plan->gens_h.empty())
-        e = hipMemcpy(base + masks_bytes, plan->gens_h.data(), plan->gens_h.size() * 4, hipMemcpyHostToDevice);
-    if (e == hipSuccess && !gamma.empty())
-        e = hipMemcpy(base + masks_bytes + gens_bytes, gamma.data(), gamma.size() * 2, hipMemcpyHostToDevice);
+    hipError_t e = hipMemset(base, 0, total);
+    for (const Part& p : parts)
+        if (e == hipSuccess && p.bytes) e = hipMemcpy(base + p.off, p.src, p.bytes, hipMemcpyHostToDevice);
     if (e != hipSuccess) {
         (void)hipGetLastError();
         return DPB_EHIP;
     }
+    P.masks = (const uint32_t*)(base + parts[0].off);
+    P.gens = (const uint32_t*)(base + parts[1].off);
+    P.gamma = base + parts[2].off;
+    P.gamma_pair = base + parts[3].off;
+    P.gamma_t = base + parts[4].off;
+    P.nt = (const uint32_t*)(base + parts[5].off);
     return DPB_OK;
 }
 
@@ -141,7 +246,7 @@ dpb_status create(dpb_plan** out, const Hierarchy& h, const uint32_t* gens, uint
     dpb_plan* plan = new (std::nothrow) dpb_plan();
     if (!plan) return DPB_ENOMEM;
     dpb_status s = fill_plan(plan, h, gens, seed);
-    if (s == DPB_OK && !dpb::plan_fits(plan->dev)) s = DPB_EUNSUPPORTED;
+    if (s == DPB_OK && (!dpb::plan_fits(plan->dev) || !dpb::code_kernels_fit(plan->dev))) s = DPB_EUNSUPPORTED;
     if (s == DPB_OK) s = upload(plan);
     if (s != DPB_OK) {
         dpb_plan_destroy(plan);
@@ -308,6 +413,8 @@ dpb_status dpb_encode(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, in
     if (!dtype_ok(x_dtype)) return DPB_EINVAL;
     if (T == 0) return DPB_OK;
     if (!x || !idx || !coef || !aligned16(x) || !aligned16(idx) || !aligned16(coef)) return DPB_EINVAL;
+    if (dpb::encode2_supported(plan->dev))
+        return launched(dpb::launch_encode2(plan->dev, x, x_dtype == DPB_BF16, T, idx, coef, (hipStream_t)stream));
     return launched(dpb::launch_encode(plan->dev, x, x_dtype == DPB_BF16, T, idx, coef, (hipStream_t)stream));
 }
 
@@ -319,7 +426,7 @@ dpb_status dpb_decode(const dpb_plan* plan, const int32_t* idx, const float* coe
     if (!dtype_ok(y_dtype)) return DPB_EINVAL;
     if (T == 0) return DPB_OK;
     if (!idx || !coef || !y || !aligned16(idx) || !aligned16(coef) || !aligned16(y)) return DPB_EINVAL;
-    return launched(dpb::launch_decode(plan->dev, idx, coef, T, y, y_dtype == DPB_BF16, (hipStream_t)stream));
+    return launched(dpb::launch_decode2(plan->dev, idx, coef, T, y, y_dtype == DPB_BF16, (hipStream_t)stream));
 }
 
 dpb_status dpb_decode_bwd(const dpb_plan* plan, const int32_t* idx, const void* grad_y, dpb_dtype g_dtype,
@@ -332,7 +439,7 @@ dpb_status dpb_decode_bwd(const dpb_plan* plan, const int32_t* idx, const void* 
     if (!idx || !grad_y || !grad_coef || !grad_x || !aligned16(idx) || !aligned16(grad_y) ||
         !aligned16(grad_coef) || !aligned16(grad_x))
         return DPB_EINVAL;
-    return launched(dpb::launch_decode_bwd(plan->dev, idx, grad_y, g_dtype == DPB_BF16, T, grad_coef, grad_x,
+    return launched(dpb::launch_decode_bwd2(plan->dev, idx, grad_y, g_dtype == DPB_BF16, T, grad_coef, grad_x,
                                            gx_dtype == DPB_BF16, (hipStream_t)stream));
 }
 

@@ -13,7 +13,7 @@ namespace dpb {
 constexpr int kMaxLevels = 8;
 constexpr int kBlock = 256;               // threads per workgroup (4 wave64)
 constexpr int kChunk = 32;                // coordinates per MFMA K step
-constexpr int kLdsBudget = 64 * 1024;     // bytes of LDS a workgroup may use
+constexpr int kLdsBudget = 160 * 1024;    // bytes of LDS a workgroup may use (gfx950: 160 KB per CU)
 
 // Everything a kernel needs to know about a plan, passed by value.
 struct DevPlan {
@@ -35,7 +35,76 @@ struct DevPlan {
     const uint32_t* masks;      // [dp] row masks, zero past d
     const uint32_t* gens;       // generators, level by level
     const void* gamma;          // per level: [mblocks][nchunk][64 lanes] x 8 bf16 (+1/-1/0)
+
+    // Code kernels (decode, decode-backward) and the scoring primitive.
+    int wave_tokens;            // tokens a wave processes together (16 / cpt of the last level)
+    int leaf_columns;           // 1: the last level decodes through parent columns on the matrix cores
+    int cpt[kMaxLevels];        // parent columns per token at level l: K_{l-1} rounded up to a power of two
+    int dpad[kMaxLevels];       // Delta_l rounded up to a multiple of 16
+    int nt_groups;              // 4-bit index groups of the widest index
+    const uint32_t* nt;         // [nt_groups][16][nchunk] sign-bitmap words of (v << 4g)
+    // Scoring A fragments with the paired coordinate order: lane L, element
+    // e = 2i + h of chunk c holds generator row 16*mb + L%16 at coordinate
+    // 32c + L/16 + 4i + 16h.  Per level: [mblocks][nchunk][64] x 8 bf16.
+    const void* gamma_pair;
+    // Column-decode B fragments: lane L of block (cb, kb) holds generator rows
+    // 16kb + 4*(L/16) + i (i < 4) at coordinate 16cb + L%16.  Per level:
+    // [dp/16][dpad/16][64] x 4 bf16.
+    const void* gamma_t;
+    int64_t gamma_t_off[kMaxLevels];  // in 8-byte units
 };
+
+// Per-wave LDS layout of the code kernels (byte offsets inside a wave's region).
+struct CodeLayout {
+    unsigned idx, coef, route, dir, par, alpha, claim, y, pairs, signw, cw, score, bytes;
+};
+
+__host__ __device__ inline unsigned align16u(unsigned v) { return (v + 15u) & ~15u; }
+
+// The scoring buffers live inside the region of the output accumulator `y`,
+// which is written only after scoring is done.  With fp32 activations the
+// region holds the fp32 values instead of bf16 pairs, and the column bitmaps
+// and scores follow it.
+__host__ __device__ inline CodeLayout code_layout(const DevPlan& P, bool with_scoring, bool act_bf16 = true)
+{
+    CodeLayout L;
+    const int TPW = P.wave_tokens, k = P.k_tot;
+    const int dleaf = P.leaf_columns ? P.dpad[P.levels - 1] : 1;  // column coefficients of the last level
+    unsigned off = 0;
+    L.idx = off;   off = align16u(off + TPW * k * 4);
+    L.coef = off;  off = align16u(off + TPW * k * 4);
+    L.route = off; off = align16u(off + TPW * k * 4);
+    L.dir = off;   off = align16u(off + TPW * k * 4);
+    L.par = off;   off = align16u(off + 16 * 4);
+    L.alpha = off; off = align16u(off + 16 * dleaf * 4);
+    L.claim = off; off = align16u(off + 16 * dleaf * 4);
+    L.y = off;
+    const unsigned yend = align16u(off + TPW * P.dp * 4);
+    L.pairs = L.signw = L.cw = L.score = yend;
+    off = yend;
+    if (with_scoring) {
+        unsigned s = act_bf16 ? L.y : yend;
+        if (act_bf16) {
+            L.pairs = s; s = align16u(s + TPW * P.dp * 2);
+            L.signw = s; s = align16u(s + TPW * P.nchunk * 4);
+        } else {
+            L.pairs = L.signw = L.y;  // fp32 activations occupy the y region
+        }
+        L.cw = s;    s = align16u(s + 16 * P.nchunk * 4);
+        L.score = s; s = align16u(s + 16 * 16 * 4);  // one 16 x 16 score tile
+        off = s > yend ? s : yend;
+    }
+    L.bytes = off;
+    return L;
+}
+
+constexpr int kCodeWaves = 4;  // waves per workgroup in the code kernels
+
+// Shared (per-workgroup) LDS of the code kernels: row masks and nibble tables.
+__host__ __device__ inline unsigned code_shared_bytes(const DevPlan& P, bool with_nt)
+{
+    return align16u(P.dp * 4) + (with_nt ? align16u(P.nt_groups * 16 * P.nchunk * 4) : 0u);
+}
 
 // LDS layout of one encoder workgroup (byte offsets), shared by host and device.
 struct EncodeLayout {
@@ -63,8 +132,25 @@ __host__ __device__ inline EncodeLayout encode_layout(const DevPlan& P, int x_by
     return L;
 }
 
+// Lets a kernel launch with more than 64 KB of dynamic LDS.
+template <typename F>
+inline void allow_lds(F* kernel, size_t bytes)
+{
+    if (bytes > 64 * 1024)
+        (void)hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+}
+
 // True when every kernel's workgroup fits the LDS budget for this plan.
 bool plan_fits(const DevPlan& P);
+
+hipError_t launch_decode2(const DevPlan& P, const int32_t* idx, const float* coef, int64_t T, void* y,
+                          bool y_bf16, hipStream_t stream);
+hipError_t launch_decode_bwd2(const DevPlan& P, const int32_t* idx, const void* g, bool g_bf16, int64_t T,
+                              float* grad_coef, void* grad_x, bool gx_bf16, hipStream_t stream);
+bool code_kernels_fit(const DevPlan& P);
+bool encode2_supported(const DevPlan& P);
+hipError_t launch_encode2(const DevPlan& P, const void* x, bool x_bf16, int64_t T, int32_t* idx, float* coef,
+                          hipStream_t stream);
 
 hipError_t launch_encode(const DevPlan& P, const void* x, bool x_bf16, int64_t T, int32_t* idx,
                          float* coef, hipStream_t stream);

@@ -426,6 +426,8 @@ hipError_t launch_encode(const DevPlan& P, const void* x, bool x_bf16, int64_t T
     if (L.bytes > (unsigned)kLdsBudget) return hipErrorInvalidValue;
     const int64_t blocks = (T + tt - 1) / tt;
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+    allow_lds(encode_kernel<true>, L.bytes);
+    allow_lds(encode_kernel<false>, L.bytes);
     if (x_bf16)
         hipLaunchKernelGGL(encode_kernel<true>, dim3((unsigned)blocks), dim3(kBlock), L.bytes, stream, P, x, T, idx,
                            coef, tt);

@@ -1,0 +1,145 @@
+// Child scoring on the matrix cores (§2.2 child-scoring equation), shared by
+// the encoder (activations x) and the decode-backward (upstream gradient g).
+//
+// For level l, a block of 16 columns r = tt*CPT + q (token tt, parent slot q)
+// with parent index p_r, and a tile of 16 generators j:
+//     S[j][r] = sum_iota gamma_j[iota] * (phi~_{p_r} (.) a_tt)[iota],
+// the 16x16x32 bf16 MFMA with Gamma_l as the A operand (exact +-1) and the
+// sign-flipped activations as B.  B is built from the column's sign bitmap
+// (nibble tables: parity is linear in the index bits) and the activations
+// held in LDS in the paired coordinate order, so that each B dword is one
+// rotate plus one and-or: lane kq's dword i holds coordinates
+// 32c + kq + 4i (low half) and 32c + kq + 4i + 16 (high half).
+#pragma once
+
+#include "device_common.hpp"
+
+namespace dpb {
+
+constexpr int kScoreBatch = 8;  // A fragments fetched per batch
+
+// A wave's activations in LDS.
+struct ActTile {
+    const uint32_t* pairs;  // bf16: [TPW][dp/2] |a| as bf16 pairs (paired order)
+    const uint32_t* signw;  // bf16: [TPW][nchunk] sign bits, natural order (bit b = coordinate 32c + b)
+    const float* f;         // fp32: [TPW][dp]
+};
+
+// Sign bitmaps of the 16 columns of block nb at level l into cw[16][nchunk];
+// for bf16 activations the activation signs are folded in.  Column r has
+// parent parents[tt * pstride + q] when q < nparents and tt < ntok.
+template <bool ACT_BF16>
+__device__ void column_bitmaps(const DevPlan& P, int lane, int ntok, int l, int nb, const int32_t* parents,
+                               int pstride, int nparents, const ActTile& A, const uint32_t* nt, uint32_t* cw)
+{
+    const int CPT = P.cpt[l], TPW = P.wave_tokens, nchunk = P.nchunk;
+    const int ncol = TPW * CPT;
+    for (int e = lane; e < 16 * nchunk; e += 64) {
+        const int col = e / nchunk, w = e - col * nchunk;
+        const int r = nb * 16 + col, tt = r / CPT, q = r % CPT;
+        const int32_t p = (r < ncol && tt < ntok && q < nparents) ? parents[tt * pstride + q] : -1;
+        uint32_t word = 0;
+        if (p >= 0) {
+            word = bitmap_word(nt, P.nt_groups, nchunk, (uint32_t)p, w);
+            if constexpr (ACT_BF16) word ^= A.signw[tt * nchunk + w];
+        }
+        cw[e] = word;
+    }
+}
+
+// Unscaled scores of generator tile mb for this lane's column (lane & 15):
+// acc[i] = S[16*mb + 4*(lane>>4) + i][column].  `valid` false gives zeros.
+template <bool ACT_BF16>
+__device__ f32x4 mfma_scores(const DevPlan& P, int lane, int l, int mb, bool valid, int trow, const ActTile& A,
+                             const uint32_t* cw)
+{
+    const int nchunk = P.nchunk, dp = P.dp, col = lane & 15, kq = lane >> 4;
+    const u32x4* Ap = (const u32x4*)P.gamma_pair + P.gamma_off[l] + (int64_t)mb * nchunk * 64 + lane;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int c0 = 0; c0 < nchunk; c0 += kScoreBatch) {
+        u32x4 a[kScoreBatch];
+        uint32_t wd[kScoreBatch];
+#pragma unroll
+        for (int e = 0; e < kScoreBatch; ++e) {
+            const int c = c0 + e < nchunk ? c0 + e : nchunk - 1;
+            a[e] = Ap[(int64_t)c * 64];
+            wd[e] = cw[col * nchunk + c];
+        }
+#pragma unroll
+        for (int e = 0; e < kScoreBatch; ++e) {
+            if (c0 + e >= nchunk) break;
+            const int c = c0 + e;
+            const bf16x8 av = __builtin_bit_cast(bf16x8, a[e]);
+            if constexpr (ACT_BF16) {
+                const uint32_t R = rotl32(wd[e], 15u - (uint32_t)kq);
+                const u32x4 pd = *(const u32x4*)(A.pairs + trow * (dp / 2) + c * 16 + kq * 4);
+                u32x4 b;
+                b.x = (R & 0x80008000u) | pd.x;
+                b.y = (__builtin_amdgcn_alignbit(R, R, 4) & 0x80008000u) | pd.y;
+                b.z = (__builtin_amdgcn_alignbit(R, R, 8) & 0x80008000u) | pd.z;
+                b.w = (__builtin_amdgcn_alignbit(R, R, 12) & 0x80008000u) | pd.w;
+                if (!valid) b = (u32x4){0u, 0u, 0u, 0u};
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
+            } else {
+                uint32_t hi[8], mi[8], lo[8];
+#pragma unroll
+                for (int x = 0; x < 8; ++x) {
+                    const int off = kq + 4 * (x >> 1) + 16 * (x & 1);
+                    float v = A.f[trow * dp + 32 * c + off];
+                    v = __uint_as_float(__float_as_uint(v) ^ (((wd[e] >> off) & 1u) << 31));
+                    if (!valid) v = 0.f;
+                    split3(v, hi[x], mi[x], lo[x]);
+                }
+                const u32x4 bh = {hi[0] | (hi[1] << 16), hi[2] | (hi[3] << 16), hi[4] | (hi[5] << 16),
+                                  hi[6] | (hi[7] << 16)};
+                const u32x4 bm = {mi[0] | (mi[1] << 16), mi[2] | (mi[3] << 16), mi[4] | (mi[5] << 16),
+                                  mi[6] | (mi[7] << 16)};
+                const u32x4 bl = {lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16), lo[4] | (lo[5] << 16),
+                                  lo[6] | (lo[7] << 16)};
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, bh), acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, bm), acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, bl), acc, 0, 0, 0);
+            }
+        }
+    }
+    return acc;
+}
+
+// Writes bf16 activations of `ntok` rows (row stride d elements) into the
+// paired layout and the sign words; rows >= ntok and coordinates >= d are 0.
+__device__ inline void load_pairs(const DevPlan& P, int lane, int ntok, int tpw, const uint16_t* src, int64_t row0,
+                                  uint32_t* pairs, uint32_t* signw)
+{
+    const int d = P.d, dp = P.dp, nchunk = P.nchunk;
+    for (int e = lane; e < tpw * (dp / 2); e += 64) {
+        const int tt = e / (dp / 2), r = e - tt * (dp / 2);
+        const int c = r >> 4, kq = (r >> 2) & 3, i = r & 3;
+        const int i0 = 32 * c + kq + 4 * i, i1 = i0 + 16;
+        const bool live = tt < ntok;
+        const uint32_t v0 = (live && i0 < d) ? src[(row0 + tt) * d + i0] : 0u;
+        const uint32_t v1 = (live && i1 < d) ? src[(row0 + tt) * d + i1] : 0u;
+        pairs[e] = (v0 & 0x7FFFu) | ((v1 & 0x7FFFu) << 16);
+    }
+    for (int base = 0; base < tpw * dp; base += 64) {
+        const int e = base + lane, tt = e / dp, iota = e - tt * dp;
+        const bool neg = tt < ntok && iota < d && (src[(row0 + tt) * d + iota] & 0x8000u);
+        const uint64_t m = __ballot(neg);
+        if (lane == 0) {
+            signw[base / 32] = (uint32_t)m;
+            if (base / 32 + 1 < tpw * nchunk) signw[base / 32 + 1] = (uint32_t)(m >> 32);
+        }
+    }
+}
+
+// Activation at coordinate iota of row tt from the paired layout.
+__device__ __forceinline__ float pair_value(const DevPlan& P, const uint32_t* pairs, const uint32_t* signw, int tt,
+                                            int iota)
+{
+    const int c = iota >> 5, b = iota & 31;
+    const uint32_t dw = pairs[tt * (P.dp / 2) + c * 16 + (b & 3) * 4 + ((b >> 2) & 3)];
+    const uint32_t mag = (b >> 4) ? (dw >> 16) : (dw & 0xFFFFu);
+    const uint32_t sg = (signw[tt * P.nchunk + c] >> b) & 1u;
+    return bf16_bits_to_f32(mag | (sg << 15));
+}
+
+}  // namespace dpb

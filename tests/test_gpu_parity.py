@@ -197,6 +197,40 @@ def test_decode_arbitrary_codes(name):
     compare_dense(y.cpu().numpy(), ref, TOL_F32)
 
 
+def _mixed_codes(name, T, seed=21):
+    """Encoder codes with edits: a repeated last-level slot (two slots compete
+    for one parent column), unroutable indices, a basis index in a hashed
+    level, a hashed index in level 0, and padding."""
+    w, m, oi, oc = _oracle_codes(name, T)
+    nb, _, K = oracle.hierarchy(w.d, w.n, w.levels, w.branching, w.beam, w.k)
+    rng = np.random.default_rng(seed)
+    idx, coef = oi.copy(), oc.copy()
+    last = sum(K[:-1])
+    idx[::2, last + 3] = idx[::2, last + 2]
+    idx[1::3, last + 5] = rng.integers(1 << nb[-2], 1 << nb[-1], size=idx[1::3].shape[0])
+    idx[::4, last + 1] = -1
+    idx[::5, K[0]] = rng.integers(0, w.d, size=idx[::5].shape[0])
+    idx[::7, 1] = rng.integers(w.d, 1 << w.n, size=idx[::7].shape[0])
+    coef[:, last + 4] *= -3.0
+    return w, m, idx, coef
+
+
+@pytest.mark.parametrize("name", ["tiny", "gpt2", "wide", "very_wide"])
+def test_decode_and_bwd_mixed_codes(name):
+    say(f"[decode+bwd mixed] {name}")
+    plan = plan_for(name)
+    w, m, idx, coef = _mixed_codes(name, 90)
+    di = torch.from_numpy(idx).to(DEV)
+    y = dpb.decode(plan, di, torch.from_numpy(coef).to(DEV))
+    g = inputs.upstream_grad(name, 90)
+    gc, gx = dpb.decode_bwd(plan, di, g.to(DEV), torch.float32)
+    torch.cuda.synchronize()
+    compare_dense(y.cpu().numpy(), oracle.decode(w.d, m, idx, coef.astype(np.float64)), TOL_F32)
+    rgc, rgx = oracle.decode_bwd(w.d, m, idx, g.double().numpy())
+    compare_dense(gc.cpu().numpy(), rgc, TOL_F32)
+    compare_dense(gx.cpu().numpy(), rgx, TOL_F32)
+
+
 def test_decode_dyadic_bit_exact_and_one_hot():
     say("[decode exact] tiny")
     plan = plan_for("tiny")
