@@ -1,6 +1,7 @@
 // C ABI of libdpb.so: argument validation, plan lifetime, launches.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <new>
@@ -83,7 +84,41 @@ dpb_status fill_plan(dpb_plan* plan, const Hierarchy& h, const uint32_t* gens, u
                          ? 1
                          : 0;
     P.nt_groups = (h.level_bits[L - 1] + 3) / 4;
+
+    // generator hash tables: load factor <= 1/4
+    P.gtab_total = 0;
+    P.gens_total = goff;
+    for (int l = 0; l < dpb::kMaxLevels; ++l) {
+        P.gtab_off[l] = P.gtab_total;
+        P.gtab_bits[l] = 0;
+        if (l >= 1 && l < L) {
+            int bits = 6;
+            while ((1 << bits) < 4 * h.branching[l]) ++bits;
+            P.gtab_bits[l] = bits;
+            P.gtab_total += 1 << bits;
+        }
+    }
+    if (P.gtab_total > 16384) P.gtab_total = 0;  // too large for LDS: slots stay unrouted
     return DPB_OK;
+}
+
+// Generator hash tables (see DevPlan::gtab).
+void build_gen_tables(const dpb_plan* plan, std::vector<int32_t>* out)
+{
+    const DevPlan& P = plan->dev;
+    out->assign((size_t)std::max(P.gtab_total, 1), -1);
+    if (!P.gtab_total) return;
+    for (int l = 1; l < P.levels; ++l) {
+        const int bits = P.gtab_bits[l];
+        const uint32_t mask = (1u << bits) - 1u;
+        int32_t* tab = out->data() + P.gtab_off[l];
+        for (int j = 0; j < P.delta[l]; ++j) {
+            const uint32_t g = plan->gens_h[P.gens_off[l] + j];
+            uint32_t hsh = (g * dpb::kGenHashMul) >> (32 - bits);
+            while (tab[hsh] >= 0) hsh = (hsh + 1) & mask;
+            tab[hsh] = j;
+        }
+    }
 }
 
 inline uint32_t row_parity(uint32_t m, uint32_t p) { return (uint32_t)__builtin_popcount(m & p) & 1u; }
@@ -184,6 +219,8 @@ dpb_status upload(dpb_plan* plan)
     DevPlan& P = plan->dev;
     std::vector<uint16_t> gamma, gamma_pair, gamma_t;
     std::vector<uint32_t> nt;
+    std::vector<int32_t> gtab;
+    build_gen_tables(plan, &gtab);
     build_gamma_fragments(plan, &gamma);
     build_gamma_pair(plan, &gamma_pair);
     build_gamma_t(plan, &gamma_t);
@@ -204,6 +241,7 @@ dpb_status upload(dpb_plan* plan)
         {gamma_pair.data(), gamma_pair.size() * 2, 0},
         {gamma_t.data(), gamma_t.size() * 2, 0},
         {nt.data(), nt.size() * 4, 0},
+        {gtab.data(), gtab.size() * 4, 0},
     };
     size_t total = 0;
     for (Part& p : parts) {
@@ -234,6 +272,7 @@ dpb_status upload(dpb_plan* plan)
     P.gamma_pair = base + parts[3].off;
     P.gamma_t = base + parts[4].off;
     P.nt = (const uint32_t*)(base + parts[5].off);
+    P.gtab = (const int32_t*)(base + parts[6].off);
     return DPB_OK;
 }
 

@@ -49,45 +49,46 @@ struct Wave {
     uint32_t* cw;     // [16][nchunk] column sign bitmaps (g's sign folded in for bf16)
     float* score;     // [16][16] scores of one column block and generator tile
     const uint32_t* mask;  // [dp] row masks (shared)
-    const uint32_t* nt;    // nibble tables (shared)
+    const int32_t* gtab;   // generator hash tables (shared)
+    const uint32_t* gens;  // generators (shared)
+    const uint32_t* nt;    // nibble tables (shared, backward only)
 };
 
 __device__ __forceinline__ int rdlane(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
 
-// Finds (q, j) with c = parent_q XOR g_j, g_j a generator of level l, parent_q
-// read from `pv` (lane q holds parent q, q < nparents <= 64).  Generators come
-// from `gv` (lane j holds g_j) when Delta <= 64.  Returns (q << 16) | j for
-// the first match in (j, q) order, or -1.
-__device__ int route_one(const DevPlan& P, int l, uint32_t c, int pv, int nparents, uint32_t gv)
+// Routes every hashed slot of levels >= lmin: finds the first parent slot q
+// of the previous level (in slot order) and the generator j with
+// c = parent_q XOR g_j, by looking c XOR parent_q up in the level's generator
+// hash table.  W.route[tt][s] = (q << 16) | j, or -1 when no pair exists.
+__device__ void route_slots(const DevPlan& P, const Wave& W, int lmin)
 {
-    const int nprev = P.level_bits[l - 1];
-    const uint32_t hi = c >> nprev;
-    const uint32_t* g = P.gens + P.gens_off[l];
-    const bool reg = P.delta[l] <= 64;
-    for (int j = 0; j < P.delta[l]; ++j) {
-        const uint32_t gj = reg ? (uint32_t)rdlane((int)gv, j) : g[j];
-        if ((gj >> nprev) != hi) continue;  // every parent lies below 2^nprev
-        const int32_t p = (int32_t)(c ^ gj);
-        for (int q = 0; q < nparents; ++q)
-            if (rdlane(pv, q) == p) return (q << 16) | j;
-    }
-    return -1;
-}
-
-// Routes slots [s_begin, s_end) of level l for every token of the wave.
-__device__ void route_level(const DevPlan& P, const Wave& W, int l, int s_begin, int s_end)
-{
-    const int k = P.k_tot, sbp = P.slot_base[l - 1], Kp = P.active[l - 1];
-    if (Kp > 64) return;  // parents beyond one register: slots stay unrouted (handled directly)
-    const uint32_t gv = (P.delta[l] <= 64 && W.lane < P.delta[l]) ? P.gens[P.gens_off[l] + W.lane] : 0u;
-    for (int tt = 0; tt < W.ntok; ++tt) {
-        const int pv = W.lane < Kp ? W.idx[tt * k + sbp + W.lane] : -1;
-        for (int s0 = s_begin; s0 < s_end; s0 += 64) {
-            const int s = s0 + W.lane;
-            if (s >= s_end) continue;
-            const int32_t c = W.idx[tt * k + s];
-            W.route[tt * k + s] = c >= P.d ? route_one(P, l, (uint32_t)c, pv, Kp, gv) : -1;
+    const int k = P.k_tot, TPW = P.wave_tokens;
+    for (int job = W.lane; job < TPW * k; job += 64) {
+        const int tt = job / k, s = job - tt * k;
+        int rt = -1;
+        const int32_t c = W.idx[job];
+        if (tt < W.ntok && c >= P.d && P.gtab_total > 0 && P.levels > 1 && s >= P.slot_base[lmin]) {
+            int l = 1;
+            while (l + 1 < P.levels && s >= P.slot_base[l + 1]) ++l;
+            const int bits = P.gtab_bits[l], Kp = P.active[l - 1];
+            const uint32_t hmask = (1u << bits) - 1u;
+            const int32_t* tab = W.gtab + P.gtab_off[l];
+            const uint32_t* gl = W.gens + P.gens_off[l];
+            const int32_t* parents = W.idx + tt * k + P.slot_base[l - 1];
+            for (int q = 0; q < Kp && rt < 0; ++q) {
+                const int32_t p = parents[q];
+                if (p < 0) continue;
+                const uint32_t x = (uint32_t)c ^ (uint32_t)p;
+                uint32_t h = (x * kGenHashMul) >> (32 - bits);
+                for (int32_t j = tab[h]; j >= 0; h = (h + 1) & hmask, j = tab[h]) {
+                    if (gl[j] == x) {
+                        rt = (q << 16) | j;
+                        break;
+                    }
+                }
+            }
         }
+        W.route[job] = rt;
     }
 }
 
@@ -273,7 +274,9 @@ __device__ Wave make_wave(const DevPlan& P, unsigned char* smem, bool scoring, b
     W.cw = (uint32_t*)(b + CL.cw);
     W.score = (float*)(b + CL.score);
     W.mask = (const uint32_t*)smem;
-    W.nt = (const uint32_t*)(smem + align16u(P.dp * 4));
+    W.gtab = (const int32_t*)(smem + align16u(P.dp * 4));
+    W.gens = (const uint32_t*)(smem + align16u(P.dp * 4) + align16u(P.gtab_total * 4));
+    W.nt = (const uint32_t*)(smem + align16u(P.dp * 4) + align16u(P.gtab_total * 4) + align16u(P.gens_total * 4));
     return W;
 }
 
@@ -288,9 +291,13 @@ __device__ void write_rows(const DevPlan& P, const Wave& W, void* out)
 __device__ void load_shared(const DevPlan& P, unsigned char* smem, bool with_nt)
 {
     uint32_t* s_mask = (uint32_t*)smem;
+    int32_t* s_gtab = (int32_t*)(smem + align16u(P.dp * 4));
+    uint32_t* s_gens = (uint32_t*)(smem + align16u(P.dp * 4) + align16u(P.gtab_total * 4));
     for (int i = threadIdx.x; i < P.dp; i += kThreads) s_mask[i] = P.masks[i];
+    for (int i = threadIdx.x; i < P.gtab_total; i += kThreads) s_gtab[i] = P.gtab[i];
+    for (int i = threadIdx.x; i < P.gens_total; i += kThreads) s_gens[i] = P.gens[i];
     if (with_nt) {
-        uint32_t* s_nt = (uint32_t*)(smem + align16u(P.dp * 4));
+        uint32_t* s_nt = (uint32_t*)((unsigned char*)s_gens + align16u(P.gens_total * 4));
         for (int i = threadIdx.x; i < P.nt_groups * 16 * P.nchunk; i += kThreads) s_nt[i] = P.nt[i];
     }
     __syncthreads();
@@ -319,8 +326,7 @@ __global__ __launch_bounds__(kThreads) void decode2_kernel(DevPlan P, const int3
         }
         wave_sync();
         if (P.leaf_columns) {
-            const int L1 = P.levels - 1;
-            route_level(P, W, L1, P.slot_base[L1], P.slot_base[L1] + P.active[L1]);
+            route_slots(P, W, P.levels - 1);
             wave_sync();
         }
         decode_tokens<!OUT_BF16, UB>(P, W, W.coef);
@@ -380,7 +386,7 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
     extern __shared__ __align__(16) unsigned char smem[];
     load_shared(P, smem, true);
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, TPW = P.wave_tokens, k = P.k_tot;
-    const int d = P.d, dp = P.dp, nchunk = P.nchunk;
+    const int d = P.d, dp = P.dp;
     Wave W = make_wave(P, smem, true, G_BF16, wave, lane);
     const int64_t ngroups = (T + TPW - 1) / TPW;
     for (int64_t grp = (int64_t)blockIdx.x * kCodeWaves + wave; grp < ngroups;
@@ -407,7 +413,7 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
         wave_sync();
 
         // route every slot of levels >= 1 to a parent slot of the previous level
-        for (int l = 1; l < P.levels; ++l) route_level(P, W, l, P.slot_base[l], P.slot_base[l] + P.active[l]);
+        route_slots(P, W, 1);
         // coefficients for basis slots and padding
         for (int job = lane; job < TPW * k; job += 64) {
             const int tt = job / k;
@@ -423,15 +429,20 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
 
         // hashed slots that route nowhere: a direct reduction over the coordinates
         for (int tt = 0; tt < W.ntok; ++tt)
-            for (int s = 0; s < k; ++s) {
-                const int32_t c = W.idx[tt * k + s];
-                if (c < d || W.route[tt * k + s] >= 0) continue;
-                float part = 0.f;
-                for (int iota = lane; iota < d; iota += 64)
-                    part += signed_by_parity(g_at<G_BF16>(P, W, tt, iota), W.mask[iota] & (uint32_t)c);
-                const float sum = wave_sum(part);
-                if (lane == 0) W.coef[tt * k + s] = P.rsd * sum;
-                wave_sync();
+            for (int s0 = 0; s0 < k; s0 += 64) {
+                const int s = s0 + lane;
+                const int32_t cs = s < k ? W.idx[tt * k + s] : -1;
+                uint64_t todo = __ballot(s < k && cs >= d && W.route[tt * k + s] < 0);
+                while (todo) {
+                    const int b = __builtin_ctzll(todo);
+                    todo &= todo - 1;
+                    const uint32_t c = (uint32_t)rdlane(cs, b);
+                    float part = 0.f;
+                    for (int iota = lane; iota < d; iota += 64)
+                        part += signed_by_parity(g_at<G_BF16>(P, W, tt, iota), W.mask[iota] & c);
+                    const float sum = wave_sum(part);
+                    if (lane == 0) W.coef[tt * k + s0 + b] = P.rsd * sum;
+                }
             }
         wave_sync();
         for (int i = lane; i < W.ntok * k; i += 64) grad_coef[t0 * k + i] = W.coef[i];

@@ -52,7 +52,16 @@ struct DevPlan {
     // [dp/16][dpad/16][64] x 4 bf16.
     const void* gamma_t;
     int64_t gamma_t_off[kMaxLevels];  // in 8-byte units
+    // Open-addressing hash of each level's generators (value -> j, -1 empty),
+    // hash h(x) = (x * kGenHashMul) >> (32 - gtab_bits[l]), linear probing.
+    const int32_t* gtab;
+    int gtab_off[kMaxLevels];
+    int gtab_bits[kMaxLevels];
+    int gtab_total;             // entries over all levels (0: routing disabled)
+    int gens_total;             // sum_l Delta_l
 };
+
+constexpr uint32_t kGenHashMul = 0x9E3779B1u;
 
 // Per-wave LDS layout of the code kernels (byte offsets inside a wave's region).
 struct CodeLayout {
@@ -100,10 +109,12 @@ __host__ __device__ inline CodeLayout code_layout(const DevPlan& P, bool with_sc
 
 constexpr int kCodeWaves = 4;  // waves per workgroup in the code kernels
 
-// Shared (per-workgroup) LDS of the code kernels: row masks and nibble tables.
+// Shared (per-workgroup) LDS of the code kernels: row masks, generator hash
+// tables and generators, then (backward only) nibble tables.
 __host__ __device__ inline unsigned code_shared_bytes(const DevPlan& P, bool with_nt)
 {
-    return align16u(P.dp * 4) + (with_nt ? align16u(P.nt_groups * 16 * P.nchunk * 4) : 0u);
+    return align16u(P.dp * 4) + align16u(P.gtab_total * 4) + align16u(P.gens_total * 4) +
+           (with_nt ? align16u(P.nt_groups * 16 * P.nchunk * 4) : 0u);
 }
 
 // LDS layout of one encoder workgroup (byte offsets), shared by host and device.
