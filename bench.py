@@ -32,15 +32,59 @@ from paper_2607_20652_amd import inputs  # noqa: E402
 
 METRIC = "DPB fwd+bwd tokens/sec at d=768,N=2^20,k=64; % of HBM/VALU roofline"
 HBM_PEAK_GBS = 8000.0
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2607_20652_amd", "csrc", f) for f in ("kernels.hip", "dpb_internal.hpp")]
+CSRC = os.path.join(ROOT, "paper_2607_20652_amd", "csrc")
+COPY_BYTES = 256 << 20      # size of the plain copy that calibrates the HBM byte counters
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 
 
 def kernel_source_digest() -> str:
+    """Digest of every source the kernels and their plan tables are built from."""
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
-        h.update(open(p, "rb").read())
+    for f in sorted(os.listdir(CSRC)):
+        if f.endswith((".hip", ".hpp", ".cpp")):
+            h.update(f.encode())
+            h.update(open(os.path.join(CSRC, f), "rb").read())
     return h.hexdigest()[:16]
+
+
+KERNEL_SYMBOLS = {"encode": "encode", "decode": "decode2_kernel", "decode_bwd": "decode_bwd2_kernel"}
+
+
+def ingest_counters(fetch_csv: str, write_csv: str, workload: str) -> dict:
+    """HBM bytes per launch from two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE,
+    KiB per dispatch) of `bench.py --only K --with-copy`, each scaled by what the
+    same counter reads for the plain copy of COPY_BYTES in the same run."""
+    import csv
+
+    def per_kernel(path, counter):
+        acc = {}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            name = r["Kernel_Name"]
+            key = "copy"  # runtime copies and fills
+            for k, sym in KERNEL_SYMBOLS.items():
+                if sym in name and not (k == "encode" and "decode" in name):
+                    key = k
+            acc.setdefault(key, []).append(float(r["Counter_Value"]) * 1024.0)
+        if not acc.get("copy"):
+            raise SystemExit(f"{path}: no calibrating copy dispatch")
+        out = {k: float(np.median(v)) for k, v in acc.items() if k != "copy"}
+        # plan set-up also issues KB-sized runtime copies; the calibrating copy is the largest
+        out["copy"] = max(acc["copy"])
+        return out
+
+    fetch, write = per_kernel(fetch_csv, "FETCH_SIZE"), per_kernel(write_csv, "WRITE_SIZE")
+    f_scale = COPY_BYTES / fetch["copy"]
+    w_scale = COPY_BYTES / write["copy"]
+    T = inputs.workload(workload).tokens
+    rec = {"kernel_source_digest": kernel_source_digest(), "workload": workload,
+           "copy_bytes": COPY_BYTES, "fetch_scale": f_scale, "write_scale": w_scale, "kernels": {}}
+    for k in KERNEL_SYMBOLS:
+        if k in fetch and k in write:
+            rec["kernels"][k] = {"tokens": T, "fetch_bytes": fetch[k] * f_scale, "write_bytes": write[k] * w_scale,
+                                 "hbm_bytes_per_launch": fetch[k] * f_scale + write[k] * w_scale}
+    return rec
 
 
 def algorithmic_bytes_per_token(w, k_tot: int) -> dict:
@@ -108,7 +152,18 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only", choices=["encode", "decode", "decode_bwd"], default=None,
                     help="time a single kernel (for counter runs)")
+    ap.add_argument("--with-copy", action="store_true",
+                    help="also run one plain device copy of a known size (calibrates byte counters)")
+    ap.add_argument("--ingest-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the committed HBM-traffic record from two counter runs and exit")
     args = ap.parse_args()
+
+    if args.ingest_counters:
+        rec = ingest_counters(*args.ingest_counters, args.workload)
+        with open(TRAFFIC_FILE, "w") as f:
+            json.dump(rec, f, indent=1)
+        print(json.dumps(rec))
+        return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build runs on one GPU only; the DPB shards by tokens with no "
@@ -163,6 +218,13 @@ def main() -> int:
 
     if args.only in ("decode", "decode_bwd"):
         dpb.encode(plan, sets[0][0], idx, coef)  # codes for the kernels under test
+    if args.with_copy:
+        src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=dev)  # contents are irrelevant
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
