@@ -80,10 +80,23 @@ dpb_status fill_plan(dpb_plan* plan, const Hierarchy& h, const uint32_t* gens, u
     }
     P.wave_tokens = maxcpt >= 16 ? 1 : 16 / maxcpt;
     P.leaf_columns = (L >= 2 && P.cpt[L - 1] >= 4 && P.cpt[L - 1] <= 16 && h.active[L - 1] >= 2 * h.active[L - 2] &&
-                      P.dpad[L - 1] <= 64)
+                      P.dpad[L - 1] == 16 && P.slot_base[L - 2] + h.active[L - 2] <= dpb::kFrMax)
                          ? 1
                          : 0;
     P.nt_groups = (h.level_bits[L - 1] + 3) / 4;
+    P.cws = P.nchunk | 1;
+    for (int l = 0; l < dpb::kMaxLevels; ++l) {
+        int sh = 0;
+        while ((1 << sh) < P.cpt[l]) ++sh;
+        P.cpt_shift[l] = sh;
+    }
+    {
+        // table decode: the slots not taken by leaf columns, plus room for a few unclaimed leaves
+        const int nonleaf = P.leaf_columns ? P.slot_base[L - 1] : P.k_tot;
+        const int want = (nonleaf + 31) / 32 * 32;
+        P.fr_cap = std::min(dpb::kFrMax, std::max(32, want));
+        P.pb_bytes = (L >= 2 && h.active[L - 2] > 8) ? 2 : 1;
+    }
 
     // generator hash tables: load factor <= 1/4
     P.gtab_total = 0;
@@ -138,7 +151,7 @@ void build_nibble_tables(const dpb_plan* plan, std::vector<uint32_t>* out)
                     const int iota = 32 * w + b;
                     if (iota < P.d) word |= row_parity(plan->masks_h[iota], v << (4 * g)) << b;
                 }
-                (*out)[((size_t)g * 16 + v) * P.nchunk + w] = word;
+                (*out)[((size_t)g * P.nchunk + w) * 16 + v] = word;
             }
 }
 

@@ -37,16 +37,20 @@ struct Wave {
     int ntok;
     int32_t* idx;     // [TPW][k]
     float* coef;      // [TPW][k]
-    int32_t* route;   // [TPW][k]: (parent slot << 16) | j, or -1
-    int32_t* dir;     // [TPW][k]: 1 when a slot is decoded directly
+    int32_t* route;   // [TPW][k]: (parent slot << 16) | j (| kClaimed when decoded by its column), or -1
     int32_t* par;     // [16] parent index of each column row
     float* alpha;     // [16][dpad] column coefficients
     int32_t* claim;   // [16][dpad] lowest slot claiming (row, j)
+    int32_t* fri;     // [fr_cap] indices of the table-decoded slots
+    float* frc;       // [fr_cap] their coefficients (0 for basis and padding slots)
+    uint32_t* frv;    // [fr_cap / 32][8][16] slot-parity tables (256-byte aligned)
+    float* frt;       // [fr_cap / 4][16] signed coefficient sums
+    void* pb;         // [TPW][dp] sign bits of the leaf level's parents (pb_bytes each)
     float* y;         // [TPW][dp] output accumulator (fp32)
     uint32_t* pairs;  // [TPW][dp/2] |g| as bf16 pairs in the paired coordinate order
     uint32_t* signw;  // [TPW][nchunk] sign bits of g, natural order
     float* gf;        // [TPW][dp] fp32 g (fp32 activations)
-    uint32_t* cw;     // [16][nchunk] column sign bitmaps (g's sign folded in for bf16)
+    uint32_t* cw;     // [16][cws] column sign bitmaps (g's sign folded in for bf16)
     float* score;     // [16][16] scores of one column block and generator tile
     const uint32_t* mask;  // [dp] row masks (shared)
     const int32_t* gtab;   // generator hash tables (shared)
@@ -56,59 +60,181 @@ struct Wave {
 
 __device__ __forceinline__ int rdlane(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
 
+typedef __attribute__((address_space(3))) uint32_t lds_u32;
+typedef __attribute__((address_space(3))) float lds_f32;
+__device__ __forceinline__ uint32_t lds_addr(const void* p)
+{
+    return (uint32_t)(size_t)(const __attribute__((address_space(3))) void*)p;
+}
+__device__ __forceinline__ uint32_t lds_ld(uint32_t a) { return *(const lds_u32*)(size_t)a; }
+__device__ __forceinline__ float lds_ldf(uint32_t a) { return *(const lds_f32*)(size_t)a; }
+
 // Routes every hashed slot of levels >= lmin: finds the first parent slot q
 // of the previous level (in slot order) and the generator j with
 // c = parent_q XOR g_j, by looking c XOR parent_q up in the level's generator
 // hash table.  W.route[tt][s] = (q << 16) | j, or -1 when no pair exists.
 __device__ void route_slots(const DevPlan& P, const Wave& W, int lmin)
 {
-    const int k = P.k_tot, TPW = P.wave_tokens;
-    for (int job = W.lane; job < TPW * k; job += 64) {
-        const int tt = job / k, s = job - tt * k;
-        int rt = -1;
-        const int32_t c = W.idx[job];
-        if (tt < W.ntok && c >= P.d && P.gtab_total > 0 && P.levels > 1 && s >= P.slot_base[lmin]) {
-            int l = 1;
-            while (l + 1 < P.levels && s >= P.slot_base[l + 1]) ++l;
-            const int bits = P.gtab_bits[l], Kp = P.active[l - 1];
-            const uint32_t hmask = (1u << bits) - 1u;
-            const int32_t* tab = W.gtab + P.gtab_off[l];
-            const uint32_t* gl = W.gens + P.gens_off[l];
-            const int32_t* parents = W.idx + tt * k + P.slot_base[l - 1];
-            for (int q = 0; q < Kp && rt < 0; ++q) {
-                const int32_t p = parents[q];
-                if (p < 0) continue;
-                const uint32_t x = (uint32_t)c ^ (uint32_t)p;
-                uint32_t h = (x * kGenHashMul) >> (32 - bits);
-                for (int32_t j = tab[h]; j >= 0; h = (h + 1) & hmask, j = tab[h]) {
-                    if (gl[j] == x) {
-                        rt = (q << 16) | j;
-                        break;
+    const int k = P.k_tot;
+    if (P.gtab_total <= 0 || P.levels < 2) return;
+    for (int tt = 0; tt < W.ntok; ++tt)
+        for (int s = P.slot_base[lmin] + W.lane; s < k; s += 64) {
+            int rt = -1;
+            const int32_t c = W.idx[tt * k + s];
+            if (c >= P.d) {
+                int l = lmin;
+                while (l + 1 < P.levels && s >= P.slot_base[l + 1]) ++l;
+                const int bits = P.gtab_bits[l], Kp = P.active[l - 1];
+                const uint32_t hmask = (1u << bits) - 1u;
+                const int32_t* tab = W.gtab + P.gtab_off[l];
+                const uint32_t* gl = W.gens + P.gens_off[l];
+                const int32_t* parents = W.idx + tt * k + P.slot_base[l - 1];
+                for (int q = 0; q < Kp && rt < 0; ++q) {
+                    const int32_t p = parents[q];
+                    if (p < 0) continue;
+                    const uint32_t x = (uint32_t)c ^ (uint32_t)p;
+                    uint32_t h = (x * kGenHashMul) >> (32 - bits);
+                    for (int32_t j = tab[h]; j >= 0; h = (h + 1) & hmask, j = tab[h]) {
+                        if (gl[j] == x) {
+                            rt = (q << 16) | j;
+                            break;
+                        }
                     }
                 }
             }
+            W.route[tt * k + s] = rt;
         }
-        W.route[job] = rt;
+}
+
+// Bit transpose inside each 32-lane half: lane s of a half holds x_s on
+// entry; on exit lane b holds the word whose bit s is bit b of x_s.
+__device__ __forceinline__ uint32_t transpose32(uint32_t x, int lane)
+{
+    uint32_t o;
+    o = swz_xor<16>(x);
+    x = (lane & 16) ? ((x & 0xFFFF0000u) | ((o >> 16) & 0x0000FFFFu)) : ((x & 0x0000FFFFu) | ((o & 0x0000FFFFu) << 16));
+    o = swz_xor<8>(x);
+    x = (lane & 8) ? ((x & 0xFF00FF00u) | ((o >> 8) & 0x00FF00FFu)) : ((x & 0x00FF00FFu) | ((o & 0x00FF00FFu) << 8));
+    o = swz_xor<4>(x);
+    x = (lane & 4) ? ((x & 0xF0F0F0F0u) | ((o >> 4) & 0x0F0F0F0Fu)) : ((x & 0x0F0F0F0Fu) | ((o & 0x0F0F0F0Fu) << 4));
+    o = swz_xor<2>(x);
+    x = (lane & 2) ? ((x & 0xCCCCCCCCu) | ((o >> 2) & 0x33333333u)) : ((x & 0x33333333u) | ((o & 0x33333333u) << 2));
+    o = swz_xor<1>(x);
+    x = (lane & 1) ? ((x & 0xAAAAAAAAu) | ((o >> 1) & 0x55555555u)) : ((x & 0x55555555u) | ((o & 0x55555555u) << 1));
+    return x;
+}
+
+// Table decode ("four Russians") of the n <= fr_cap slots listed in
+// W.fri / W.frc for token tt.  For a coordinate iota the signs of the listed
+// slots form bit words U(iota), bit j = parity(M_iota & fri[j]) (App. A.4,
+// packed-parity equation).  Parity is linear in M_iota, so each word is the
+// XOR of one table row per 4-bit group of M_iota; the tables (frv) come from
+// the bit transpose of the listed indices.  The decode at iota is then
+//     y[iota] = (1/sqrt d) sum_j frc[j] (-1)^U_j(iota),
+// summed four slots at a time from 16-entry tables of signed sums (frt).
+// `first` overwrites y, otherwise adds.  When pbn > 0, bits pbpos ..
+// pbpos + pbn - 1 of U (the leaf level's parents) are stored in W.pb.
+// NG = number of 4-bit groups of the widest index.
+template <int NG, bool PB16>
+__device__ void fr_chunk(const DevPlan& P, const Wave& W, int tt, int n, bool first, int pbpos, int pbn)
+{
+    const int lane = W.lane, dp = P.dp;
+    const int Wn = (n + 31) >> 5;
+    // slot-parity tables: frv[w][g][v] = bits over the slots of word w of parity(idx & (v << 4g))
+    for (int h = 0; 64 * h < n; ++h) {
+        const int j = 64 * h + lane;
+        const uint32_t x = j < n ? (uint32_t)W.fri[j] : 0u;
+        const uint32_t E = transpose32(x, lane);
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+            const int w = 2 * h + hh;
+            if (w >= Wn) break;
+#pragma unroll
+            for (int pass = 0; pass < (NG + 3) / 4; ++pass) {
+                const int g = 4 * pass + (lane >> 4), v = lane & 15;
+                uint32_t V = 0;
+#pragma unroll
+                for (int b = 0; b < 4; ++b) {
+                    const uint32_t e = (uint32_t)__shfl((int)E, 32 * hh + 4 * g + b, 64);
+                    if ((v >> b) & 1) V ^= e;
+                }
+                if (g < NG) W.frv[(w * 8 + g) * 16 + v] = V;
+            }
+        }
     }
+    // signed sums of four coefficients: frt[i][v] = rsd * sum_b (-1)^(v_b) frc[4i + b],
+    // for every group of the used words (groups past n are zero)
+    for (int i0 = 0; i0 < 8 * Wn; i0 += 4) {
+        const int i = i0 + (lane >> 4), v = lane & 15;
+        const float4 c = *(const float4*)(W.frc + 4 * i);
+        const float t0 = __uint_as_float(__float_as_uint(c.x) ^ ((uint32_t)(v & 1) << 31)) +
+                         __uint_as_float(__float_as_uint(c.y) ^ ((uint32_t)((v >> 1) & 1) << 31));
+        const float t1 = __uint_as_float(__float_as_uint(c.z) ^ ((uint32_t)((v >> 2) & 1) << 31)) +
+                         __uint_as_float(__float_as_uint(c.w) ^ ((uint32_t)((v >> 3) & 1) << 31));
+        W.frt[i * 16 + v] = P.rsd * (t0 + t1);
+    }
+    wave_sync();
+
+    const uint32_t vbase = lds_addr(W.frv), tbase = lds_addr(W.frt);
+    float* yt = W.y + tt * dp;
+    const int w0 = pbpos >> 5, sh = pbpos & 31;
+    const uint32_t pmask = pbn >= 32 ? ~0u : ((1u << pbn) - 1u);
+    for (int iota = lane; iota < dp; iota += 64) {
+        // 4 x nibble g of the row mask: even groups in s0, odd groups in s1, byte g / 2
+        const uint32_t M = W.mask[iota];
+        const uint32_t s0 = (M << 2) & 0x3C3C3C3Cu, s1 = (M >> 2) & 0x3C3C3C3Cu;
+        float acc = 0.f;
+        uint32_t lo = 0, hi = 0;
+        for (int w = 0; w < Wn; ++w) {
+            const uint32_t vb = vbase + (uint32_t)(w * 512), tb = tbase + (uint32_t)(w * 512);
+            uint32_t U = 0;
+#pragma unroll
+            for (int g = 0; g < NG; ++g)
+                U ^= lds_ld(__builtin_amdgcn_perm(vb, (g & 1) ? s1 : s0, 0x07060500u | (uint32_t)(g >> 1)) +
+                            (uint32_t)(g * 64));
+#pragma unroll
+            for (int i8 = 0; i8 < 8; ++i8) {
+                // frt is 64-byte aligned: the nibble goes in with one and-or
+                const uint32_t sh4 = i8 == 0 ? (U << 2) : (U >> (4 * i8 - 2));
+                acc += lds_ldf((sh4 & 0x3Cu) | tb + (uint32_t)(i8 * 64));
+            }
+            lo = w == w0 ? U : lo;
+            hi = w == w0 + 1 ? U : hi;
+        }
+        if (first) yt[iota] = acc;
+        else yt[iota] += acc;
+        if (pbn > 0) {
+            const uint32_t bits = (sh ? ((lo >> sh) | (hi << (32 - sh))) : lo) & pmask;
+            if constexpr (PB16) ((uint16_t*)W.pb)[tt * dp + iota] = (uint16_t)bits;
+            else ((uint8_t*)W.pb)[tt * dp + iota] = (uint8_t)bits;
+        }
+    }
+    wave_sync();
 }
 
 // Decode of the wave's tokens from W.idx and coefficients `cf` into W.y.
-// W.route holds the routes of the last level's slots.
-template <bool EXACT3, int UB>
+// W.route holds the routes of the last level's slots (when decoding through
+// leaf columns).  PB16: the leaf parents' sign bits take 16 bits (else 8).
+template <bool EXACT3, int NG, bool PB16>
 __device__ void decode_tokens(const DevPlan& P, const Wave& W, const float* cf)
 {
     const int k = P.k_tot, d = P.d, dp = P.dp, TPW = P.wave_tokens, lane = W.lane;
     const int L1 = P.levels - 1;
     const bool cols = P.leaf_columns != 0;
+    const int sbL = cols ? P.slot_base[L1] : k;
+    const int row = lane & 15, grp = lane >> 4;
 
+    // leaf columns: claim (row, j) cells, then take the column coefficients into
+    // matrix-core A fragments (alpha and claims live in the y region until then)
+    bf16x4 ahi = {}, amid = {}, alo = {};
     if (cols) {
-        const int Kc = P.active[L1 - 1], CPT = P.cpt[L1], KL = P.active[L1], dpad = P.dpad[L1];
-        const int sbL = P.slot_base[L1], sbP = P.slot_base[L1 - 1];
+        const int Kc = P.active[L1 - 1], CPT = P.cpt[L1], KL = P.active[L1];
+        const int sbP = P.slot_base[L1 - 1];
         if (lane < 16) {
-            const int tt = lane / CPT, q = lane % CPT;
+            const int tt = lane >> P.cpt_shift[L1], q = lane & (CPT - 1);
             W.par[lane] = (tt < W.ntok && q < Kc) ? W.idx[tt * k + sbP + q] : -1;
         }
-        for (int i = lane; i < 16 * dpad; i += 64) {
+        for (int i = lane; i < 16 * 16; i += 64) {
             W.alpha[i] = 0.f;
             W.claim[i] = 0x7FFFFFFF;
         }
@@ -116,123 +242,105 @@ __device__ void decode_tokens(const DevPlan& P, const Wave& W, const float* cf)
         for (int tt = 0; tt < W.ntok; ++tt)
             for (int s = sbL + lane; s < sbL + KL; s += 64) {
                 const int rt = W.route[tt * k + s];
-                if (rt >= 0) atomicMin(&W.claim[(tt * CPT + (rt >> 16)) * dpad + (rt & 0xFFFF)], s);
+                if (rt >= 0) atomicMin(&W.claim[(tt * CPT + (rt >> 16)) * 16 + (rt & 0xFFFF)], s);
             }
         wave_sync();
         for (int tt = 0; tt < W.ntok; ++tt)
             for (int s = sbL + lane; s < sbL + KL; s += 64) {
                 const int rt = W.route[tt * k + s];
-                const int at = rt >= 0 ? (tt * CPT + (rt >> 16)) * dpad + (rt & 0xFFFF) : 0;
+                const int at = rt >= 0 ? (tt * CPT + (rt >> 16)) * 16 + (rt & 0xFFFF) : 0;
                 const bool mine = rt >= 0 && W.claim[at] == s;
-                if (mine) W.alpha[at] = cf[tt * k + s];
-                W.dir[tt * k + s] = mine ? 0 : 1;
-            }
-        wave_sync();
-
-        // Gamma^T alpha on the matrix cores, then the parent's signs
-        const int nkb = dpad / 16, row = lane & 15, grp = lane >> 4;
-        bf16x4 ahi[4], amid[4], alo[4];
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-            uint32_t h[4] = {0, 0, 0, 0}, m[4] = {0, 0, 0, 0}, lo[4] = {0, 0, 0, 0};
-            if (kb < nkb) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float a = W.alpha[row * dpad + 16 * kb + 4 * grp + i];
-                    if constexpr (EXACT3) {
-                        split3(a, h[i], m[i], lo[i]);
-                    } else {
-                        h[i] = f32_to_bf16_rne(a);
-                        lo[i] = f32_to_bf16_rne(a - bf16_bits_to_f32(h[i]));
-                    }
+                if (mine) {
+                    W.alpha[at] = cf[tt * k + s];
+                    W.route[tt * k + s] = rt | kClaimed;
                 }
             }
-            ahi[kb] = __builtin_bit_cast(bf16x4, (u32x2){h[0] | (h[1] << 16), h[2] | (h[3] << 16)});
-            amid[kb] = __builtin_bit_cast(bf16x4, (u32x2){m[0] | (m[1] << 16), m[2] | (m[3] << 16)});
-            alo[kb] = __builtin_bit_cast(bf16x4, (u32x2){lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16)});
-        }
-        uint32_t pr[4];
+        wave_sync();
+        uint32_t h[4] = {0, 0, 0, 0}, m[4] = {0, 0, 0, 0}, lo[4] = {0, 0, 0, 0};
 #pragma unroll
-        for (int i = 0; i < 4; ++i) pr[i] = (uint32_t)W.par[4 * grp + i];
+        for (int i = 0; i < 4; ++i) {
+            const float a = W.alpha[row * 16 + 4 * grp + i];
+            if constexpr (EXACT3) {
+                split3(a, h[i], m[i], lo[i]);
+            } else {
+                h[i] = f32_to_bf16_rne(a);
+                lo[i] = f32_to_bf16_rne(a - bf16_bits_to_f32(h[i]));
+            }
+        }
+        ahi = __builtin_bit_cast(bf16x4, (u32x2){h[0] | (h[1] << 16), h[2] | (h[3] << 16)});
+        amid = __builtin_bit_cast(bf16x4, (u32x2){m[0] | (m[1] << 16), m[2] | (m[3] << 16)});
+        alo = __builtin_bit_cast(bf16x4, (u32x2){lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16)});
+        wave_sync();
+    }
+
+    // table decode of every slot not taken by a column, in chunks of fr_cap
+    const int pbpos = cols ? P.slot_base[L1 - 1] : 0, pbn = cols ? P.active[L1 - 1] : 0, cap = P.fr_cap;
+    for (int tt = 0; tt < W.ntok; ++tt) {
+        const int32_t* it = W.idx + tt * k;
+        const int32_t* rt = W.route + tt * k;
+        const float* ct = cf + tt * k;
+        for (int cs = 0;; cs += cap) {
+            int base = 0;
+            for (int s0 = 0; s0 < k; s0 += 64) {
+                const int s = s0 + lane;
+                const int32_t c = s < k ? it[s] : -1;
+                const bool claimed = s < k && rt[s] >= 0 && (rt[s] & kClaimed);
+                const bool take = s < k && (s < sbL || (!claimed && c >= d));
+                const uint64_t m = __ballot(take);
+                const int pos = base + (int)__popcll(m & ((1ull << lane) - 1ull)) - cs;
+                if (take && pos >= 0 && pos < cap) {
+                    W.fri[pos] = c > 0 ? c : 0;
+                    W.frc[pos] = c >= d ? ct[s] : 0.f;
+                }
+                base += (int)__popcll(m);
+            }
+            const int n = max(0, min(base - cs, cap));
+            for (int j = n + lane; j < ((n + 31) & ~31); j += 64) W.frc[j] = 0.f;  // zero the rest of the last word
+            wave_sync();
+            fr_chunk<NG, PB16>(P, W, tt, n, cs == 0, pbpos - cs, (pbpos >= cs && pbpos < cs + cap) ? pbn : 0);
+            if (base <= cs + cap) break;
+        }
+    }
+
+    if (cols) {
+        // Gamma^T alpha on the matrix cores, then the parent's signs
+        const int CPT = P.cpt[L1];
         const u32x2* bfr = (const u32x2*)P.gamma_t + P.gamma_t_off[L1] + lane;
-        const int tok = (4 * grp) / CPT;
-        const bool writer = (grp % (CPT / 4)) == 0 && tok < TPW;
+        const int tok = (4 * grp) >> P.cpt_shift[L1], q0 = (4 * grp) & (CPT - 1);
+        const bool writer = (grp & ((CPT >> 2) - 1)) == 0 && tok < W.ntok;
+        const int pbo = (tok < TPW ? tok : 0) * dp + row;
+        float* yt = W.y + pbo;
+        const int x32 = ((lane ^ 32) << 2);
         const int ncb = dp / 16;
         for (int cb0 = 0; cb0 < ncb; cb0 += kBatch) {
-            u32x2 bf[kBatch][4];
-            uint32_t M[kBatch];
+            u32x2 bf[kBatch];
+            uint32_t pbv[kBatch];
 #pragma unroll
             for (int e = 0; e < kBatch; ++e) {
                 const int cb = cb0 + e < ncb ? cb0 + e : ncb - 1;
-#pragma unroll
-                for (int kb = 0; kb < 4; ++kb)
-                    if (kb < nkb) bf[e][kb] = bfr[((int64_t)cb * nkb + kb) * 64];
-                M[e] = W.mask[16 * cb + row];
+                bf[e] = bfr[(int64_t)cb * 64];
+                if constexpr (PB16) pbv[e] = (uint32_t)((const uint16_t*)W.pb)[pbo + 16 * cb] >> q0;
+                else pbv[e] = (uint32_t)((const uint8_t*)W.pb)[pbo + 16 * cb] >> q0;
             }
 #pragma unroll
             for (int e = 0; e < kBatch; ++e) {
+                const bf16x4 b = __builtin_bit_cast(bf16x4, bf[e]);
                 f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int kb = 0; kb < 4; ++kb) {
-                    if (kb >= nkb) break;
-                    const bf16x4 b = __builtin_bit_cast(bf16x4, bf[e][kb]);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ahi[kb], b, acc, 0, 0, 0);
-                    if constexpr (EXACT3) acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(amid[kb], b, acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(alo[kb], b, acc, 0, 0, 0);
-                }
-                float v = signed_by_parity(acc[0], M[e] & pr[0]) + signed_by_parity(acc[1], M[e] & pr[1]) +
-                          signed_by_parity(acc[2], M[e] & pr[2]) + signed_by_parity(acc[3], M[e] & pr[3]);
-                if (CPT >= 8) v += __shfl_xor(v, 16, 64);
-                if (CPT >= 16) v += __shfl_xor(v, 32, 64);
-                if (writer && cb0 + e < ncb) W.y[tok * dp + 16 * (cb0 + e) + row] = v;
+                acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ahi, b, acc, 0, 0, 0);
+                if constexpr (EXACT3) acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(amid, b, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(alo, b, acc, 0, 0, 0);
+                const uint32_t pv = pbv[e];
+                float v = (__uint_as_float(__float_as_uint(acc[0]) ^ (pv << 31)) +
+                           __uint_as_float(__float_as_uint(acc[1]) ^ ((pv >> 1) << 31))) +
+                          (__uint_as_float(__float_as_uint(acc[2]) ^ ((pv >> 2) << 31)) +
+                           __uint_as_float(__float_as_uint(acc[3]) ^ ((pv >> 3) << 31)));
+                if (CPT >= 8) v += swz_xorf16(v);
+                if (CPT >= 16) v += __int_as_float(__builtin_amdgcn_ds_bpermute(x32, __float_as_int(v)));
+                if (writer && cb0 + e < ncb) yt[16 * (cb0 + e)] += P.rsd * v;
             }
         }
-    } else {
-        for (int i = lane; i < TPW * dp; i += 64) W.y[i] = 0.f;
+        wave_sync();
     }
-    wave_sync();
-
-    // direct slots: +-coef at every coordinate; lanes own iota = lane + 64u.
-    // Slot data sits in registers (lane s <-> slot s0 + s) and is broadcast.
-    const int U = (dp + 63) / 64;
-    const int sbL = P.slot_base[L1];
-    for (int tt = 0; tt < W.ntok; ++tt) {
-        float* yt = W.y + tt * dp;
-        for (int u0 = 0; u0 < U; u0 += UB) {
-            float acc[UB];
-            uint32_t M[UB];
-#pragma unroll
-            for (int uu = 0; uu < UB; ++uu) {
-                const int iota = lane + 64 * (u0 + uu);
-                const bool ok = iota < dp;
-                acc[uu] = ok ? yt[iota] : 0.f;
-                M[uu] = ok ? W.mask[iota] : 0u;
-            }
-            for (int s0 = 0; s0 < k; s0 += 64) {
-                const int s = s0 + lane;
-                int32_t cv = s < k ? W.idx[tt * k + s] : -1;
-                if (s < k && cols && s >= sbL && W.dir[tt * k + s] == 0) cv = -1;  // decoded through its column
-                const int av = s < k ? __float_as_int(cf[tt * k + s]) : 0;
-                uint64_t live = __ballot(cv >= d);
-                while (live) {
-                    const int b = __builtin_ctzll(live);
-                    live &= live - 1;
-                    const uint32_t c = (uint32_t)rdlane(cv, b);
-                    const uint32_t au = (uint32_t)rdlane(av, b);
-                    const uint32_t sg = au >> 31, mag = au & 0x7FFFFFFFu;
-#pragma unroll
-                    for (int uu = 0; uu < UB; ++uu)
-                        acc[uu] += __uint_as_float(((__popc(M[uu] & c) + sg) << 31) | mag);
-                }
-            }
-#pragma unroll
-            for (int uu = 0; uu < UB; ++uu) {
-                const int iota = lane + 64 * (u0 + uu);
-                if (iota < dp) yt[iota] = P.rsd * acc[uu];
-            }
-        }
-    }
-    wave_sync();
 
     // basis slots: coefficient at their own coordinate, in slot order
     for (int tt = 0; tt < W.ntok; ++tt)
@@ -263,73 +371,115 @@ __device__ Wave make_wave(const DevPlan& P, unsigned char* smem, bool scoring, b
     W.idx = (int32_t*)(b + CL.idx);
     W.coef = (float*)(b + CL.coef);
     W.route = (int32_t*)(b + CL.route);
-    W.dir = (int32_t*)(b + CL.dir);
     W.par = (int32_t*)(b + CL.par);
     W.alpha = (float*)(b + CL.alpha);
     W.claim = (int32_t*)(b + CL.claim);
+    W.fri = (int32_t*)(b + CL.fri);
+    W.frc = (float*)(b + CL.frc);
+    W.frv = (uint32_t*)(b + CL.frv);
+    W.frt = (float*)(b + CL.frt);
+    W.pb = (void*)(b + CL.pb);
     W.y = (float*)(b + CL.y);
     W.pairs = (uint32_t*)(b + CL.pairs);
     W.signw = (uint32_t*)(b + CL.signw);
     W.gf = (float*)(b + CL.y);
     W.cw = (uint32_t*)(b + CL.cw);
     W.score = (float*)(b + CL.score);
+    const unsigned o_gtab = align16u(P.dp * 4);
+    const unsigned o_gens = o_gtab + align16u(P.gtab_total * 4), o_nt = o_gens + align16u(P.gens_total * 4);
     W.mask = (const uint32_t*)smem;
-    W.gtab = (const int32_t*)(smem + align16u(P.dp * 4));
-    W.gens = (const uint32_t*)(smem + align16u(P.dp * 4) + align16u(P.gtab_total * 4));
-    W.nt = (const uint32_t*)(smem + align16u(P.dp * 4) + align16u(P.gtab_total * 4) + align16u(P.gens_total * 4));
+    W.gtab = (const int32_t*)(smem + o_gtab);
+    W.gens = (const uint32_t*)(smem + o_gens);
+    W.nt = (const uint32_t*)(smem + o_nt);
     return W;
 }
 
+// Converts the wave's fp32 rows to the output type, 8 coordinates per lane
+// (16- or 32-byte stores when d is a multiple of 8).
 template <bool OUT_BF16>
 __device__ void write_rows(const DevPlan& P, const Wave& W, void* out)
 {
-    for (int tt = 0; tt < W.ntok; ++tt)
-        for (int iota = W.lane; iota < P.d; iota += 64)
-            store_act<OUT_BF16>(out, (W.t0 + tt) * P.d + iota, W.y[tt * P.dp + iota]);
+    const int d = P.d, dp = P.dp;
+    const bool vec = (d & 7) == 0;
+    for (int tt = 0; tt < W.ntok; ++tt) {
+        const float* yt = W.y + tt * dp;
+        const int64_t r0 = (W.t0 + tt) * d;
+        for (int o = W.lane * 8; o < d; o += 512) {
+            const float4 a = *(const float4*)(yt + o), b = *(const float4*)(yt + o + 4);
+            if (vec) {
+                if constexpr (OUT_BF16) {
+                    u32x4 v;
+                    v.x = f32_to_bf16_rne(a.x) | (f32_to_bf16_rne(a.y) << 16);
+                    v.y = f32_to_bf16_rne(a.z) | (f32_to_bf16_rne(a.w) << 16);
+                    v.z = f32_to_bf16_rne(b.x) | (f32_to_bf16_rne(b.y) << 16);
+                    v.w = f32_to_bf16_rne(b.z) | (f32_to_bf16_rne(b.w) << 16);
+                    *(u32x4*)((uint16_t*)out + r0 + o) = v;
+                } else {
+                    *(float4*)((float*)out + r0 + o) = a;
+                    *(float4*)((float*)out + r0 + o + 4) = b;
+                }
+            } else {
+                const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    if (o + e < d) store_act<OUT_BF16>(out, r0 + o + e, v[e]);
+            }
+        }
+    }
 }
 
 __device__ void load_shared(const DevPlan& P, unsigned char* smem, bool with_nt)
 {
+    const unsigned o_gtab = align16u(P.dp * 4);
+    const unsigned o_gens = o_gtab + align16u(P.gtab_total * 4), o_nt = o_gens + align16u(P.gens_total * 4);
     uint32_t* s_mask = (uint32_t*)smem;
-    int32_t* s_gtab = (int32_t*)(smem + align16u(P.dp * 4));
-    uint32_t* s_gens = (uint32_t*)(smem + align16u(P.dp * 4) + align16u(P.gtab_total * 4));
+    int32_t* s_gtab = (int32_t*)(smem + o_gtab);
+    uint32_t* s_gens = (uint32_t*)(smem + o_gens);
     for (int i = threadIdx.x; i < P.dp; i += kThreads) s_mask[i] = P.masks[i];
     for (int i = threadIdx.x; i < P.gtab_total; i += kThreads) s_gtab[i] = P.gtab[i];
     for (int i = threadIdx.x; i < P.gens_total; i += kThreads) s_gens[i] = P.gens[i];
     if (with_nt) {
-        uint32_t* s_nt = (uint32_t*)((unsigned char*)s_gens + align16u(P.gens_total * 4));
+        uint32_t* s_nt = (uint32_t*)(smem + o_nt);
         for (int i = threadIdx.x; i < P.nt_groups * 16 * P.nchunk; i += kThreads) s_nt[i] = P.nt[i];
     }
     __syncthreads();
 }
 
-template <bool OUT_BF16, int UB>
+// Loads the codes of the wave's tokens into LDS and resets routes.
+__device__ void load_codes(const DevPlan& P, const Wave& W, const int32_t* idx, const float* coef)
+{
+    const int k = P.k_tot, TPW = P.wave_tokens;
+    for (int tt = 0; tt < TPW; ++tt) {
+        const bool live = tt < W.ntok;
+        for (int s = W.lane; s < k; s += 64) {
+            W.idx[tt * k + s] = live ? idx[(W.t0 + tt) * k + s] : -1;
+            if (coef) W.coef[tt * k + s] = live ? coef[(W.t0 + tt) * k + s] : 0.f;
+            W.route[tt * k + s] = -1;
+        }
+    }
+}
+
+template <bool OUT_BF16, int NG, bool PB16>
 __global__ __launch_bounds__(kThreads) void decode2_kernel(DevPlan P, const int32_t* __restrict__ idx,
                                                            const float* __restrict__ coef, int64_t T,
                                                            void* __restrict__ y)
 {
     extern __shared__ __align__(16) unsigned char smem[];
     load_shared(P, smem, false);
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, TPW = P.wave_tokens, k = P.k_tot;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, TPW = P.wave_tokens;
     Wave W = make_wave(P, smem, false, true, wave, lane);
     const int64_t ngroups = (T + TPW - 1) / TPW;
     for (int64_t grp = (int64_t)blockIdx.x * kCodeWaves + wave; grp < ngroups;
          grp += (int64_t)gridDim.x * kCodeWaves) {
         W.t0 = grp * TPW;
         W.ntok = (int)min((int64_t)TPW, T - W.t0);
-        for (int i = lane; i < TPW * k; i += 64) {
-            const bool live = i / k < W.ntok;
-            W.idx[i] = live ? idx[W.t0 * k + i] : -1;
-            W.coef[i] = live ? coef[W.t0 * k + i] : 0.f;
-            W.route[i] = -1;
-            W.dir[i] = 1;
-        }
+        load_codes(P, W, idx, coef);
         wave_sync();
         if (P.leaf_columns) {
             route_slots(P, W, P.levels - 1);
             wave_sync();
         }
-        decode_tokens<!OUT_BF16, UB>(P, W, W.coef);
+        decode_tokens<!OUT_BF16, NG, PB16>(P, W, W.coef);
         write_rows<OUT_BF16>(P, W, y);
         wave_sync();
     }
@@ -377,7 +527,7 @@ __device__ void score_level(const DevPlan& P, const Wave& W, int l)
     }
 }
 
-template <bool G_BF16, bool GX_BF16, int UB>
+template <bool G_BF16, bool GX_BF16, int NG, bool PB16>
 __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const int32_t* __restrict__ idx,
                                                                const void* __restrict__ g, int64_t T,
                                                                float* __restrict__ grad_coef,
@@ -396,32 +546,27 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
         W.ntok = (int)min((int64_t)TPW, T - t0);
 
         // codes, routes reset, and g in LDS
-        for (int i = lane; i < TPW * k; i += 64) {
-            W.idx[i] = i / k < W.ntok ? idx[t0 * k + i] : -1;
-            W.route[i] = -1;
-            W.dir[i] = 1;
-        }
+        load_codes(P, W, idx, nullptr);
         if constexpr (G_BF16) {
             load_pairs(P, lane, W.ntok, TPW, (const uint16_t*)g, t0, W.pairs, W.signw);
         } else {
             const float* gfp = (const float*)g;
-            for (int e = lane; e < TPW * dp; e += 64) {
-                const int tt = e / dp, iota = e - tt * dp;
-                W.gf[e] = (tt < W.ntok && iota < d) ? gfp[(t0 + tt) * d + iota] : 0.f;
-            }
+            for (int tt = 0; tt < TPW; ++tt)
+                for (int iota = lane; iota < dp; iota += 64)
+                    W.gf[tt * dp + iota] = (tt < W.ntok && iota < d) ? gfp[(t0 + tt) * d + iota] : 0.f;
         }
         wave_sync();
 
         // route every slot of levels >= 1 to a parent slot of the previous level
         route_slots(P, W, 1);
         // coefficients for basis slots and padding
-        for (int job = lane; job < TPW * k; job += 64) {
-            const int tt = job / k;
-            const int32_t c = W.idx[job];
-            float v = 0.f;
-            if (tt < W.ntok && c >= 0 && c < d) v = g_at<G_BF16>(P, W, tt, c);
-            W.coef[job] = v;
-        }
+        for (int tt = 0; tt < TPW; ++tt)
+            for (int s = lane; s < k; s += 64) {
+                const int32_t c = W.idx[tt * k + s];
+                float v = 0.f;
+                if (tt < W.ntok && c >= 0 && c < d) v = g_at<G_BF16>(P, W, tt, c);
+                W.coef[tt * k + s] = v;
+            }
         wave_sync();
 
         // grad_coef of routed slots: child scores of each parent column against g
@@ -448,16 +593,10 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
         for (int i = lane; i < W.ntok * k; i += 64) grad_coef[t0 * k + i] = W.coef[i];
 
         // grad_x = decode(idx, grad_coef); the scoring buffers are dead now
-        decode_tokens<!GX_BF16, UB>(P, W, W.coef);
+        decode_tokens<!GX_BF16, NG, PB16>(P, W, W.coef);
         write_rows<GX_BF16>(P, W, grad_x);
         wave_sync();
     }
-}
-
-int pick_ub(const DevPlan& P)
-{
-    const int U = (P.dp + 63) / 64;
-    return U <= 4 ? 4 : U <= 8 ? 8 : U <= 12 ? 12 : 16;
 }
 
 size_t code_lds_bytes(const DevPlan& P, bool scoring, bool act_bf16)
@@ -495,11 +634,34 @@ bool code_kernels_fit(const DevPlan& P)
     return code_lds_bytes(P, true, true) <= (size_t)kLdsBudget && code_lds_bytes(P, true, false) <= (size_t)kLdsBudget;
 }
 
-#define DPB_DECODE_CASE(OB, UBV)                                                                          \
-    do {                                                                                                  \
-        allow_lds(decode2_kernel<OB, UBV>, lds);                                                          \
-        hipLaunchKernelGGL((decode2_kernel<OB, UBV>), grid, dim3(kThreads), lds, stream, P, idx, coef, T, y); \
-    } while (0)
+// Kernel variants: index groups NG in {3, 4, 5, 6, 8} (a larger NG than the
+// plan needs is exact: the extra table rows are zero) and the width of the
+// leaf parents' sign bits.
+int ng_variant(const DevPlan& P)
+{
+    return P.nt_groups <= 3 ? 3 : P.nt_groups <= 6 ? P.nt_groups : 8;
+}
+
+template <bool OB, int NG, bool PB>
+static void launch_decode_v(const DevPlan& P, dim3 grid, size_t lds, hipStream_t stream, const int32_t* idx,
+                            const float* coef, int64_t T, void* y)
+{
+    allow_lds(decode2_kernel<OB, NG, PB>, lds);
+    hipLaunchKernelGGL((decode2_kernel<OB, NG, PB>), grid, dim3(kThreads), lds, stream, P, idx, coef, T, y);
+}
+
+template <bool OB, bool PB>
+static void launch_decode_ng(const DevPlan& P, dim3 grid, size_t lds, hipStream_t stream, const int32_t* idx,
+                             const float* coef, int64_t T, void* y)
+{
+    switch (ng_variant(P)) {
+    case 3: launch_decode_v<OB, 3, PB>(P, grid, lds, stream, idx, coef, T, y); break;
+    case 4: launch_decode_v<OB, 4, PB>(P, grid, lds, stream, idx, coef, T, y); break;
+    case 5: launch_decode_v<OB, 5, PB>(P, grid, lds, stream, idx, coef, T, y); break;
+    case 6: launch_decode_v<OB, 6, PB>(P, grid, lds, stream, idx, coef, T, y); break;
+    default: launch_decode_v<OB, 8, PB>(P, grid, lds, stream, idx, coef, T, y); break;
+    }
+}
 
 hipError_t launch_decode2(const DevPlan& P, const int32_t* idx, const float* coef, int64_t T, void* y, bool y_bf16,
                           hipStream_t stream)
@@ -507,38 +669,41 @@ hipError_t launch_decode2(const DevPlan& P, const int32_t* idx, const float* coe
     const size_t lds = code_lds_bytes(P, false, true);
     if (lds > (size_t)kLdsBudget) return hipErrorInvalidValue;
     const dim3 grid = code_grid(P, T, lds);
-    const int ub = pick_ub(P);
-    if (y_bf16) {
-        if (ub == 4) DPB_DECODE_CASE(true, 4);
-        else if (ub == 8) DPB_DECODE_CASE(true, 8);
-        else if (ub == 12) DPB_DECODE_CASE(true, 12);
-        else DPB_DECODE_CASE(true, 16);
-    } else {
-        if (ub == 4) DPB_DECODE_CASE(false, 4);
-        else if (ub == 8) DPB_DECODE_CASE(false, 8);
-        else if (ub == 12) DPB_DECODE_CASE(false, 12);
-        else DPB_DECODE_CASE(false, 16);
-    }
+    const bool pb16 = P.pb_bytes == 2;
+    if (y_bf16 && pb16) launch_decode_ng<true, true>(P, grid, lds, stream, idx, coef, T, y);
+    else if (y_bf16) launch_decode_ng<true, false>(P, grid, lds, stream, idx, coef, T, y);
+    else if (pb16) launch_decode_ng<false, true>(P, grid, lds, stream, idx, coef, T, y);
+    else launch_decode_ng<false, false>(P, grid, lds, stream, idx, coef, T, y);
     return hipGetLastError();
+}
+
+template <bool GB, bool XB, int NG, bool PB>
+static void launch_bwd_v(const DevPlan& P, dim3 grid, size_t lds, hipStream_t stream, const int32_t* idx,
+                         const void* g, int64_t T, float* gc, void* gx)
+{
+    allow_lds(decode_bwd2_kernel<GB, XB, NG, PB>, lds);
+    hipLaunchKernelGGL((decode_bwd2_kernel<GB, XB, NG, PB>), grid, dim3(kThreads), lds, stream, P, idx, g, T, gc, gx);
+}
+
+template <bool GB, bool XB, bool PB>
+static void launch_bwd_ng(const DevPlan& P, dim3 grid, size_t lds, hipStream_t stream, const int32_t* idx,
+                          const void* g, int64_t T, float* gc, void* gx)
+{
+    switch (ng_variant(P)) {
+    case 3: launch_bwd_v<GB, XB, 3, PB>(P, grid, lds, stream, idx, g, T, gc, gx); break;
+    case 4: launch_bwd_v<GB, XB, 4, PB>(P, grid, lds, stream, idx, g, T, gc, gx); break;
+    case 5: launch_bwd_v<GB, XB, 5, PB>(P, grid, lds, stream, idx, g, T, gc, gx); break;
+    case 6: launch_bwd_v<GB, XB, 6, PB>(P, grid, lds, stream, idx, g, T, gc, gx); break;
+    default: launch_bwd_v<GB, XB, 8, PB>(P, grid, lds, stream, idx, g, T, gc, gx); break;
+    }
 }
 
 template <bool GB, bool XB>
 static void launch_bwd_ub(const DevPlan& P, dim3 grid, size_t lds, hipStream_t stream, const int32_t* idx,
                           const void* g, int64_t T, float* gc, void* gx)
 {
-    const int ub = pick_ub(P);
-    allow_lds(decode_bwd2_kernel<GB, XB, 4>, lds);
-    allow_lds(decode_bwd2_kernel<GB, XB, 8>, lds);
-    allow_lds(decode_bwd2_kernel<GB, XB, 12>, lds);
-    allow_lds(decode_bwd2_kernel<GB, XB, 16>, lds);
-    if (ub == 4)
-        hipLaunchKernelGGL((decode_bwd2_kernel<GB, XB, 4>), grid, dim3(kThreads), lds, stream, P, idx, g, T, gc, gx);
-    else if (ub == 8)
-        hipLaunchKernelGGL((decode_bwd2_kernel<GB, XB, 8>), grid, dim3(kThreads), lds, stream, P, idx, g, T, gc, gx);
-    else if (ub == 12)
-        hipLaunchKernelGGL((decode_bwd2_kernel<GB, XB, 12>), grid, dim3(kThreads), lds, stream, P, idx, g, T, gc, gx);
-    else
-        hipLaunchKernelGGL((decode_bwd2_kernel<GB, XB, 16>), grid, dim3(kThreads), lds, stream, P, idx, g, T, gc, gx);
+    if (P.pb_bytes == 2) launch_bwd_ng<GB, XB, true>(P, grid, lds, stream, idx, g, T, gc, gx);
+    else launch_bwd_ng<GB, XB, false>(P, grid, lds, stream, idx, g, T, gc, gx);
 }
 
 hipError_t launch_decode_bwd2(const DevPlan& P, const int32_t* idx, const void* g, bool g_bf16, int64_t T,

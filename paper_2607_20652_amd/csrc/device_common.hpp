@@ -72,15 +72,15 @@ __device__ __forceinline__ void store_act(void* p, int64_t i, float v)
     else ((float*)p)[i] = v;
 }
 
-// Word w of the sign bitmap of index p (bit b = sign bit at coordinate
-// 32w + b): the XOR of one nibble-table row per 4-bit group of p, because
-// parity(M & p) is linear in the bits of p.
-__device__ __forceinline__ uint32_t bitmap_word(const uint32_t* nt, int groups, int nchunk, uint32_t p, int w)
+// Lane exchanges without address arithmetic: XOR of the lane index by
+// 1..16 inside 32-lane halves (ds_swizzle bit mode), and by 32.
+template <int J>
+__device__ __forceinline__ uint32_t swz_xor(uint32_t v)
 {
-    uint32_t acc = 0;
-    for (int g = 0; g < groups; ++g) acc ^= nt[(g * 16 + ((p >> (4 * g)) & 15u)) * nchunk + w];
-    return acc;
+    static_assert(J >= 1 && J <= 16, "swizzle xor within 32 lanes");
+    return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, (J << 10) | 0x1F);
 }
+__device__ __forceinline__ float swz_xorf16(float v) { return __uint_as_float(swz_xor<16>(__float_as_uint(v))); }
 
 // Rotates left by r (0..31).
 __device__ __forceinline__ uint32_t rotl32(uint32_t v, uint32_t r) { return __builtin_amdgcn_alignbit(v, v, (32u - r) & 31u); }

@@ -42,7 +42,11 @@ struct DevPlan {
     int cpt[kMaxLevels];        // parent columns per token at level l: K_{l-1} rounded up to a power of two
     int dpad[kMaxLevels];       // Delta_l rounded up to a multiple of 16
     int nt_groups;              // 4-bit index groups of the widest index
-    const uint32_t* nt;         // [nt_groups][16][nchunk] sign-bitmap words of (v << 4g)
+    int cws;                    // row stride of column bitmaps in LDS (odd, >= nchunk)
+    int cpt_shift[kMaxLevels];  // log2 cpt[l]
+    const uint32_t* nt;         // [nt_groups][nchunk][16] sign-bitmap word w of (v << 4g)
+    int fr_cap;                 // slots per table-decode chunk (multiple of 32, <= kFrMax)
+    int pb_bytes;               // bytes per coordinate of the leaf parents' sign bits (1 or 2)
     // Scoring A fragments with the paired coordinate order: lane L, element
     // e = 2i + h of chunk c holds generator row 16*mb + L%16 at coordinate
     // 32c + L/16 + 4i + 16h.  Per level: [mblocks][nchunk][64] x 8 bf16.
@@ -65,8 +69,11 @@ constexpr uint32_t kGenHashMul = 0x9E3779B1u;
 
 // Per-wave LDS layout of the code kernels (byte offsets inside a wave's region).
 struct CodeLayout {
-    unsigned idx, coef, route, dir, par, alpha, claim, y, pairs, signw, cw, score, bytes;
+    unsigned idx, coef, route, par, alpha, claim, fri, frc, frv, frt, pb, y, pairs, signw, cw, score, bytes;
 };
+
+constexpr int kFrMax = 256;          // largest table-decode chunk
+constexpr int kClaimed = 1 << 29;    // route flag: the slot is decoded through its column
 
 __host__ __device__ inline unsigned align16u(unsigned v) { return (v + 15u) & ~15u; }
 
@@ -83,12 +90,19 @@ __host__ __device__ inline CodeLayout code_layout(const DevPlan& P, bool with_sc
     L.idx = off;   off = align16u(off + TPW * k * 4);
     L.coef = off;  off = align16u(off + TPW * k * 4);
     L.route = off; off = align16u(off + TPW * k * 4);
-    L.dir = off;   off = align16u(off + TPW * k * 4);
     L.par = off;   off = align16u(off + 16 * 4);
-    L.alpha = off; off = align16u(off + 16 * dleaf * 4);
-    L.claim = off; off = align16u(off + 16 * dleaf * 4);
+    L.fri = off;   off = align16u(off + P.fr_cap * 4);
+    L.frc = off;   off = align16u(off + P.fr_cap * 4);
+    L.frv = off = (off + 255u) & ~255u;  off += (P.fr_cap / 32) * 8 * 16 * 4;
+    L.frt = off;   off = align16u(off + (P.fr_cap / 4) * 16 * 4);
+    L.pb = off;    off = align16u(off + (P.leaf_columns ? TPW * P.dp * P.pb_bytes : 0));
     L.y = off;
-    const unsigned yend = align16u(off + TPW * P.dp * 4);
+    // column coefficients and claims are done with before y is written
+    L.alpha = off;
+    L.claim = align16u(off + 16 * dleaf * 4);
+    unsigned yend = align16u(off + TPW * P.dp * 4);
+    const unsigned cend = align16u(L.claim + 16 * dleaf * 4);
+    if (cend > yend) yend = cend;
     L.pairs = L.signw = L.cw = L.score = yend;
     off = yend;
     if (with_scoring) {
@@ -99,11 +113,11 @@ __host__ __device__ inline CodeLayout code_layout(const DevPlan& P, bool with_sc
         } else {
             L.pairs = L.signw = L.y;  // fp32 activations occupy the y region
         }
-        L.cw = s;    s = align16u(s + 16 * P.nchunk * 4);
+        L.cw = s;    s = align16u(s + 16 * P.cws * 4);
         L.score = s; s = align16u(s + 16 * 16 * 4);  // one 16 x 16 score tile
         off = s > yend ? s : yend;
     }
-    L.bytes = off;
+    L.bytes = (off + 255u) & ~255u;  // keeps every wave's table region 256-byte aligned
     return L;
 }
 
@@ -113,8 +127,9 @@ constexpr int kCodeWaves = 4;  // waves per workgroup in the code kernels
 // tables and generators, then (backward only) nibble tables.
 __host__ __device__ inline unsigned code_shared_bytes(const DevPlan& P, bool with_nt)
 {
-    return align16u(P.dp * 4) + align16u(P.gtab_total * 4) + align16u(P.gens_total * 4) +
-           (with_nt ? align16u(P.nt_groups * 16 * P.nchunk * 4) : 0u);
+    const unsigned b = align16u(P.dp * 4) + align16u(P.gtab_total * 4) + align16u(P.gens_total * 4) +
+                       (with_nt ? align16u(P.nt_groups * 16 * P.nchunk * 4) : 0u);
+    return (b + 255u) & ~255u;
 }
 
 // LDS layout of one encoder workgroup (byte offsets), shared by host and device.

@@ -57,7 +57,7 @@ __host__ __device__ inline EncLayout enc_layout(const DevPlan& P, bool act_bf16)
     unsigned off = 0;
     L.act = off;
     off = align16u(off + (act_bf16 ? TPW * (P.dp * 2 + P.nchunk * 4) : TPW * P.dp * 4));
-    L.cw = off;   off = align16u(off + 16 * P.nchunk * 4);
+    L.cw = off;   off = align16u(off + 16 * P.cws * 4);
     L.par = off;  off = align16u(off + TPW * L.kmaxp * 4);
     L.list = off; off = align16u(off + TPW * listn * 8);
     L.bytes = off;

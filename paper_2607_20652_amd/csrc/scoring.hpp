@@ -25,25 +25,34 @@ struct ActTile {
     const float* f;         // fp32: [TPW][dp]
 };
 
-// Sign bitmaps of the 16 columns of block nb at level l into cw[16][nchunk];
+// Sign bitmaps of the 16 columns of block nb at level l into cw[16][cws];
 // for bf16 activations the activation signs are folded in.  Column r has
-// parent parents[tt * pstride + q] when q < nparents and tt < ntok.
+// parent parents[tt * pstride + q] when q < nparents and tt < ntok.  Lane
+// (col, w0) builds words w0, w0 + 4, ... of column col: one nibble-table row
+// per 4-bit group of the parent index (parity is linear in the index bits).
 template <bool ACT_BF16>
 __device__ void column_bitmaps(const DevPlan& P, int lane, int ntok, int l, int nb, const int32_t* parents,
                                int pstride, int nparents, const ActTile& A, const uint32_t* nt, uint32_t* cw)
 {
-    const int CPT = P.cpt[l], TPW = P.wave_tokens, nchunk = P.nchunk;
-    const int ncol = TPW * CPT;
-    for (int e = lane; e < 16 * nchunk; e += 64) {
-        const int col = e / nchunk, w = e - col * nchunk;
-        const int r = nb * 16 + col, tt = r / CPT, q = r % CPT;
-        const int32_t p = (r < ncol && tt < ntok && q < nparents) ? parents[tt * pstride + q] : -1;
+    const int CPT = P.cpt[l], nchunk = P.nchunk;
+    const int col = lane & 15, r = nb * 16 + col, tt = r >> P.cpt_shift[l], q = r & (CPT - 1);
+    int32_t p = -1;
+    if (r < P.wave_tokens * CPT && tt < ntok && q < nparents) p = parents[tt * pstride + q];
+    // nibble table layout [g][w][16]: word w of group g for nibble value v at (g * nchunk + w) * 16 + v
+    const uint32_t* rows[8];
+#pragma unroll
+    for (int g = 0; g < 8; ++g) rows[g] = nt + g * nchunk * 16 + ((p >> (4 * g)) & 15);
+    const uint32_t* sw = A.signw + (p >= 0 ? tt : 0) * nchunk;
+    uint32_t* dst = cw + col * P.cws;
+    for (int w = lane >> 4; w < nchunk; w += 4) {
         uint32_t word = 0;
         if (p >= 0) {
-            word = bitmap_word(nt, P.nt_groups, nchunk, (uint32_t)p, w);
-            if constexpr (ACT_BF16) word ^= A.signw[tt * nchunk + w];
+#pragma unroll
+            for (int g = 0; g < 8; ++g)
+                if (g < P.nt_groups) word ^= rows[g][w * 16];
+            if constexpr (ACT_BF16) word ^= sw[w];
         }
-        cw[e] = word;
+        dst[w] = word;
     }
 }
 
@@ -63,7 +72,7 @@ __device__ f32x4 mfma_scores(const DevPlan& P, int lane, int l, int mb, bool val
         for (int e = 0; e < kScoreBatch; ++e) {
             const int c = c0 + e < nchunk ? c0 + e : nchunk - 1;
             a[e] = Ap[(int64_t)c * 64];
-            wd[e] = cw[col * nchunk + c];
+            wd[e] = cw[col * P.cws + c];
         }
 #pragma unroll
         for (int e = 0; e < kScoreBatch; ++e) {
@@ -107,26 +116,42 @@ __device__ f32x4 mfma_scores(const DevPlan& P, int lane, int l, int mb, bool val
 
 // Writes bf16 activations of `ntok` rows (row stride d elements) into the
 // paired layout and the sign words; rows >= ntok and coordinates >= d are 0.
+// Each lane reads 8 consecutive coordinates (one 16-byte load when d is a
+// multiple of 8) and scatters them as half-words.
 __device__ inline void load_pairs(const DevPlan& P, int lane, int ntok, int tpw, const uint16_t* src, int64_t row0,
                                   uint32_t* pairs, uint32_t* signw)
 {
     const int d = P.d, dp = P.dp, nchunk = P.nchunk;
-    for (int e = lane; e < tpw * (dp / 2); e += 64) {
-        const int tt = e / (dp / 2), r = e - tt * (dp / 2);
-        const int c = r >> 4, kq = (r >> 2) & 3, i = r & 3;
-        const int i0 = 32 * c + kq + 4 * i, i1 = i0 + 16;
+    uint16_t* ph = (uint16_t*)pairs;
+    const bool vec = (d & 7) == 0;
+    for (int tt = 0; tt < tpw; ++tt) {
         const bool live = tt < ntok;
-        const uint32_t v0 = (live && i0 < d) ? src[(row0 + tt) * d + i0] : 0u;
-        const uint32_t v1 = (live && i1 < d) ? src[(row0 + tt) * d + i1] : 0u;
-        pairs[e] = (v0 & 0x7FFFu) | ((v1 & 0x7FFFu) << 16);
-    }
-    for (int base = 0; base < tpw * dp; base += 64) {
-        const int e = base + lane, tt = e / dp, iota = e - tt * dp;
-        const bool neg = tt < ntok && iota < d && (src[(row0 + tt) * d + iota] & 0x8000u);
-        const uint64_t m = __ballot(neg);
-        if (lane == 0) {
-            signw[base / 32] = (uint32_t)m;
-            if (base / 32 + 1 < tpw * nchunk) signw[base / 32 + 1] = (uint32_t)(m >> 32);
+        const uint16_t* row = src + (row0 + tt) * d;
+        for (int o = lane * 8; o < dp; o += 512) {
+            uint32_t v[4] = {0u, 0u, 0u, 0u};
+            if (live && vec && o < d) {
+                const u32x4 q = *(const u32x4*)(row + o);
+                v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+            } else if (live) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    if (o + e < d) v[e >> 1] |= (uint32_t)row[o + e] << (16 * (e & 1));
+            }
+            // coordinate o + e sits at paired dword kq * 4 + i of chunk c, half h
+            const int c = o >> 5, base = o & 31;
+            uint32_t sg = 0;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const uint32_t h16 = (v[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
+                const int b = base + e, h = b >> 4, kq = b & 3, i = (b >> 2) & 3;
+                ph[(tt * (dp / 2) + c * 16 + kq * 4 + i) * 2 + h] = (uint16_t)(h16 & 0x7FFFu);
+                sg |= (h16 >> 15) << e;
+            }
+            // 8 sign bits of this lane -> bits base..base+7 of word c (4 lanes per word)
+            uint32_t part = sg << base;
+            part |= __shfl_xor(part, 1, 64);
+            part |= __shfl_xor(part, 2, 64);
+            if ((lane & 3) == 0) signw[tt * nchunk + c] = part;
         }
     }
 }
