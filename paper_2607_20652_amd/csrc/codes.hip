@@ -499,18 +499,18 @@ template <bool G_BF16>
 __device__ void score_level(const DevPlan& P, const Wave& W, int l)
 {
     const int k = P.k_tot, TPW = P.wave_tokens, lane = W.lane;
-    const int CPT = P.cpt[l], Kp = P.active[l - 1], Kl = P.active[l];
-    const int ncol = TPW * CPT, NB = (ncol + 15) / 16, sbp = P.slot_base[l - 1], sbl = P.slot_base[l];
+    const int CPT = P.cpt[l], csh = P.cpt_shift[l], Kp = P.active[l - 1], Kl = P.active[l];
+    const int ncol = TPW * CPT, NB = (ncol + 15) >> 4, sbp = P.slot_base[l - 1], sbl = P.slot_base[l];
     const ActTile A{W.pairs, W.signw, W.gf};
+    const int col = lane & 15, kq = lane >> 4;
     for (int nb = 0; nb < NB; ++nb) {
-        column_bitmaps<G_BF16>(P, lane, W.ntok, l, nb, W.idx + sbp, k, Kp, A, W.nt, W.cw);
+        column_bitmaps<G_BF16>(P, lane, W.ntok, csh, nb, W.idx + sbp, k, Kp, A, W.nt, W.cw);
         wave_sync();
-        const int col = lane & 15, kq = lane >> 4;
-        const int r = nb * 16 + col, tt = r / CPT, q = r % CPT;
+        const int r = nb * 16 + col, tt = r >> csh, q = r & (CPT - 1);
         const bool valid = r < ncol && tt < W.ntok && q < Kp && W.idx[tt * k + sbp + q] >= 0;
         const int trow = valid ? tt : 0;
         for (int mb = 0; mb < P.mblocks[l]; ++mb) {
-            const f32x4 acc = mfma_scores<G_BF16>(P, lane, l, mb, valid, trow, A, W.cw);
+            const f32x4 acc = mfma_scores<G_BF16>(P, lane, l, mb, trow, A, W.cw);
 #pragma unroll
             for (int i = 0; i < 4; ++i) W.score[col * 16 + kq * 4 + i] = acc[i] * P.rsd;
             wave_sync();
@@ -519,8 +519,8 @@ __device__ void score_level(const DevPlan& P, const Wave& W, int l)
                 for (int s = sbl + lane; s < sbl + Kl; s += 64) {
                     const int rt = W.route[tt2 * k + s];
                     if (rt < 0) continue;
-                    const int r2 = tt2 * CPT + (rt >> 16), j = rt & 0xFFFF;
-                    if (r2 / 16 == nb && j / 16 == mb) W.coef[tt2 * k + s] = W.score[(r2 - nb * 16) * 16 + (j & 15)];
+                    const int r2 = (tt2 << csh) + (rt >> 16), j = rt & 0xFFFF;
+                    if ((r2 >> 4) == nb && (j >> 4) == mb) W.coef[tt2 * k + s] = W.score[(r2 & 15) * 16 + (j & 15)];
                 }
             wave_sync();
         }

@@ -1,19 +1,23 @@
 // Encoder for gfx950: the top-down beam search of §2.2.
 //
-// A wave owns `wave_tokens` tokens; their activations stay in LDS in the
+// A wave owns `wave_tokens` tokens (16 / CPT, CPT = parent columns per
+// token rounded up to a power of two); their activations stay in LDS in the
 // paired layout of scoring.hpp.
 //
 //  * Level 0 (§2.1 Eq. 2: scoring a basis feature is a coordinate read):
 //    each token's lanes take the maximum key over their coordinates; the
 //    K_0-th largest lane maximum tau bounds the answer from below (the K_0
-//    largest lane maxima are distinct keys >= tau), so only keys >= tau --
-//    at most K_0 lanes' worth -- are ranked exactly.
+//    largest lane maxima are distinct keys >= tau), so only the few keys >= tau
+//    are ranked exactly.  With bf16 activations a key is 32 bits: the bf16
+//    magnitude above the complemented coordinate.
 //  * Levels l >= 1: the children of every active parent are scored on the
-//    matrix cores; the keys (|s| desc, index asc, see device_common.hpp) are
-//    sorted in registers by a bitonic network laid over the MFMA output
-//    layout; a child reached from several parents has bit-identical keys
-//    (same products, same reduction), so it appears as adjacent duplicates
-//    and is kept once; the first K_l survivors are emitted in order.
+//    matrix cores (§2.2 child-scoring equation); the 64-bit keys (|s| desc,
+//    index asc, see device_common.hpp) are sorted by a bitonic network laid
+//    over the MFMA output layout, unrolled at compile time, with DPP and
+//    swizzle lane exchanges; a child reached from several parents has
+//    bit-identical keys (same products, same reduction), so it appears as
+//    adjacent duplicates and is kept once; the first K_l survivors are emitted
+//    in order.
 #include <algorithm>
 
 #include "scoring.hpp"
@@ -25,7 +29,7 @@ constexpr int kEncWaves = 4;
 constexpr int kEncThreads = 64 * kEncWaves;
 
 struct EncLayout {
-    unsigned act, cw, par, list, bytes;
+    unsigned act, cw, par, list, cnt, bytes;
     int kmaxp;   // row stride of par
     int listn;   // keys per token in list
 };
@@ -48,10 +52,11 @@ __host__ __device__ inline EncLayout enc_layout(const DevPlan& P, bool act_bf16)
 {
     EncLayout L;
     const int TPW = P.wave_tokens, LPT = 64 / TPW;
-    const int U0 = (P.dp + LPT - 1) / LPT;
+    const int ND = (P.dp / 2 + LPT - 1) / LPT;  // activation dwords per lane at level 0
     const int R = enc_r(P);
-    int listn = P.active[0] * U0;
-    for (int l = 1; l < P.levels; ++l) listn = P.cpt[l] * 4 * R > listn ? P.cpt[l] * 4 * R : listn;
+    int listn = P.active[0] * 2 * ND;           // level-0 candidates: K_0 lanes with at most 2 ND keys each
+    if (act_bf16 == false && P.active[0] * ((P.d + LPT - 1) / LPT) > listn) listn = P.active[0] * ((P.d + LPT - 1) / LPT);
+    if (16 / TPW * 4 * R > listn) listn = 16 / TPW * 4 * R;
     L.listn = listn;
     L.kmaxp = P.kmax;
     unsigned off = 0;
@@ -60,96 +65,145 @@ __host__ __device__ inline EncLayout enc_layout(const DevPlan& P, bool act_bf16)
     L.cw = off;   off = align16u(off + 16 * P.cws * 4);
     L.par = off;  off = align16u(off + TPW * L.kmaxp * 4);
     L.list = off; off = align16u(off + TPW * listn * 8);
+    L.cnt = off;  off = align16u(off + TPW * 4);
     L.bytes = off;
     return L;
 }
 
 __host__ __device__ inline unsigned enc_shared_bytes(const DevPlan& P)
 {
-    return align16u(P.dp * 4) + align16u(P.nt_groups * 16 * P.nchunk * 4);
+    return align16u(P.nt_groups * 16 * P.nchunk * 4) + align16u(P.gens_total * 4);
 }
 
-__device__ __forceinline__ uint64_t shfl_xor64(uint64_t v, int mask)
+// Exchange with the lane whose index differs by m (a power of two): DPP for
+// 1 and 2, swizzles up to 16, a permute for 32.
+__device__ __forceinline__ uint32_t xlane(uint32_t v, int m, int x32addr)
 {
-    const uint32_t hi = (uint32_t)__shfl_xor((int)(v >> 32), mask, 64);
-    const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, mask, 64);
-    return ((uint64_t)hi << 32) | lo;
+    switch (m) {
+    case 1: return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);
+    case 2: return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);
+    case 4: return swz_xor<4>(v);
+    case 8: return swz_xor<8>(v);
+    case 16: return swz_xor<16>(v);
+    default: return (uint32_t)__builtin_amdgcn_ds_bpermute(x32addr, (int)v);
+    }
 }
 
-__device__ __forceinline__ uint64_t shfl64(uint64_t v, int src)
+__device__ __forceinline__ uint64_t xlane64(uint64_t v, int m, int x32addr)
+{
+    return ((uint64_t)xlane((uint32_t)(v >> 32), m, x32addr) << 32) | xlane((uint32_t)v, m, x32addr);
+}
+
+template <typename K>
+__device__ __forceinline__ K xlaneK(K v, int m, int x32addr)
+{
+    if constexpr (sizeof(K) == 8) return xlane64(v, m, x32addr);
+    else return xlane(v, m, x32addr);
+}
+
+__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src)
 {
     const uint32_t hi = (uint32_t)__shfl((int)(v >> 32), src, 64);
     const uint32_t lo = (uint32_t)__shfl((int)(uint32_t)v, src, 64);
     return ((uint64_t)hi << 32) | lo;
 }
 
-// Descending bitonic sort of one token's keys: element e = lanepos * R + r
-// lives in register r of the lane whose position is lanepos.  Bits of lanepos
-// map to lane bits through `lane_xor(b)`.  nbits = log2(R) + bits of lanepos.
-template <int R, typename LaneXor>
-__device__ void bitonic_desc(uint64_t (&v)[R], int lanepos, int nbits, LaneXor lane_xor)
+// Descending bitonic sort of one token's R * 2^NB keys: element e =
+// lanepos * R + r lives in register r of the lane at position lanepos.  In
+// the MFMA layout lanepos = q * 4 + kq (q = lane bits 0.., kq = lane bits
+// 4, 5); otherwise lanepos bit b is lane bit b.  Every loop is unrolled, so
+// the exchange pattern and the in-lane directions are compile-time constants.
+template <int R, int NB, bool MFMA_LAYOUT, typename K>
+__device__ __forceinline__ void sort_desc(K (&v)[R], int lanepos, int x32addr)
 {
-    constexpr int LR = R == 4 ? 2 : R == 8 ? 3 : R == 16 ? 4 : R == 2 ? 1 : 0;
-    for (int ks = 1; ks <= nbits; ++ks) {
-        const int k = 1 << ks;
+    constexpr int LR = R == 1 ? 0 : R == 2 ? 1 : R == 4 ? 2 : R == 8 ? 3 : 4;
+#pragma unroll
+    for (int ks = 1; ks <= LR + NB; ++ks) {
+#pragma unroll
         for (int js = ks - 1; js >= 0; --js) {
-            const int j = 1 << js;
             if (js >= LR) {
-                const int m = lane_xor(js - LR);
+                const int b = js - LR;
+                const int m = MFMA_LAYOUT ? (b < 2 ? (16 << b) : (1 << (b - 2))) : (1 << b);
+                const bool up = (ks - LR < NB) && ((lanepos >> (ks - LR)) & 1);
+                const bool lower = !((lanepos >> b) & 1);
+                const bool tmax = lower != up;
 #pragma unroll
                 for (int r = 0; r < R; ++r) {
-                    const uint64_t o = shfl_xor64(v[r], m);
-                    const int e = lanepos * R + r;
-                    const bool take_max = ((e & j) == 0) == ((e & k) == 0);
-                    v[r] = take_max ? (o > v[r] ? o : v[r]) : (o < v[r] ? o : v[r]);
+                    const K o = xlaneK(v[r], m, x32addr);
+                    const bool gt = o > v[r];
+                    v[r] = (gt == tmax) ? o : v[r];
                 }
             } else {
+                const int j = 1 << js;
 #pragma unroll
-                for (int jj = 1; jj < R; jj <<= 1) {
-                    if (jj != j) continue;
-#pragma unroll
-                    for (int r = 0; r < R; ++r) {
-                        if (r & jj) continue;
-                        const bool desc = ((lanepos * R + r) & k) == 0;
-                        const uint64_t a = v[r], b = v[r | jj];
-                        const bool sw = desc ? (a < b) : (a > b);
-                        v[r] = sw ? b : a;
-                        v[r | jj] = sw ? a : b;
-                    }
+                for (int r = 0; r < R; ++r) {
+                    if (r & j) continue;
+                    const bool up = (ks < LR) ? ((r >> ks) & 1) : ((ks - LR < NB) && ((lanepos >> (ks - LR)) & 1));
+                    const K a = v[r], c = v[r | j];
+                    const bool sw = up ? (a > c) : (a < c);
+                    v[r] = sw ? c : a;
+                    v[r | j] = sw ? a : c;
                 }
             }
         }
     }
 }
 
+// Exclusive prefix and total of per-lane counts (0..31) over the LPT lanes
+// of a token group (lanes tt*LPT .. tt*LPT + LPT - 1).
+template <int LPT>
+__device__ __forceinline__ void group_scan(int lane, int cnt, int& before, int& total)
+{
+    const uint64_t grp = LPT == 64 ? ~0ull : (((1ull << LPT) - 1ull) << (lane & ~(LPT - 1)));
+    const uint64_t lower = (1ull << lane) - 1ull;
+    before = 0;
+    total = 0;
+#pragma unroll
+    for (int b = 0; b < 5; ++b) {
+        const uint64_t m = __ballot((cnt >> b) & 1) & grp;
+        before += (int)__popcll(m & lower) << b;
+        total += (int)__popcll(m) << b;
+    }
+}
+
 // Emits the first K distinct keys of each token's sorted list (duplicates are
 // adjacent) to slots [sb, sb + K), and records them as the next parents.
-__device__ void emit_level(const DevPlan& P, int lane, int64_t t0, int ntok, const uint64_t* list, int listn, int n,
-                           int K, int sb, int32_t* par, int kmaxp, int32_t* out_idx, float* out_coef)
+// Lane li of the token handles sorted positions li*R .. li*R + R - 1.
+template <int R, int LPT>
+__device__ void emit_sorted(const DevPlan& P, int lane, int64_t t0, int ntok, const uint64_t* list, int listn,
+                            int K, int sb, int32_t* par, int kmaxp, int32_t* out_idx, float* out_coef)
 {
-    const int TPW = P.wave_tokens, LPT = 64 / TPW, tt = lane / LPT, li = lane % LPT, k_tot = P.k_tot;
-    const uint64_t block = LPT == 64 ? ~0ull : (((1ull << LPT) - 1ull) << (tt * LPT));
+    const int tt = lane / LPT, li = lane & (LPT - 1), k_tot = P.k_tot;
+    const uint64_t* row = list + tt * listn + li * R;
+    uint64_t key[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) key[r] = row[r];
+    uint64_t prev = li > 0 ? row[-1] : 0ull;
+    int kept = 0, cnt = 0;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const bool k = key[r] != 0ull && key[r] != prev;
+        kept |= (int)k << r;
+        cnt += (int)k;
+        prev = key[r];
+    }
+    int before, total;
+    group_scan<LPT>(lane, cnt, before, total);
     const bool live = tt < ntok;
-    const uint64_t* row = list + tt * listn;
-    int count = 0;
-    for (int e0 = 0; e0 < n; e0 += LPT) {
-        const int e = e0 + li;
-        const uint64_t key = e < n ? row[e] : 0ull;
-        const uint64_t prev = (e > 0 && e < n) ? row[e - 1] : 0ull;
-        const bool kept = key != 0ull && key != prev;
-        const uint64_t m = __ballot(kept) & block;
-        const int rank = count + __popcll(m & ((1ull << lane) - 1ull));
-        if (kept && rank < K) {
-            const uint32_t ci = key_index(key);
+    int rank = before;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        if (((kept >> r) & 1) && rank < K) {
+            const uint32_t ci = key_index(key[r]);
             par[tt * kmaxp + rank] = (int32_t)ci;
             if (live) {
                 out_idx[(t0 + tt) * k_tot + sb + rank] = (int32_t)ci;
-                out_coef[(t0 + tt) * k_tot + sb + rank] = key_value(key);
+                out_coef[(t0 + tt) * k_tot + sb + rank] = key_value(key[r]);
             }
         }
-        count += __popcll(m);
+        rank += (kept >> r) & 1;
     }
-    for (int r = count + li; r < K; r += LPT) {
+    for (int r = total + li; r < K; r += LPT) {
         par[tt * kmaxp + r] = -1;
         if (live) {
             out_idx[(t0 + tt) * k_tot + sb + r] = -1;
@@ -158,23 +212,119 @@ __device__ void emit_level(const DevPlan& P, int lane, int64_t t0, int ntok, con
     }
 }
 
-template <bool X_BF16, int R>
-__global__ __launch_bounds__(kEncThreads) void encode2_kernel(DevPlan P, const void* __restrict__ xin, int64_t T,
+// Level 0, bf16 activations: 32-bit keys (|x| bf16 bits << 16 | 0xFFFF - iota).
+// Lane li of token tt reads the paired dwords e = li + LPT m; dword e holds
+// coordinates 32 (e >> 4) + ((e >> 2) & 3) + 4 (e & 3) and that + 16.
+// Coordinates past d hold zeros, so their keys sort below every real key.
+template <int LPT, int LLP>
+__device__ void level0_bf16(const DevPlan& P, int lane, int64_t t0, int ntok, const uint32_t* pairs,
+                            const uint32_t* signw, uint64_t* list, int listn, int* cnt, int32_t* par, int kmaxp,
+                            int32_t* out_idx, float* out_coef, int x32addr)
+{
+    const int tt = lane >> LLP, li = lane & (LPT - 1), K0 = P.active[0], dp2 = P.dp / 2;
+    const uint32_t* row = pairs + tt * dp2;
+    const int lo0 = 32 * (li >> 4) + ((li >> 2) & 3) + 4 * (li & 3);  // coordinate of dword li (low half)
+    constexpr uint32_t STEP = 2 * LPT;                                 // coordinate step per dword row
+    uint32_t best = 0;
+    {
+        uint32_t c = 0xFFFFu - (uint32_t)lo0;
+        for (int e = li; e < dp2; e += LPT, c -= STEP) {
+            const uint32_t D = row[e];
+            const uint32_t klo = (D << 16) | c, khi = (D & 0xFFFF0000u) | (c - 16u);
+            best = max(best, max(klo, khi));
+        }
+    }
+    uint32_t sv[1] = {best};
+    sort_desc<1, LLP, false>(sv, li, x32addr);
+    const uint32_t tau = (uint32_t)__shfl((int)sv[0], (lane & ~(LPT - 1)) + K0 - 1, 64);
+    if (li == 0) cnt[tt] = 0;
+    wave_sync();
+    uint32_t* lst = (uint32_t*)(list + tt * listn);
+    {
+        uint32_t c = 0xFFFFu - (uint32_t)lo0;
+        for (int e = li; e < dp2; e += LPT, c -= STEP) {
+            const uint32_t D = row[e];
+            const uint32_t klo = (D << 16) | c, khi = (D & 0xFFFF0000u) | (c - 16u);
+            if (klo >= tau) lst[atomicAdd(&cnt[tt], 1)] = klo;
+            if (khi >= tau) lst[atomicAdd(&cnt[tt], 1)] = khi;
+        }
+    }
+    wave_sync();
+    const int n = cnt[tt];
+    const bool live = tt < ntok;
+    for (int e = li; e < n; e += LPT) {
+        const uint32_t ke = lst[e];
+        int rank = 0;
+        for (int f = 0; f < n; ++f) rank += lst[f] > ke;
+        if (rank < K0) {
+            const uint32_t iota = 0xFFFFu - (ke & 0xFFFFu);
+            par[tt * kmaxp + rank] = (int32_t)iota;
+            if (live) {
+                const uint32_t sg = (signw[tt * P.nchunk + (iota >> 5)] >> (iota & 31)) & 1u;
+                out_idx[(t0 + tt) * P.k_tot + rank] = (int32_t)iota;
+                out_coef[(t0 + tt) * P.k_tot + rank] = __uint_as_float(((ke >> 16) | (sg << 15)) << 16);
+            }
+        }
+    }
+}
+
+// Level 0, fp32 activations: 64-bit keys over natural-order coordinates.
+template <int LPT, int LLP>
+__device__ void level0_f32(const DevPlan& P, int lane, int64_t t0, int ntok, const float* xf, uint64_t* list,
+                           int listn, int* cnt, int32_t* par, int kmaxp, int32_t* out_idx, float* out_coef,
+                           int x32addr)
+{
+    const int tt = lane >> LLP, li = lane & (LPT - 1), K0 = P.active[0], d = P.d, dp = P.dp;
+    const float* row = xf + tt * dp;
+    uint64_t best = 0;
+    for (int iota = li; iota < d; iota += LPT) best = max(best, make_key(row[iota], (uint32_t)iota));
+    uint64_t sv[1] = {best};
+    sort_desc<1, LLP, false>(sv, li, x32addr);
+    const uint64_t tau = shfl_u64(sv[0], (lane & ~(LPT - 1)) + K0 - 1);
+    if (li == 0) cnt[tt] = 0;
+    wave_sync();
+    uint64_t* lst = list + tt * listn;
+    for (int iota = li; iota < d; iota += LPT) {
+        const uint64_t kk = make_key(row[iota], (uint32_t)iota);
+        if (kk >= tau) lst[atomicAdd(&cnt[tt], 1)] = kk;
+    }
+    wave_sync();
+    const int n = cnt[tt];
+    const bool live = tt < ntok;
+    for (int e = li; e < n; e += LPT) {
+        const uint64_t ke = lst[e];
+        int rank = 0;
+        for (int f = 0; f < n; ++f) rank += lst[f] > ke;
+        if (rank < K0) {
+            const uint32_t iota = key_index(ke);
+            par[tt * kmaxp + rank] = (int32_t)iota;
+            if (live) {
+                out_idx[(t0 + tt) * P.k_tot + rank] = (int32_t)iota;
+                out_coef[(t0 + tt) * P.k_tot + rank] = key_value(ke);
+            }
+        }
+    }
+}
+
+template <bool X_BF16, int CPT, int R>
+__global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const void* __restrict__ xin, int64_t T,
                                                               int32_t* __restrict__ out_idx,
                                                               float* __restrict__ out_coef)
 {
+    constexpr int TPW = 16 / CPT, LPT = 64 / TPW;
+    constexpr int CB = CPT == 4 ? 2 : CPT == 8 ? 3 : 4;  // log2 CPT
+    constexpr int NB = CB + 2;                            // lane bits of a token in the MFMA layout
+    constexpr int LLP = LPT == 16 ? 4 : LPT == 32 ? 5 : 6;
     extern __shared__ __align__(16) unsigned char smem[];
-    {
-        uint32_t* s_mask = (uint32_t*)smem;
-        uint32_t* s_nt = (uint32_t*)(smem + align16u(P.dp * 4));
-        for (int i = threadIdx.x; i < P.dp; i += kEncThreads) s_mask[i] = P.masks[i];
-        for (int i = threadIdx.x; i < P.nt_groups * 16 * P.nchunk; i += kEncThreads) s_nt[i] = P.nt[i];
-    }
+    uint32_t* s_nt = (uint32_t*)smem;
+    uint32_t* s_gens = (uint32_t*)(smem + align16u(P.nt_groups * 16 * P.nchunk * 4));
+    for (int i = threadIdx.x; i < P.nt_groups * 16 * P.nchunk; i += kEncThreads) s_nt[i] = P.nt[i];
+    for (int i = threadIdx.x; i < P.gens_total; i += kEncThreads) s_gens[i] = P.gens[i];
     __syncthreads();
-    const uint32_t* s_nt = (const uint32_t*)(smem + align16u(P.dp * 4));
 
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int TPW = P.wave_tokens, LPT = 64 / TPW, d = P.d, dp = P.dp, nchunk = P.nchunk;
+    const int d = P.d, dp = P.dp;
+    const int x32 = (lane ^ 32) << 2;
     const EncLayout EL = enc_layout(P, X_BF16);
     unsigned char* wb = smem + enc_shared_bytes(P) + (unsigned)wave * EL.bytes;
     uint32_t* pairs = (uint32_t*)(wb + EL.act);
@@ -183,7 +333,10 @@ __global__ __launch_bounds__(kEncThreads) void encode2_kernel(DevPlan P, const v
     uint32_t* cw = (uint32_t*)(wb + EL.cw);
     int32_t* par = (int32_t*)(wb + EL.par);
     uint64_t* list = (uint64_t*)(wb + EL.list);
+    int* cnt = (int*)(wb + EL.cnt);
     const ActTile A{pairs, signw, xf};
+
+    const int col = lane & 15, kq = lane >> 4, ct = col >> CB, q = col & (CPT - 1), lanepos = q * 4 + kq;
 
     const int64_t ngroups = (T + TPW - 1) / TPW;
     for (int64_t grp = (int64_t)blockIdx.x * kEncWaves + wave; grp < ngroups;
@@ -195,105 +348,49 @@ __global__ __launch_bounds__(kEncThreads) void encode2_kernel(DevPlan P, const v
             load_pairs(P, lane, ntok, TPW, (const uint16_t*)xin, t0, pairs, signw);
         } else {
             const float* xs = (const float*)xin;
-            for (int e = lane; e < TPW * dp; e += 64) {
-                const int tt = e / dp, iota = e - tt * dp;
-                xf[e] = (tt < ntok && iota < d) ? xs[(t0 + tt) * d + iota] : 0.f;
-            }
+            for (int tt = 0; tt < TPW; ++tt)
+                for (int iota = lane; iota < dp; iota += 64)
+                    xf[tt * dp + iota] = (tt < ntok && iota < d) ? xs[(t0 + tt) * d + iota] : 0.f;
         }
         wave_sync();
 
         // ---- level 0
-        {
-            const int tt = lane / LPT, li = lane % LPT, K0 = P.active[0];
-            const int U0 = (dp + LPT - 1) / LPT;
-            const bool live = tt < ntok;
-            auto key0 = [&](int u) -> uint64_t {
-                const int iota = li + LPT * u;
-                if (!live || iota >= d) return 0ull;
-                float v;
-                if constexpr (X_BF16) v = pair_value(P, pairs, signw, tt, iota);
-                else v = xf[tt * dp + iota];
-                return make_key(v, (uint32_t)iota);
-            };
-            uint64_t best = 0;
-            for (int u = 0; u < U0; ++u) {
-                const uint64_t kk = key0(u);
-                best = kk > best ? kk : best;
-            }
-            // the K0-th largest lane maximum of the token
-            uint64_t sv[1] = {best};
-            int lb = 0;
-            while ((1 << lb) < LPT) ++lb;
-            bitonic_desc<1>(sv, li, lb, [](int b) { return 1 << b; });
-            const uint64_t tau = shfl64(sv[0], tt * LPT + K0 - 1);
-            int cnt = 0;
-            for (int u = 0; u < U0; ++u) cnt += key0(u) >= tau && tau != 0ull;
-            int incl = cnt;
-            for (int off = 1; off < LPT; off <<= 1) {
-                const int o = __shfl_up(incl, off, LPT);
-                if (li >= off) incl += o;
-            }
-            const int total = __shfl(incl, tt * LPT + LPT - 1, 64);
-            int pos = incl - cnt;
-            uint64_t* row = list + tt * EL.listn;
-            for (int u = 0; u < U0; ++u) {
-                const uint64_t kk = key0(u);
-                if (kk >= tau && tau != 0ull) row[pos++] = kk;
-            }
-            wave_sync();
-            for (int e = li; e < total; e += LPT) {
-                const uint64_t ke = row[e];
-                int rank = 0;
-                for (int f = 0; f < total; ++f) rank += row[f] > ke;
-                if (rank < K0) {
-                    const uint32_t iota = key_index(ke);
-                    par[tt * EL.kmaxp + rank] = (int32_t)iota;
-                    if (live) {
-                        out_idx[(t0 + tt) * P.k_tot + rank] = (int32_t)iota;
-                        out_coef[(t0 + tt) * P.k_tot + rank] = key_value(ke);
-                    }
-                }
-            }
-            for (int r = total + li; r < K0; r += LPT) par[tt * EL.kmaxp + r] = -1;
-            wave_sync();
-        }
+        if constexpr (X_BF16)
+            level0_bf16<LPT, LLP>(P, lane, t0, ntok, pairs, signw, list, EL.listn, cnt, par, EL.kmaxp, out_idx,
+                                  out_coef, x32);
+        else
+            level0_f32<LPT, LLP>(P, lane, t0, ntok, xf, list, EL.listn, cnt, par, EL.kmaxp, out_idx, out_coef, x32);
+        wave_sync();
 
         // ---- levels l >= 1
         for (int l = 1; l < P.levels; ++l) {
-            const int CPT = P.cpt[l], Kp = P.active[l - 1], Dl = P.delta[l];
-            column_bitmaps<X_BF16>(P, lane, ntok, l, 0, par, EL.kmaxp, Kp, A, s_nt, cw);
+            const int Kp = P.active[l - 1], Dl = P.delta[l];
+            column_bitmaps<X_BF16>(P, lane, ntok, CB, 0, par, EL.kmaxp, Kp, A, s_nt, cw);
             wave_sync();
-            const int col = lane & 15, kq = lane >> 4;
-            const int tt = col / CPT, q = col % CPT;
-            const int32_t p = (col < TPW * CPT && tt < ntok && q < Kp) ? par[tt * EL.kmaxp + q] : -1;
+            const int32_t p = (ct < ntok && q < Kp) ? par[ct * EL.kmaxp + q] : -1;
             const bool valid = p >= 0;
-            const int trow = valid ? tt : 0;
-            const uint32_t* gens = P.gens + P.gens_off[l];
+            const int trow = valid ? ct : 0;
+            const uint32_t* gens = s_gens + P.gens_off[l];
             uint64_t keys[R];
 #pragma unroll
             for (int mb = 0; mb < R / 4; ++mb) {
                 f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-                if (mb < P.mblocks[l]) acc = mfma_scores<X_BF16>(P, lane, l, mb, valid, trow, A, cw);
+                if (mb < P.mblocks[l]) acc = mfma_scores<X_BF16>(P, lane, l, mb, trow, A, cw);
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int j = 16 * mb + 4 * kq + i;
-                    keys[4 * mb + i] =
-                        (valid && j < Dl) ? make_key(acc[i] * P.rsd, (uint32_t)p ^ gens[j]) : 0ull;
+                    keys[4 * mb + i] = (valid && j < Dl) ? make_key(acc[i] * P.rsd, (uint32_t)p ^ gens[j]) : 0ull;
                 }
             }
-            int cb = 0;
-            while ((1 << cb) < CPT) ++cb;
-            const int lanepos = q * 4 + kq;
-            int lr = 0;
-            while ((1 << lr) < R) ++lr;
-            bitonic_desc<R>(keys, lanepos, lr + 2 + cb, [](int b) { return b < 2 ? (16 << b) : (1 << (b - 2)); });
-            if (col < TPW * CPT) {
+            sort_desc<R, NB, true>(keys, lanepos, x32);
+            {
+                uint64_t* dst = list + ct * EL.listn + lanepos * R;
 #pragma unroll
-                for (int r = 0; r < R; ++r) list[tt * EL.listn + lanepos * R + r] = keys[r];
+                for (int r = 0; r < R; ++r) dst[r] = keys[r];
             }
             wave_sync();
-            emit_level(P, lane, t0, ntok, list, EL.listn, CPT * 4 * R, P.active[l], P.slot_base[l], par, EL.kmaxp,
-                       out_idx, out_coef);
+            emit_sorted<R, LPT>(P, lane, t0, ntok, list, EL.listn, P.active[l], P.slot_base[l], par, EL.kmaxp,
+                                out_idx, out_coef);
             wave_sync();
         }
     }
@@ -304,9 +401,10 @@ __global__ __launch_bounds__(kEncThreads) void encode2_kernel(DevPlan P, const v
 bool encode2_supported(const DevPlan& P)
 {
     const int TPW = P.wave_tokens, LPT = 64 / TPW;
-    if (P.active[0] > LPT || enc_r(P) > 16) return false;
+    if (P.active[0] > LPT || enc_r(P) > 16 || P.d > 65535) return false;
     for (int l = 1; l < P.levels; ++l)
         if (P.cpt[l] > 16 || TPW * P.cpt[l] > 16) return false;
+    if (16 / TPW != 4 && 16 / TPW != 8 && 16 / TPW != 16) return false;
     const size_t lds = enc_shared_bytes(P) + (size_t)kEncWaves * enc_layout(P, false).bytes;
     return lds <= (size_t)kLdsBudget;
 }
@@ -323,21 +421,28 @@ hipError_t launch_encode2(const DevPlan& P, const void* x, bool x_bf16, int64_t 
         cus = prop.multiProcessorCount;
     const int per_cu = (int)std::max<size_t>(1, (160 * 1024) / std::max<size_t>(lds, 1));
     const dim3 grid((unsigned)std::max<int64_t>(1, std::min<int64_t>(need, (int64_t)cus * std::min(per_cu, 8) * 4)));
-    const int R = enc_r(P);
-#define DPB_ENC(XB, RV)                                                                                       \
-    do {                                                                                                      \
-        allow_lds(encode2_kernel<XB, RV>, lds);                                                               \
-        hipLaunchKernelGGL((encode2_kernel<XB, RV>), grid, dim3(kEncThreads), lds, stream, P, x, T, idx, coef); \
+    const int R = enc_r(P), CPT = 16 / P.wave_tokens;
+#define DPB_ENC(XB, CV, RV)                                                                                       \
+    do {                                                                                                          \
+        allow_lds(encode3_kernel<XB, CV, RV>, lds);                                                               \
+        hipLaunchKernelGGL((encode3_kernel<XB, CV, RV>), grid, dim3(kEncThreads), lds, stream, P, x, T, idx, coef); \
+    } while (0)
+#define DPB_ENC_R(XB, CV)                    \
+    do {                                     \
+        if (R == 4) DPB_ENC(XB, CV, 4);      \
+        else if (R == 8) DPB_ENC(XB, CV, 8); \
+        else DPB_ENC(XB, CV, 16);            \
     } while (0)
     if (x_bf16) {
-        if (R == 4) DPB_ENC(true, 4);
-        else if (R == 8) DPB_ENC(true, 8);
-        else DPB_ENC(true, 16);
+        if (CPT == 4) DPB_ENC_R(true, 4);
+        else if (CPT == 8) DPB_ENC_R(true, 8);
+        else DPB_ENC_R(true, 16);
     } else {
-        if (R == 4) DPB_ENC(false, 4);
-        else if (R == 8) DPB_ENC(false, 8);
-        else DPB_ENC(false, 16);
+        if (CPT == 4) DPB_ENC_R(false, 4);
+        else if (CPT == 8) DPB_ENC_R(false, 8);
+        else DPB_ENC_R(false, 16);
     }
+#undef DPB_ENC_R
 #undef DPB_ENC
     return hipGetLastError();
 }

@@ -25,19 +25,20 @@ struct ActTile {
     const float* f;         // fp32: [TPW][dp]
 };
 
-// Sign bitmaps of the 16 columns of block nb at level l into cw[16][cws];
-// for bf16 activations the activation signs are folded in.  Column r has
-// parent parents[tt * pstride + q] when q < nparents and tt < ntok.  Lane
+// Sign bitmaps of the 16 columns of block nb into cw[16][cws]; for bf16
+// activations the activation signs are folded in.  Column r is parent slot
+// q = r mod 2^csh of token tt = r / 2^csh, with parent parents[tt * pstride + q]
+// when q < nparents and tt < ntok.  Lane
 // (col, w0) builds words w0, w0 + 4, ... of column col: one nibble-table row
 // per 4-bit group of the parent index (parity is linear in the index bits).
 template <bool ACT_BF16>
-__device__ void column_bitmaps(const DevPlan& P, int lane, int ntok, int l, int nb, const int32_t* parents,
+__device__ void column_bitmaps(const DevPlan& P, int lane, int ntok, int csh, int nb, const int32_t* parents,
                                int pstride, int nparents, const ActTile& A, const uint32_t* nt, uint32_t* cw)
 {
-    const int CPT = P.cpt[l], nchunk = P.nchunk;
-    const int col = lane & 15, r = nb * 16 + col, tt = r >> P.cpt_shift[l], q = r & (CPT - 1);
+    const int nchunk = P.nchunk;
+    const int col = lane & 15, r = nb * 16 + col, tt = r >> csh, q = r & ((1 << csh) - 1);
     int32_t p = -1;
-    if (r < P.wave_tokens * CPT && tt < ntok && q < nparents) p = parents[tt * pstride + q];
+    if (r < (P.wave_tokens << csh) && tt < ntok && q < nparents) p = parents[tt * pstride + q];
     // nibble table layout [g][w][16]: word w of group g for nibble value v at (g * nchunk + w) * 16 + v
     const uint32_t* rows[8];
 #pragma unroll
@@ -57,60 +58,62 @@ __device__ void column_bitmaps(const DevPlan& P, int lane, int ntok, int l, int 
 }
 
 // Unscaled scores of generator tile mb for this lane's column (lane & 15):
-// acc[i] = S[16*mb + 4*(lane>>4) + i][column].  `valid` false gives zeros.
+// acc[i] = S[16*mb + 4*(lane>>4) + i][column].  Columns without a parent
+// produce scores of row trow that the callers discard.
 template <bool ACT_BF16>
-__device__ f32x4 mfma_scores(const DevPlan& P, int lane, int l, int mb, bool valid, int trow, const ActTile& A,
-                             const uint32_t* cw)
+__device__ __forceinline__ void score_chunk(const DevPlan& P, int kq, u32x4 a, uint32_t wd, const uint32_t* prow,
+                                            const float* frow, int c, f32x4& acc)
+{
+    const bf16x8 av = __builtin_bit_cast(bf16x8, a);
+    if constexpr (ACT_BF16) {
+        const uint32_t R = rotl32(wd, 15u - (uint32_t)kq);
+        const u32x4 pd = *(const u32x4*)(prow + c * 16);
+        u32x4 b;
+        b.x = (R & 0x80008000u) | pd.x;
+        b.y = (__builtin_amdgcn_alignbit(R, R, 4) & 0x80008000u) | pd.y;
+        b.z = (__builtin_amdgcn_alignbit(R, R, 8) & 0x80008000u) | pd.z;
+        b.w = (__builtin_amdgcn_alignbit(R, R, 12) & 0x80008000u) | pd.w;
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
+    } else {
+        uint32_t hi[8], mi[8], lo[8];
+#pragma unroll
+        for (int x = 0; x < 8; ++x) {
+            const int off = kq + 4 * (x >> 1) + 16 * (x & 1);
+            float v = frow[32 * c + off];
+            v = __uint_as_float(__float_as_uint(v) ^ (((wd >> off) & 1u) << 31));
+            split3(v, hi[x], mi[x], lo[x]);
+        }
+        const u32x4 bh = {hi[0] | (hi[1] << 16), hi[2] | (hi[3] << 16), hi[4] | (hi[5] << 16), hi[6] | (hi[7] << 16)};
+        const u32x4 bm = {mi[0] | (mi[1] << 16), mi[2] | (mi[3] << 16), mi[4] | (mi[5] << 16), mi[6] | (mi[7] << 16)};
+        const u32x4 bl = {lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16), lo[4] | (lo[5] << 16), lo[6] | (lo[7] << 16)};
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, bh), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, bm), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, bl), acc, 0, 0, 0);
+    }
+}
+
+template <bool ACT_BF16>
+__device__ f32x4 mfma_scores(const DevPlan& P, int lane, int l, int mb, int trow, const ActTile& A, const uint32_t* cw)
 {
     const int nchunk = P.nchunk, dp = P.dp, col = lane & 15, kq = lane >> 4;
     const u32x4* Ap = (const u32x4*)P.gamma_pair + P.gamma_off[l] + (int64_t)mb * nchunk * 64 + lane;
+    const uint32_t* cwp = cw + col * P.cws;
+    const uint32_t* prow = A.pairs + trow * (dp / 2) + kq * 4;
+    const float* frow = A.f + trow * dp;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int c0 = 0; c0 < nchunk; c0 += kScoreBatch) {
+    int c0 = 0;
+    for (; c0 + kScoreBatch <= nchunk; c0 += kScoreBatch) {
         u32x4 a[kScoreBatch];
         uint32_t wd[kScoreBatch];
 #pragma unroll
         for (int e = 0; e < kScoreBatch; ++e) {
-            const int c = c0 + e < nchunk ? c0 + e : nchunk - 1;
-            a[e] = Ap[(int64_t)c * 64];
-            wd[e] = cw[col * P.cws + c];
+            a[e] = Ap[(int64_t)(c0 + e) * 64];
+            wd[e] = cwp[c0 + e];
         }
 #pragma unroll
-        for (int e = 0; e < kScoreBatch; ++e) {
-            if (c0 + e >= nchunk) break;
-            const int c = c0 + e;
-            const bf16x8 av = __builtin_bit_cast(bf16x8, a[e]);
-            if constexpr (ACT_BF16) {
-                const uint32_t R = rotl32(wd[e], 15u - (uint32_t)kq);
-                const u32x4 pd = *(const u32x4*)(A.pairs + trow * (dp / 2) + c * 16 + kq * 4);
-                u32x4 b;
-                b.x = (R & 0x80008000u) | pd.x;
-                b.y = (__builtin_amdgcn_alignbit(R, R, 4) & 0x80008000u) | pd.y;
-                b.z = (__builtin_amdgcn_alignbit(R, R, 8) & 0x80008000u) | pd.z;
-                b.w = (__builtin_amdgcn_alignbit(R, R, 12) & 0x80008000u) | pd.w;
-                if (!valid) b = (u32x4){0u, 0u, 0u, 0u};
-                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
-            } else {
-                uint32_t hi[8], mi[8], lo[8];
-#pragma unroll
-                for (int x = 0; x < 8; ++x) {
-                    const int off = kq + 4 * (x >> 1) + 16 * (x & 1);
-                    float v = A.f[trow * dp + 32 * c + off];
-                    v = __uint_as_float(__float_as_uint(v) ^ (((wd[e] >> off) & 1u) << 31));
-                    if (!valid) v = 0.f;
-                    split3(v, hi[x], mi[x], lo[x]);
-                }
-                const u32x4 bh = {hi[0] | (hi[1] << 16), hi[2] | (hi[3] << 16), hi[4] | (hi[5] << 16),
-                                  hi[6] | (hi[7] << 16)};
-                const u32x4 bm = {mi[0] | (mi[1] << 16), mi[2] | (mi[3] << 16), mi[4] | (mi[5] << 16),
-                                  mi[6] | (mi[7] << 16)};
-                const u32x4 bl = {lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16), lo[4] | (lo[5] << 16),
-                                  lo[6] | (lo[7] << 16)};
-                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, bh), acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, bm), acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, bl), acc, 0, 0, 0);
-            }
-        }
+        for (int e = 0; e < kScoreBatch; ++e) score_chunk<ACT_BF16>(P, kq, a[e], wd[e], prow, frow, c0 + e, acc);
     }
+    for (; c0 < nchunk; ++c0) score_chunk<ACT_BF16>(P, kq, Ap[(int64_t)c0 * 64], cwp[c0], prow, frow, c0, acc);
     return acc;
 }
 
