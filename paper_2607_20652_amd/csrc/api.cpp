@@ -98,38 +98,63 @@ dpb_status fill_plan(dpb_plan* plan, const Hierarchy& h, const uint32_t* gens, u
         P.pb_bytes = (L >= 2 && h.active[L - 2] > 8) ? 2 : 1;
     }
 
-    // generator hash tables: load factor <= 1/4
+    // generator hash tables: a collision-free hash h(x) = (x ^ (x >> r)) & (2^bits - 1)
+    // of each level's generators, the smallest table (>= 2 Delta entries) that has one
     P.gtab_total = 0;
     P.gens_total = goff;
+    bool hashed = true;
     for (int l = 0; l < dpb::kMaxLevels; ++l) {
         P.gtab_off[l] = P.gtab_total;
         P.gtab_bits[l] = 0;
+        P.gtab_shift[l] = 0;
         if (l >= 1 && l < L) {
-            int bits = 6;
-            while ((1 << bits) < 4 * h.branching[l]) ++bits;
-            P.gtab_bits[l] = bits;
-            P.gtab_total += 1 << bits;
+            const uint32_t* g = plan->gens_h.data() + P.gens_off[l];
+            const int n = h.branching[l];
+            int bits = 1;
+            while ((1 << bits) < 2 * n) ++bits;
+            bool found = false;
+            std::vector<char> used;
+            for (; bits <= 12 && !found; ++bits) {
+                const uint32_t mask = (1u << bits) - 1u;
+                for (int r = 1; r < 32 && !found; ++r) {
+                    used.assign((size_t)1 << bits, 0);
+                    bool ok = true;
+                    for (int j = 0; j < n && ok; ++j) {
+                        const uint32_t x = g[j], hs = (x ^ (x >> r)) & mask;
+                        ok = !used[hs];
+                        used[hs] = 1;
+                    }
+                    if (ok) {
+                        found = true;
+                        P.gtab_bits[l] = bits;
+                        P.gtab_shift[l] = r;
+                    }
+                }
+                if (found) break;
+            }
+            if (!found) hashed = false;
+            P.gtab_total += 1 << P.gtab_bits[l];
         }
     }
-    if (P.gtab_total > 16384) P.gtab_total = 0;  // too large for LDS: slots stay unrouted
+    if (!hashed || P.gtab_total > 8192) P.gtab_total = 0;  // no routing: slots are decoded by table
     return DPB_OK;
 }
 
-// Generator hash tables (see DevPlan::gtab).
-void build_gen_tables(const dpb_plan* plan, std::vector<int32_t>* out)
+// Generator hash tables (see DevPlan::gtab): entry h holds (g_j, j) for the
+// generator that hashes to h, or (0, -1).
+void build_gen_tables(const dpb_plan* plan, std::vector<uint32_t>* out)
 {
     const DevPlan& P = plan->dev;
-    out->assign((size_t)std::max(P.gtab_total, 1), -1);
+    out->assign((size_t)std::max(P.gtab_total, 1) * 2, 0);
+    for (size_t i = 1; i < out->size(); i += 2) (*out)[i] = 0xFFFFFFFFu;
     if (!P.gtab_total) return;
     for (int l = 1; l < P.levels; ++l) {
-        const int bits = P.gtab_bits[l];
-        const uint32_t mask = (1u << bits) - 1u;
-        int32_t* tab = out->data() + P.gtab_off[l];
+        const uint32_t mask = (1u << P.gtab_bits[l]) - 1u, r = (uint32_t)P.gtab_shift[l];
+        uint32_t* tab = out->data() + 2 * (size_t)P.gtab_off[l];
         for (int j = 0; j < P.delta[l]; ++j) {
-            const uint32_t g = plan->gens_h[P.gens_off[l] + j];
-            uint32_t hsh = (g * dpb::kGenHashMul) >> (32 - bits);
-            while (tab[hsh] >= 0) hsh = (hsh + 1) & mask;
-            tab[hsh] = j;
+            const uint32_t x = plan->gens_h[P.gens_off[l] + j], hs = (x ^ (x >> r)) & mask;
+            tab[2 * hs] = x;
+            tab[2 * hs + 1] = (uint32_t)j;
         }
     }
 }
@@ -232,7 +257,7 @@ dpb_status upload(dpb_plan* plan)
     DevPlan& P = plan->dev;
     std::vector<uint16_t> gamma, gamma_pair, gamma_t;
     std::vector<uint32_t> nt;
-    std::vector<int32_t> gtab;
+    std::vector<uint32_t> gtab;
     build_gen_tables(plan, &gtab);
     build_gamma_fragments(plan, &gamma);
     build_gamma_pair(plan, &gamma_pair);
@@ -285,7 +310,7 @@ dpb_status upload(dpb_plan* plan)
     P.gamma_pair = base + parts[3].off;
     P.gamma_t = base + parts[4].off;
     P.nt = (const uint32_t*)(base + parts[5].off);
-    P.gtab = (const int32_t*)(base + parts[6].off);
+    P.gtab = (const uint32_t*)(base + parts[6].off);
     return DPB_OK;
 }
 

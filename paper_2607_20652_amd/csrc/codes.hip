@@ -53,7 +53,7 @@ struct Wave {
     uint32_t* cw;     // [16][cws] column sign bitmaps (g's sign folded in for bf16)
     float* score;     // [16][16] scores of one column block and generator tile
     const uint32_t* mask;  // [dp] row masks (shared)
-    const int32_t* gtab;   // generator hash tables (shared)
+    const uint32_t* gtab;  // generator hash tables (shared): (g_j, j) pairs
     const uint32_t* gens;  // generators (shared)
     const uint32_t* nt;    // nibble tables (shared, backward only)
 };
@@ -71,11 +71,12 @@ __device__ __forceinline__ float lds_ldf(uint32_t a) { return *(const lds_f32*)(
 
 // Routes every hashed slot of levels >= lmin: finds the first parent slot q
 // of the previous level (in slot order) and the generator j with
-// c = parent_q XOR g_j, by looking c XOR parent_q up in the level's generator
-// hash table.  W.route[tt][s] = (q << 16) | j, or -1 when no pair exists.
+// c = parent_q XOR g_j, by looking c XOR parent_q up in the level's
+// collision-free generator hash: one probe per parent, all parents tried.
+// W.route[tt][s] = (q << 16) | j, or -1 when no pair exists.
 __device__ void route_slots(const DevPlan& P, const Wave& W, int lmin)
 {
-    const int k = P.k_tot;
+    const int k = P.k_tot, kmax = P.kmax;
     if (P.gtab_total <= 0 || P.levels < 2) return;
     for (int tt = 0; tt < W.ntok; ++tt)
         for (int s = P.slot_base[lmin] + W.lane; s < k; s += 64) {
@@ -84,26 +85,20 @@ __device__ void route_slots(const DevPlan& P, const Wave& W, int lmin)
             if (c >= P.d) {
                 int l = lmin;
                 while (l + 1 < P.levels && s >= P.slot_base[l + 1]) ++l;
-                const int bits = P.gtab_bits[l], Kp = P.active[l - 1];
-                const uint32_t hmask = (1u << bits) - 1u;
-                const int32_t* tab = W.gtab + P.gtab_off[l];
-                const uint32_t* gl = W.gens + P.gens_off[l];
+                const int Kp = P.active[l - 1], r = P.gtab_shift[l];
+                const uint32_t hmask = (1u << P.gtab_bits[l]) - 1u;
+                const u32x2* tab = (const u32x2*)W.gtab + P.gtab_off[l];
                 const int32_t* parents = W.idx + tt * k + P.slot_base[l - 1];
-                for (int q = 0; q < Kp && rt < 0; ++q) {
+                for (int q = Kp - 1; q >= 0; --q) {
                     const int32_t p = parents[q];
-                    if (p < 0) continue;
                     const uint32_t x = (uint32_t)c ^ (uint32_t)p;
-                    uint32_t h = (x * kGenHashMul) >> (32 - bits);
-                    for (int32_t j = tab[h]; j >= 0; h = (h + 1) & hmask, j = tab[h]) {
-                        if (gl[j] == x) {
-                            rt = (q << 16) | j;
-                            break;
-                        }
-                    }
+                    const u32x2 e = tab[(x ^ (x >> r)) & hmask];
+                    if (p >= 0 && x != 0u && e.x == x) rt = (q << 16) | (int)e.y;
                 }
             }
             W.route[tt * k + s] = rt;
         }
+    (void)kmax;
 }
 
 // Bit transpose inside each 32-lane half: lane s of a half holds x_s on
@@ -386,9 +381,9 @@ __device__ Wave make_wave(const DevPlan& P, unsigned char* smem, bool scoring, b
     W.cw = (uint32_t*)(b + CL.cw);
     W.score = (float*)(b + CL.score);
     const unsigned o_gtab = align16u(P.dp * 4);
-    const unsigned o_gens = o_gtab + align16u(P.gtab_total * 4), o_nt = o_gens + align16u(P.gens_total * 4);
+    const unsigned o_gens = o_gtab + align16u(P.gtab_total * 8), o_nt = o_gens + align16u(P.gens_total * 4);
     W.mask = (const uint32_t*)smem;
-    W.gtab = (const int32_t*)(smem + o_gtab);
+    W.gtab = (const uint32_t*)(smem + o_gtab);
     W.gens = (const uint32_t*)(smem + o_gens);
     W.nt = (const uint32_t*)(smem + o_nt);
     return W;
@@ -431,12 +426,12 @@ __device__ void write_rows(const DevPlan& P, const Wave& W, void* out)
 __device__ void load_shared(const DevPlan& P, unsigned char* smem, bool with_nt)
 {
     const unsigned o_gtab = align16u(P.dp * 4);
-    const unsigned o_gens = o_gtab + align16u(P.gtab_total * 4), o_nt = o_gens + align16u(P.gens_total * 4);
+    const unsigned o_gens = o_gtab + align16u(P.gtab_total * 8), o_nt = o_gens + align16u(P.gens_total * 4);
     uint32_t* s_mask = (uint32_t*)smem;
-    int32_t* s_gtab = (int32_t*)(smem + o_gtab);
+    uint32_t* s_gtab = (uint32_t*)(smem + o_gtab);
     uint32_t* s_gens = (uint32_t*)(smem + o_gens);
     for (int i = threadIdx.x; i < P.dp; i += kThreads) s_mask[i] = P.masks[i];
-    for (int i = threadIdx.x; i < P.gtab_total; i += kThreads) s_gtab[i] = P.gtab[i];
+    for (int i = threadIdx.x; i < 2 * P.gtab_total; i += kThreads) s_gtab[i] = P.gtab[i];
     for (int i = threadIdx.x; i < P.gens_total; i += kThreads) s_gens[i] = P.gens[i];
     if (with_nt) {
         uint32_t* s_nt = (uint32_t*)(smem + o_nt);

@@ -56,16 +56,17 @@ struct DevPlan {
     // [dp/16][dpad/16][64] x 4 bf16.
     const void* gamma_t;
     int64_t gamma_t_off[kMaxLevels];  // in 8-byte units
-    // Open-addressing hash of each level's generators (value -> j, -1 empty),
-    // hash h(x) = (x * kGenHashMul) >> (32 - gtab_bits[l]), linear probing.
-    const int32_t* gtab;
-    int gtab_off[kMaxLevels];
+    // Collision-free hash of each level's generators: entry
+    // h(x) = (x ^ (x >> gtab_shift[l])) & (2^gtab_bits[l] - 1) holds the pair
+    // (g_j, j) of the generator with that hash, or (0, -1).
+    const uint32_t* gtab;
+    int gtab_off[kMaxLevels];   // in entries (pairs)
     int gtab_bits[kMaxLevels];
+    int gtab_shift[kMaxLevels];
     int gtab_total;             // entries over all levels (0: routing disabled)
     int gens_total;             // sum_l Delta_l
 };
 
-constexpr uint32_t kGenHashMul = 0x9E3779B1u;
 
 // Per-wave LDS layout of the code kernels (byte offsets inside a wave's region).
 struct CodeLayout {
@@ -127,7 +128,7 @@ constexpr int kCodeWaves = 4;  // waves per workgroup in the code kernels
 // tables and generators, then (backward only) nibble tables.
 __host__ __device__ inline unsigned code_shared_bytes(const DevPlan& P, bool with_nt)
 {
-    const unsigned b = align16u(P.dp * 4) + align16u(P.gtab_total * 4) + align16u(P.gens_total * 4) +
+    const unsigned b = align16u(P.dp * 4) + align16u(P.gtab_total * 8) + align16u(P.gens_total * 4) +
                        (with_nt ? align16u(P.nt_groups * 16 * P.nchunk * 4) : 0u);
     return (b + 255u) & ~255u;
 }
