@@ -180,7 +180,7 @@ void build_nibble_tables(const dpb_plan* plan, std::vector<uint32_t>* out)
             }
 }
 
-// Scoring A fragments in the paired coordinate order (see DevPlan::gamma_pair).
+// Scoring A fragments in the interleaved-halves coordinate order (see DevPlan::gamma_pair).
 void build_gamma_pair(const dpb_plan* plan, std::vector<uint16_t>* out)
 {
     const DevPlan& P = plan->dev;
@@ -195,7 +195,7 @@ void build_gamma_pair(const dpb_plan* plan, std::vector<uint16_t>* out)
                     const int j = 16 * mb + (lane & 15), kq = lane >> 4;
                     uint16_t* dst = out->data() + (P.gamma_off[l] + ((int64_t)mb * P.nchunk + c) * 64 + lane) * 8;
                     for (int e = 0; e < 8; ++e) {
-                        const int iota = 32 * c + kq + 4 * (e >> 1) + 16 * (e & 1);
+                        const int iota = 32 * c + 4 * kq + (e >> 1) + 16 * (e & 1);
                         dst[e] = (j < P.delta[l] && iota < P.d) ? pm_one(row_parity(plan->masks_h[iota], g[j])) : 0;
                     }
                 }

@@ -47,10 +47,9 @@ struct Wave {
     float* frt;       // [fr_cap / 4][16] signed coefficient sums
     void* pb;         // [TPW][dp] sign bits of the leaf level's parents (pb_bytes each)
     float* y;         // [TPW][dp] output accumulator (fp32)
-    uint32_t* pairs;  // [TPW][dp/2] |g| as bf16 pairs in the paired coordinate order
-    uint32_t* signw;  // [TPW][nchunk] sign bits of g, natural order
+    uint32_t* pairs;  // [TPW][dp/2] g as signed bf16 pairs, interleaved halves
     float* gf;        // [TPW][dp] fp32 g (fp32 activations)
-    uint32_t* cw;     // [16][cws] column sign bitmaps (g's sign folded in for bf16)
+    uint32_t* cw;     // [16][cws] column sign bitmaps
     float* score;     // [16][16] scores of one column block and generator tile
     const uint32_t* mask;  // [dp] row masks (shared)
     const uint32_t* gtab;  // generator hash tables (shared): (g_j, j) pairs
@@ -376,7 +375,6 @@ __device__ Wave make_wave(const DevPlan& P, unsigned char* smem, bool scoring, b
     W.pb = (void*)(b + CL.pb);
     W.y = (float*)(b + CL.y);
     W.pairs = (uint32_t*)(b + CL.pairs);
-    W.signw = (uint32_t*)(b + CL.signw);
     W.gf = (float*)(b + CL.y);
     W.cw = (uint32_t*)(b + CL.cw);
     W.score = (float*)(b + CL.score);
@@ -484,7 +482,7 @@ __global__ __launch_bounds__(kThreads) void decode2_kernel(DevPlan P, const int3
 template <bool G_BF16>
 __device__ __forceinline__ float g_at(const DevPlan& P, const Wave& W, int tt, int iota)
 {
-    if constexpr (G_BF16) return pair_value(P, W.pairs, W.signw, tt, iota);
+    if constexpr (G_BF16) return pair_value(P, W.pairs, tt, iota);
     else return W.gf[tt * P.dp + iota];
 }
 
@@ -496,10 +494,10 @@ __device__ void score_level(const DevPlan& P, const Wave& W, int l)
     const int k = P.k_tot, TPW = P.wave_tokens, lane = W.lane;
     const int CPT = P.cpt[l], csh = P.cpt_shift[l], Kp = P.active[l - 1], Kl = P.active[l];
     const int ncol = TPW * CPT, NB = (ncol + 15) >> 4, sbp = P.slot_base[l - 1], sbl = P.slot_base[l];
-    const ActTile A{W.pairs, W.signw, W.gf};
+    const ActTile A{W.pairs, W.gf};
     const int col = lane & 15, kq = lane >> 4;
     for (int nb = 0; nb < NB; ++nb) {
-        column_bitmaps<G_BF16>(P, lane, W.ntok, csh, nb, W.idx + sbp, k, Kp, A, W.nt, W.cw);
+        column_bitmaps(P, lane, W.ntok, csh, nb, W.idx + sbp, k, Kp, W.nt, W.cw);
         wave_sync();
         const int r = nb * 16 + col, tt = r >> csh, q = r & (CPT - 1);
         const bool valid = r < ncol && tt < W.ntok && q < Kp && W.idx[tt * k + sbp + q] >= 0;
@@ -543,7 +541,7 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
         // codes, routes reset, and g in LDS
         load_codes(P, W, idx, nullptr);
         if constexpr (G_BF16) {
-            load_pairs(P, lane, W.ntok, TPW, (const uint16_t*)g, t0, W.pairs, W.signw);
+            load_pairs(P, lane, W.ntok, TPW, (const uint16_t*)g, t0, W.pairs);
         } else {
             const float* gfp = (const float*)g;
             for (int tt = 0; tt < TPW; ++tt)

@@ -47,9 +47,9 @@ struct DevPlan {
     const uint32_t* nt;         // [nt_groups][nchunk][16] sign-bitmap word w of (v << 4g)
     int fr_cap;                 // slots per table-decode chunk (multiple of 32, <= kFrMax)
     int pb_bytes;               // bytes per coordinate of the leaf parents' sign bits (1 or 2)
-    // Scoring A fragments with the paired coordinate order: lane L, element
-    // e = 2i + h of chunk c holds generator row 16*mb + L%16 at coordinate
-    // 32c + L/16 + 4i + 16h.  Per level: [mblocks][nchunk][64] x 8 bf16.
+    // Scoring A fragments in the interleaved-halves coordinate order: lane L,
+    // element e = 2i + h of chunk c holds generator row 16*mb + L%16 at
+    // coordinate 32c + 4*(L/16) + i + 16h.  Per level: [mblocks][nchunk][64] x 8 bf16.
     const void* gamma_pair;
     // Column-decode B fragments: lane L of block (cb, kb) holds generator rows
     // 16kb + 4*(L/16) + i (i < 4) at coordinate 16cb + L%16.  Per level:
@@ -70,7 +70,7 @@ struct DevPlan {
 
 // Per-wave LDS layout of the code kernels (byte offsets inside a wave's region).
 struct CodeLayout {
-    unsigned idx, coef, route, par, alpha, claim, fri, frc, frv, frt, pb, y, pairs, signw, cw, score, bytes;
+    unsigned idx, coef, route, par, alpha, claim, fri, frc, frv, frt, pb, y, pairs, cw, score, bytes;
 };
 
 constexpr int kFrMax = 256;          // largest table-decode chunk
@@ -104,15 +104,14 @@ __host__ __device__ inline CodeLayout code_layout(const DevPlan& P, bool with_sc
     unsigned yend = align16u(off + TPW * P.dp * 4);
     const unsigned cend = align16u(L.claim + 16 * dleaf * 4);
     if (cend > yend) yend = cend;
-    L.pairs = L.signw = L.cw = L.score = yend;
+    L.pairs = L.cw = L.score = yend;
     off = yend;
     if (with_scoring) {
         unsigned s = act_bf16 ? L.y : yend;
         if (act_bf16) {
             L.pairs = s; s = align16u(s + TPW * P.dp * 2);
-            L.signw = s; s = align16u(s + TPW * P.nchunk * 4);
         } else {
-            L.pairs = L.signw = L.y;  // fp32 activations occupy the y region
+            L.pairs = L.y;  // fp32 activations occupy the y region
         }
         L.cw = s;    s = align16u(s + 16 * P.cws * 4);
         L.score = s; s = align16u(s + 16 * 16 * 4);  // one 16 x 16 score tile

@@ -2,7 +2,7 @@
 //
 // A wave owns `wave_tokens` tokens (16 / CPT, CPT = parent columns per
 // token rounded up to a power of two); their activations stay in LDS in the
-// paired layout of scoring.hpp.
+// interleaved-halves layout of scoring.hpp.
 //
 //  * Level 0 (§2.1 Eq. 2: scoring a basis feature is a coordinate read):
 //    each token's lanes take the maximum key over their coordinates; the
@@ -61,7 +61,7 @@ __host__ __device__ inline EncLayout enc_layout(const DevPlan& P, bool act_bf16)
     L.kmaxp = P.kmax;
     unsigned off = 0;
     L.act = off;
-    off = align16u(off + (act_bf16 ? TPW * (P.dp * 2 + P.nchunk * 4) : TPW * P.dp * 4));
+    off = align16u(off + (act_bf16 ? TPW * P.dp * 2 : TPW * P.dp * 4));
     L.cw = off;   off = align16u(off + 16 * P.cws * 4);
     L.par = off;  off = align16u(off + TPW * L.kmaxp * 4);
     L.list = off; off = align16u(off + TPW * listn * 8);
@@ -213,24 +213,24 @@ __device__ void emit_sorted(const DevPlan& P, int lane, int64_t t0, int ntok, co
 }
 
 // Level 0, bf16 activations: 32-bit keys (|x| bf16 bits << 16 | 0xFFFF - iota).
-// Lane li of token tt reads the paired dwords e = li + LPT m; dword e holds
-// coordinates 32 (e >> 4) + ((e >> 2) & 3) + 4 (e & 3) and that + 16.
+// Lane li of token tt reads the interleaved dwords e = li + LPT m; dword e
+// holds coordinates 32 (e >> 4) + (e & 15) (low half) and that + 16.
 // Coordinates past d hold zeros, so their keys sort below every real key.
 template <int LPT, int LLP>
-__device__ void level0_bf16(const DevPlan& P, int lane, int64_t t0, int ntok, const uint32_t* pairs,
-                            const uint32_t* signw, uint64_t* list, int listn, int* cnt, int32_t* par, int kmaxp,
-                            int32_t* out_idx, float* out_coef, int x32addr)
+__device__ void level0_bf16(const DevPlan& P, int lane, int64_t t0, int ntok, const uint32_t* pairs, uint64_t* list,
+                            int listn, int* cnt, int32_t* par, int kmaxp, int32_t* out_idx, float* out_coef,
+                            int x32addr)
 {
     const int tt = lane >> LLP, li = lane & (LPT - 1), K0 = P.active[0], dp2 = P.dp / 2;
     const uint32_t* row = pairs + tt * dp2;
-    const int lo0 = 32 * (li >> 4) + ((li >> 2) & 3) + 4 * (li & 3);  // coordinate of dword li (low half)
-    constexpr uint32_t STEP = 2 * LPT;                                 // coordinate step per dword row
+    const int lo0 = 32 * (li >> 4) + (li & 15);  // coordinate of the low half of dword li
+    constexpr uint32_t STEP = 2 * LPT;           // coordinate step per dword row
     uint32_t best = 0;
     {
         uint32_t c = 0xFFFFu - (uint32_t)lo0;
         for (int e = li; e < dp2; e += LPT, c -= STEP) {
             const uint32_t D = row[e];
-            const uint32_t klo = (D << 16) | c, khi = (D & 0xFFFF0000u) | (c - 16u);
+            const uint32_t klo = ((D << 16) & 0x7FFF0000u) | c, khi = (D & 0x7FFF0000u) | (c - 16u);
             best = max(best, max(klo, khi));
         }
     }
@@ -244,7 +244,7 @@ __device__ void level0_bf16(const DevPlan& P, int lane, int64_t t0, int ntok, co
         uint32_t c = 0xFFFFu - (uint32_t)lo0;
         for (int e = li; e < dp2; e += LPT, c -= STEP) {
             const uint32_t D = row[e];
-            const uint32_t klo = (D << 16) | c, khi = (D & 0xFFFF0000u) | (c - 16u);
+            const uint32_t klo = ((D << 16) & 0x7FFF0000u) | c, khi = (D & 0x7FFF0000u) | (c - 16u);
             if (klo >= tau) lst[atomicAdd(&cnt[tt], 1)] = klo;
             if (khi >= tau) lst[atomicAdd(&cnt[tt], 1)] = khi;
         }
@@ -260,9 +260,8 @@ __device__ void level0_bf16(const DevPlan& P, int lane, int64_t t0, int ntok, co
             const uint32_t iota = 0xFFFFu - (ke & 0xFFFFu);
             par[tt * kmaxp + rank] = (int32_t)iota;
             if (live) {
-                const uint32_t sg = (signw[tt * P.nchunk + (iota >> 5)] >> (iota & 31)) & 1u;
                 out_idx[(t0 + tt) * P.k_tot + rank] = (int32_t)iota;
-                out_coef[(t0 + tt) * P.k_tot + rank] = __uint_as_float(((ke >> 16) | (sg << 15)) << 16);
+                out_coef[(t0 + tt) * P.k_tot + rank] = pair_value(P, pairs, tt, (int)iota);
             }
         }
     }
@@ -328,13 +327,12 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
     const EncLayout EL = enc_layout(P, X_BF16);
     unsigned char* wb = smem + enc_shared_bytes(P) + (unsigned)wave * EL.bytes;
     uint32_t* pairs = (uint32_t*)(wb + EL.act);
-    uint32_t* signw = pairs + TPW * (dp / 2);
     float* xf = (float*)(wb + EL.act);
     uint32_t* cw = (uint32_t*)(wb + EL.cw);
     int32_t* par = (int32_t*)(wb + EL.par);
     uint64_t* list = (uint64_t*)(wb + EL.list);
     int* cnt = (int*)(wb + EL.cnt);
-    const ActTile A{pairs, signw, xf};
+    const ActTile A{pairs, xf};
 
     const int col = lane & 15, kq = lane >> 4, ct = col >> CB, q = col & (CPT - 1), lanepos = q * 4 + kq;
 
@@ -345,7 +343,7 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
         const int ntok = (int)min((int64_t)TPW, T - t0);
 
         if constexpr (X_BF16) {
-            load_pairs(P, lane, ntok, TPW, (const uint16_t*)xin, t0, pairs, signw);
+            load_pairs(P, lane, ntok, TPW, (const uint16_t*)xin, t0, pairs);
         } else {
             const float* xs = (const float*)xin;
             for (int tt = 0; tt < TPW; ++tt)
@@ -356,7 +354,7 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
 
         // ---- level 0
         if constexpr (X_BF16)
-            level0_bf16<LPT, LLP>(P, lane, t0, ntok, pairs, signw, list, EL.listn, cnt, par, EL.kmaxp, out_idx,
+            level0_bf16<LPT, LLP>(P, lane, t0, ntok, pairs, list, EL.listn, cnt, par, EL.kmaxp, out_idx,
                                   out_coef, x32);
         else
             level0_f32<LPT, LLP>(P, lane, t0, ntok, xf, list, EL.listn, cnt, par, EL.kmaxp, out_idx, out_coef, x32);
@@ -365,7 +363,7 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
         // ---- levels l >= 1
         for (int l = 1; l < P.levels; ++l) {
             const int Kp = P.active[l - 1], Dl = P.delta[l];
-            column_bitmaps<X_BF16>(P, lane, ntok, CB, 0, par, EL.kmaxp, Kp, A, s_nt, cw);
+            column_bitmaps(P, lane, ntok, CB, 0, par, EL.kmaxp, Kp, s_nt, cw);
             wave_sync();
             const int32_t p = (ct < ntok && q < Kp) ? par[ct * EL.kmaxp + q] : -1;
             const bool valid = p >= 0;

@@ -7,9 +7,10 @@
 // the 16x16x32 bf16 MFMA with Gamma_l as the A operand (exact +-1) and the
 // sign-flipped activations as B.  B is built from the column's sign bitmap
 // (nibble tables: parity is linear in the index bits) and the activations
-// held in LDS in the paired coordinate order, so that each B dword is one
-// rotate plus one and-or: lane kq's dword i holds coordinates
-// 32c + kq + 4i (low half) and 32c + kq + 4i + 16 (high half).
+// held in LDS in the "interleaved halves" order: dword o (0..15) of chunk c
+// holds coordinate 32c + o in its low half and 32c + o + 16 in its high half,
+// so that each B dword is one rotate plus one bit-select.  MFMA lane kq's K
+// values 8kq + 2i + h are coordinates 32c + 4kq + i + 16h.
 #pragma once
 
 #include "device_common.hpp"
@@ -20,40 +21,42 @@ constexpr int kScoreBatch = 8;  // A fragments fetched per batch
 
 // A wave's activations in LDS.
 struct ActTile {
-    const uint32_t* pairs;  // bf16: [TPW][dp/2] |a| as bf16 pairs (paired order)
-    const uint32_t* signw;  // bf16: [TPW][nchunk] sign bits, natural order (bit b = coordinate 32c + b)
+    const uint32_t* pairs;  // bf16: [TPW][dp/2] signed bf16 pairs, interleaved halves
     const float* f;         // fp32: [TPW][dp]
 };
 
-// Sign bitmaps of the 16 columns of block nb into cw[16][cws]; for bf16
-// activations the activation signs are folded in.  Column r is parent slot
-// q = r mod 2^csh of token tt = r / 2^csh, with parent parents[tt * pstride + q]
-// when q < nparents and tt < ntok.  Lane
-// (col, w0) builds words w0, w0 + 4, ... of column col: one nibble-table row
-// per 4-bit group of the parent index (parity is linear in the index bits).
-template <bool ACT_BF16>
+// Sign bitmaps of the 16 columns of block nb into cw[16][cws] (bit b of word
+// w = sign at coordinate 32w + b).  Column r is parent slot q = r mod 2^csh
+// of token tt = r / 2^csh, with parent parents[tt * pstride + q] when
+// q < nparents and tt < ntok.  Lane (col, w0) builds words w0, w0 + 4, ... of
+// column col: one nibble-table row per 4-bit group of the parent index
+// (parity is linear in the index bits).
 __device__ void column_bitmaps(const DevPlan& P, int lane, int ntok, int csh, int nb, const int32_t* parents,
-                               int pstride, int nparents, const ActTile& A, const uint32_t* nt, uint32_t* cw)
+                               int pstride, int nparents, const uint32_t* nt, uint32_t* cw)
 {
-    const int nchunk = P.nchunk;
+    constexpr int MW = 8;  // words per lane kept in registers (nchunk <= 32)
+    const int nchunk = P.nchunk, w0 = lane >> 4;
     const int col = lane & 15, r = nb * 16 + col, tt = r >> csh, q = r & ((1 << csh) - 1);
     int32_t p = -1;
     if (r < (P.wave_tokens << csh) && tt < ntok && q < nparents) p = parents[tt * pstride + q];
-    // nibble table layout [g][w][16]: word w of group g for nibble value v at (g * nchunk + w) * 16 + v
-    const uint32_t* rows[8];
-#pragma unroll
-    for (int g = 0; g < 8; ++g) rows[g] = nt + g * nchunk * 16 + ((p >> (4 * g)) & 15);
-    const uint32_t* sw = A.signw + (p >= 0 ? tt : 0) * nchunk;
+    const uint32_t pu = p >= 0 ? (uint32_t)p : 0u;
     uint32_t* dst = cw + col * P.cws;
-    for (int w = lane >> 4; w < nchunk; w += 4) {
-        uint32_t word = 0;
-        if (p >= 0) {
+    // nibble table layout [g][w][16]: word w of group g for nibble value v at (g * nchunk + w) * 16 + v
+    for (int wb = 0; wb < nchunk; wb += 4 * MW) {
+        uint32_t acc[MW];
 #pragma unroll
-            for (int g = 0; g < 8; ++g)
-                if (g < P.nt_groups) word ^= rows[g][w * 16];
-            if constexpr (ACT_BF16) word ^= sw[w];
+        for (int m = 0; m < MW; ++m) acc[m] = 0;
+        for (int g = 0; g < P.nt_groups; ++g) {
+            const uint32_t* rg = nt + (g * nchunk + wb + w0) * 16 + ((pu >> (4 * g)) & 15u);
+#pragma unroll
+            for (int m = 0; m < MW; ++m)
+                if (wb + w0 + 4 * m < nchunk) acc[m] ^= rg[m * 64];
         }
-        dst[w] = word;
+#pragma unroll
+        for (int m = 0; m < MW; ++m) {
+            const int w = wb + w0 + 4 * m;
+            if (w < nchunk) dst[w] = p >= 0 ? acc[m] : 0u;
+        }
     }
 }
 
@@ -66,19 +69,20 @@ __device__ __forceinline__ void score_chunk(const DevPlan& P, int kq, u32x4 a, u
 {
     const bf16x8 av = __builtin_bit_cast(bf16x8, a);
     if constexpr (ACT_BF16) {
-        const uint32_t R = rotl32(wd, 15u - (uint32_t)kq);
+        // dword i: coordinates 4kq + i (low half) and 4kq + i + 16 (high half)
+        const uint32_t R = rotl32(wd, 15u - 4u * (uint32_t)kq);
         const u32x4 pd = *(const u32x4*)(prow + c * 16);
         u32x4 b;
-        b.x = (R & 0x80008000u) | pd.x;
-        b.y = (__builtin_amdgcn_alignbit(R, R, 4) & 0x80008000u) | pd.y;
-        b.z = (__builtin_amdgcn_alignbit(R, R, 8) & 0x80008000u) | pd.z;
-        b.w = (__builtin_amdgcn_alignbit(R, R, 12) & 0x80008000u) | pd.w;
+        b.x = pd.x ^ (R & 0x80008000u);
+        b.y = pd.y ^ (__builtin_amdgcn_alignbit(R, R, 1) & 0x80008000u);
+        b.z = pd.z ^ (__builtin_amdgcn_alignbit(R, R, 2) & 0x80008000u);
+        b.w = pd.w ^ (__builtin_amdgcn_alignbit(R, R, 3) & 0x80008000u);
         acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
     } else {
         uint32_t hi[8], mi[8], lo[8];
 #pragma unroll
         for (int x = 0; x < 8; ++x) {
-            const int off = kq + 4 * (x >> 1) + 16 * (x & 1);
+            const int off = 4 * kq + (x >> 1) + 16 * (x & 1);
             float v = frow[32 * c + off];
             v = __uint_as_float(__float_as_uint(v) ^ (((wd >> off) & 1u) << 31));
             split3(v, hi[x], mi[x], lo[x]);
@@ -118,15 +122,17 @@ __device__ f32x4 mfma_scores(const DevPlan& P, int lane, int l, int mb, int trow
 }
 
 // Writes bf16 activations of `ntok` rows (row stride d elements) into the
-// paired layout and the sign words; rows >= ntok and coordinates >= d are 0.
-// Each lane reads 8 consecutive coordinates (one 16-byte load when d is a
-// multiple of 8) and scatters them as half-words.
+// interleaved-halves layout; rows >= ntok and coordinates >= d are 0.  Lane
+// 4c + h reads coordinates 32c + 8h .. 32c + 8h + 7 (one 16-byte load when d
+// is a multiple of 8); lanes h and h + 2 of a quad swap two dwords so that
+// each lane writes four complete dwords with one 16-byte store.
 __device__ inline void load_pairs(const DevPlan& P, int lane, int ntok, int tpw, const uint16_t* src, int64_t row0,
-                                  uint32_t* pairs, uint32_t* signw)
+                                  uint32_t* pairs)
 {
-    const int d = P.d, dp = P.dp, nchunk = P.nchunk;
-    uint16_t* ph = (uint16_t*)pairs;
+    const int d = P.d, dp = P.dp;
     const bool vec = (d & 7) == 0;
+    const int h = lane & 3;
+    const bool lowq = h < 2;
     for (int tt = 0; tt < tpw; ++tt) {
         const bool live = tt < ntok;
         const uint16_t* row = src + (row0 + tt) * d;
@@ -140,34 +146,30 @@ __device__ inline void load_pairs(const DevPlan& P, int lane, int ntok, int tpw,
                 for (int e = 0; e < 8; ++e)
                     if (o + e < d) v[e >> 1] |= (uint32_t)row[o + e] << (16 * (e & 1));
             }
-            // coordinate o + e sits at paired dword kq * 4 + i of chunk c, half h
-            const int c = o >> 5, base = o & 31;
-            uint32_t sg = 0;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const uint32_t h16 = (v[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
-                const int b = base + e, h = b >> 4, kq = b & 3, i = (b >> 2) & 3;
-                ph[(tt * (dp / 2) + c * 16 + kq * 4 + i) * 2 + h] = (uint16_t)(h16 & 0x7FFFu);
-                sg |= (h16 >> 15) << e;
-            }
-            // 8 sign bits of this lane -> bits base..base+7 of word c (4 lanes per word)
-            uint32_t part = sg << base;
-            part |= __shfl_xor(part, 1, 64);
-            part |= __shfl_xor(part, 2, 64);
-            if ((lane & 3) == 0) signw[tt * nchunk + c] = part;
+            // lane h < 2 keeps coordinates 8h + 0..3 and takes 16 + 8h + 0..3 from lane h + 2;
+            // lane h + 2 keeps 16 + 8h + 4..7 and takes 8h + 4..7 from lane h
+            const uint32_t s0 = lowq ? v[2] : v[0], s1 = lowq ? v[3] : v[1];
+            const uint32_t r0 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)s0, 0x4E, 0xF, 0xF, false);
+            const uint32_t r1 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)s1, 0x4E, 0xF, 0xF, false);
+            const uint32_t l0 = lowq ? v[0] : r0, l1 = lowq ? v[1] : r1;  // low halves (coordinates < 16)
+            const uint32_t h0 = lowq ? r0 : v[2], h1 = lowq ? r1 : v[3];  // high halves
+            u32x4 w;
+            w.x = __builtin_amdgcn_perm(h0, l0, 0x05040100u);
+            w.y = __builtin_amdgcn_perm(h0, l0, 0x07060302u);
+            w.z = __builtin_amdgcn_perm(h1, l1, 0x05040100u);
+            w.w = __builtin_amdgcn_perm(h1, l1, 0x07060302u);
+            const int c = o >> 5;
+            *(u32x4*)(pairs + tt * (dp / 2) + c * 16 + 8 * (h & 1) + 4 * (h >> 1)) = w;
         }
     }
 }
 
-// Activation at coordinate iota of row tt from the paired layout.
-__device__ __forceinline__ float pair_value(const DevPlan& P, const uint32_t* pairs, const uint32_t* signw, int tt,
-                                            int iota)
+// Activation at coordinate iota of row tt from the interleaved-halves layout.
+__device__ __forceinline__ float pair_value(const DevPlan& P, const uint32_t* pairs, int tt, int iota)
 {
     const int c = iota >> 5, b = iota & 31;
-    const uint32_t dw = pairs[tt * (P.dp / 2) + c * 16 + (b & 3) * 4 + ((b >> 2) & 3)];
-    const uint32_t mag = (b >> 4) ? (dw >> 16) : (dw & 0xFFFFu);
-    const uint32_t sg = (signw[tt * P.nchunk + c] >> b) & 1u;
-    return bf16_bits_to_f32(mag | (sg << 15));
+    const uint32_t dw = pairs[tt * (P.dp / 2) + c * 16 + (b & 15)];
+    return bf16_bits_to_f32((b >> 4) ? (dw >> 16) : (dw & 0xFFFFu));
 }
 
 }  // namespace dpb
