@@ -85,6 +85,7 @@ dpb_status fill_plan(dpb_plan* plan, const Hierarchy& h, const uint32_t* gens, u
                          : 0;
     P.nt_groups = (h.level_bits[L - 1] + 3) / 4;
     P.cws = P.nchunk | 1;
+    P.prow = P.dp / 2 + 16;
     for (int l = 0; l < dpb::kMaxLevels; ++l) {
         int sh = 0;
         while ((1 << sh) < P.cpt[l]) ++sh;

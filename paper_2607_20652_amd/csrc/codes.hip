@@ -47,7 +47,7 @@ struct Wave {
     float* frt;       // [fr_cap / 4][16] signed coefficient sums
     void* pb;         // [TPW][dp] sign bits of the leaf level's parents (pb_bytes each)
     float* y;         // [TPW][dp] output accumulator (fp32)
-    uint32_t* pairs;  // [TPW][dp/2] g as signed bf16 pairs, interleaved halves
+    uint32_t* pairs;  // [TPW][prow] g as signed bf16 pairs, interleaved halves
     float* gf;        // [TPW][dp] fp32 g (fp32 activations)
     uint32_t* cw;     // [16][cws] column sign bitmaps
     float* score;     // [16][16] scores of one column block and generator tile

@@ -43,6 +43,7 @@ struct DevPlan {
     int dpad[kMaxLevels];       // Delta_l rounded up to a multiple of 16
     int nt_groups;              // 4-bit index groups of the widest index
     int cws;                    // row stride of column bitmaps in LDS (odd, >= nchunk)
+    int prow;                   // row stride (dwords) of bf16 activation pairs in LDS: dp/2 + 16
     int cpt_shift[kMaxLevels];  // log2 cpt[l]
     const uint32_t* nt;         // [nt_groups][nchunk][16] sign-bitmap word w of (v << 4g)
     int fr_cap;                 // slots per table-decode chunk (multiple of 32, <= kFrMax)
@@ -109,7 +110,7 @@ __host__ __device__ inline CodeLayout code_layout(const DevPlan& P, bool with_sc
     if (with_scoring) {
         unsigned s = act_bf16 ? L.y : yend;
         if (act_bf16) {
-            L.pairs = s; s = align16u(s + TPW * P.dp * 2);
+            L.pairs = s; s = align16u(s + TPW * P.prow * 4);
         } else {
             L.pairs = L.y;  // fp32 activations occupy the y region
         }

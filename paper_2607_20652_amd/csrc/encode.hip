@@ -53,15 +53,13 @@ __host__ __device__ inline EncLayout enc_layout(const DevPlan& P, bool act_bf16)
     EncLayout L;
     const int TPW = P.wave_tokens, LPT = 64 / TPW;
     const int ND = (P.dp / 2 + LPT - 1) / LPT;  // activation dwords per lane at level 0
-    const int R = enc_r(P);
-    int listn = P.active[0] * 2 * ND;           // level-0 candidates: K_0 lanes with at most 2 ND keys each
-    if (act_bf16 == false && P.active[0] * ((P.d + LPT - 1) / LPT) > listn) listn = P.active[0] * ((P.d + LPT - 1) / LPT);
-    if (16 / TPW * 4 * R > listn) listn = 16 / TPW * 4 * R;
+    // level-0 candidates: the K_0 lanes whose maximum reaches tau, each with all its keys
+    int listn = P.active[0] * (act_bf16 ? 2 * ND : (P.d + LPT - 1) / LPT);
     L.listn = listn;
     L.kmaxp = P.kmax;
     unsigned off = 0;
     L.act = off;
-    off = align16u(off + (act_bf16 ? TPW * P.dp * 2 : TPW * P.dp * 4));
+    off = align16u(off + (act_bf16 ? TPW * P.prow * 4 : TPW * P.dp * 4));
     L.cw = off;   off = align16u(off + 16 * P.cws * 4);
     L.par = off;  off = align16u(off + TPW * L.kmaxp * 4);
     L.list = off; off = align16u(off + TPW * listn * 8);
@@ -149,36 +147,21 @@ __device__ __forceinline__ void sort_desc(K (&v)[R], int lanepos, int x32addr)
     }
 }
 
-// Exclusive prefix and total of per-lane counts (0..31) over the LPT lanes
-// of a token group (lanes tt*LPT .. tt*LPT + LPT - 1).
-template <int LPT>
-__device__ __forceinline__ void group_scan(int lane, int cnt, int& before, int& total)
+// Emits the first K distinct keys of each token straight from the sorted
+// registers of the MFMA layout (position lanepos * R + r): duplicates are
+// adjacent, the predecessor of register 0 comes from the lane at lanepos - 1,
+// and ranks are prefix counts in lanepos order.  Writes slots [sb, sb + K)
+// and records them as the next parents.
+template <int R, int CPT>
+__device__ __forceinline__ void emit_mfma(const DevPlan& P, const uint64_t (&key)[R], int lane, int lanepos, int ct,
+                                          int prev_addr, uint64_t before_mask, uint64_t token_mask, int64_t t0,
+                                          int ntok, int K, int sb, int32_t* par, int kmaxp, int32_t* out_idx,
+                                          float* out_coef)
 {
-    const uint64_t grp = LPT == 64 ? ~0ull : (((1ull << LPT) - 1ull) << (lane & ~(LPT - 1)));
-    const uint64_t lower = (1ull << lane) - 1ull;
-    before = 0;
-    total = 0;
-#pragma unroll
-    for (int b = 0; b < 5; ++b) {
-        const uint64_t m = __ballot((cnt >> b) & 1) & grp;
-        before += (int)__popcll(m & lower) << b;
-        total += (int)__popcll(m) << b;
-    }
-}
-
-// Emits the first K distinct keys of each token's sorted list (duplicates are
-// adjacent) to slots [sb, sb + K), and records them as the next parents.
-// Lane li of the token handles sorted positions li*R .. li*R + R - 1.
-template <int R, int LPT>
-__device__ void emit_sorted(const DevPlan& P, int lane, int64_t t0, int ntok, const uint64_t* list, int listn,
-                            int K, int sb, int32_t* par, int kmaxp, int32_t* out_idx, float* out_coef)
-{
-    const int tt = lane / LPT, li = lane & (LPT - 1), k_tot = P.k_tot;
-    const uint64_t* row = list + tt * listn + li * R;
-    uint64_t key[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) key[r] = row[r];
-    uint64_t prev = li > 0 ? row[-1] : 0ull;
+    const int k_tot = P.k_tot;
+    const uint32_t ph = (uint32_t)__builtin_amdgcn_ds_bpermute(prev_addr, (int)(uint32_t)(key[R - 1] >> 32));
+    const uint32_t pl = (uint32_t)__builtin_amdgcn_ds_bpermute(prev_addr, (int)(uint32_t)key[R - 1]);
+    uint64_t prev = lanepos > 0 ? (((uint64_t)ph << 32) | pl) : 0ull;
     int kept = 0, cnt = 0;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
@@ -187,27 +170,32 @@ __device__ void emit_sorted(const DevPlan& P, int lane, int64_t t0, int ntok, co
         cnt += (int)k;
         prev = key[r];
     }
-    int before, total;
-    group_scan<LPT>(lane, cnt, before, total);
-    const bool live = tt < ntok;
+    int before = 0, total = 0;
+#pragma unroll
+    for (int b = 0; b < 5; ++b) {
+        const uint64_t m = __ballot((cnt >> b) & 1);
+        before += (int)__popcll(m & before_mask) << b;
+        total += (int)__popcll(m & token_mask) << b;
+    }
+    const bool live = ct < ntok;
     int rank = before;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
         if (((kept >> r) & 1) && rank < K) {
             const uint32_t ci = key_index(key[r]);
-            par[tt * kmaxp + rank] = (int32_t)ci;
+            par[ct * kmaxp + rank] = (int32_t)ci;
             if (live) {
-                out_idx[(t0 + tt) * k_tot + sb + rank] = (int32_t)ci;
-                out_coef[(t0 + tt) * k_tot + sb + rank] = key_value(key[r]);
+                out_idx[(t0 + ct) * k_tot + sb + rank] = (int32_t)ci;
+                out_coef[(t0 + ct) * k_tot + sb + rank] = key_value(key[r]);
             }
         }
         rank += (kept >> r) & 1;
     }
-    for (int r = total + li; r < K; r += LPT) {
-        par[tt * kmaxp + r] = -1;
+    for (int r = total + lanepos; r < K; r += 4 * CPT) {
+        par[ct * kmaxp + r] = -1;
         if (live) {
-            out_idx[(t0 + tt) * k_tot + sb + r] = -1;
-            out_coef[(t0 + tt) * k_tot + sb + r] = 0.f;
+            out_idx[(t0 + ct) * k_tot + sb + r] = -1;
+            out_coef[(t0 + ct) * k_tot + sb + r] = 0.f;
         }
     }
 }
@@ -222,7 +210,7 @@ __device__ void level0_bf16(const DevPlan& P, int lane, int64_t t0, int ntok, co
                             int x32addr)
 {
     const int tt = lane >> LLP, li = lane & (LPT - 1), K0 = P.active[0], dp2 = P.dp / 2;
-    const uint32_t* row = pairs + tt * dp2;
+    const uint32_t* row = pairs + tt * P.prow;
     const int lo0 = 32 * (li >> 4) + (li & 15);  // coordinate of the low half of dword li
     constexpr uint32_t STEP = 2 * LPT;           // coordinate step per dword row
     uint32_t best = 0;
@@ -335,6 +323,15 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
     const ActTile A{pairs, xf};
 
     const int col = lane & 15, kq = lane >> 4, ct = col >> CB, q = col & (CPT - 1), lanepos = q * 4 + kq;
+    // lanepos order inside a token: lanes of positions below mine, all lanes of my token, lane of lanepos - 1
+    uint64_t before_mask = 0, token_mask = 0;
+    for (int q2 = 0; q2 < CPT; ++q2)
+        for (int k2 = 0; k2 < 4; ++k2) {
+            const uint64_t bit = 1ull << (ct * CPT + q2 + 16 * k2);
+            token_mask |= bit;
+            if (q2 * 4 + k2 < lanepos) before_mask |= bit;
+        }
+    const int prev_addr = (kq > 0 ? lane - 16 : lane + 47) << 2;
 
     const int64_t ngroups = (T + TPW - 1) / TPW;
     for (int64_t grp = (int64_t)blockIdx.x * kEncWaves + wave; grp < ngroups;
@@ -381,14 +378,8 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
                 }
             }
             sort_desc<R, NB, true>(keys, lanepos, x32);
-            {
-                uint64_t* dst = list + ct * EL.listn + lanepos * R;
-#pragma unroll
-                for (int r = 0; r < R; ++r) dst[r] = keys[r];
-            }
-            wave_sync();
-            emit_sorted<R, LPT>(P, lane, t0, ntok, list, EL.listn, P.active[l], P.slot_base[l], par, EL.kmaxp,
-                                out_idx, out_coef);
+            emit_mfma<R, CPT>(P, keys, lane, lanepos, ct, prev_addr, before_mask, token_mask, t0, ntok, P.active[l],
+                              P.slot_base[l], par, EL.kmaxp, out_idx, out_coef);
             wave_sync();
         }
     }

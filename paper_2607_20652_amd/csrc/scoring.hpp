@@ -21,7 +21,7 @@ constexpr int kScoreBatch = 8;  // A fragments fetched per batch
 
 // A wave's activations in LDS.
 struct ActTile {
-    const uint32_t* pairs;  // bf16: [TPW][dp/2] signed bf16 pairs, interleaved halves
+    const uint32_t* pairs;  // bf16: [TPW][prow] signed bf16 pairs, interleaved halves
     const float* f;         // fp32: [TPW][dp]
 };
 
@@ -102,7 +102,7 @@ __device__ f32x4 mfma_scores(const DevPlan& P, int lane, int l, int mb, int trow
     const int nchunk = P.nchunk, dp = P.dp, col = lane & 15, kq = lane >> 4;
     const u32x4* Ap = (const u32x4*)P.gamma_pair + P.gamma_off[l] + (int64_t)mb * nchunk * 64 + lane;
     const uint32_t* cwp = cw + col * P.cws;
-    const uint32_t* prow = A.pairs + trow * (dp / 2) + kq * 4;
+    const uint32_t* prow = A.pairs + trow * P.prow + kq * 4;
     const float* frow = A.f + trow * dp;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     int c0 = 0;
@@ -159,7 +159,7 @@ __device__ inline void load_pairs(const DevPlan& P, int lane, int ntok, int tpw,
             w.z = __builtin_amdgcn_perm(h1, l1, 0x05040100u);
             w.w = __builtin_amdgcn_perm(h1, l1, 0x07060302u);
             const int c = o >> 5;
-            *(u32x4*)(pairs + tt * (dp / 2) + c * 16 + 8 * (h & 1) + 4 * (h >> 1)) = w;
+            *(u32x4*)(pairs + tt * P.prow + c * 16 + 8 * (h & 1) + 4 * (h >> 1)) = w;
         }
     }
 }
@@ -168,7 +168,7 @@ __device__ inline void load_pairs(const DevPlan& P, int lane, int ntok, int tpw,
 __device__ __forceinline__ float pair_value(const DevPlan& P, const uint32_t* pairs, int tt, int iota)
 {
     const int c = iota >> 5, b = iota & 31;
-    const uint32_t dw = pairs[tt * (P.dp / 2) + c * 16 + (b & 15)];
+    const uint32_t dw = pairs[tt * P.prow + c * 16 + (b & 15)];
     return bf16_bits_to_f32((b >> 4) ? (dw >> 16) : (dw & 0xFFFFu));
 }
 
