@@ -54,7 +54,6 @@ struct Wave {
     const uint32_t* mask;  // [dp] row masks (shared)
     const uint32_t* gtab;  // generator hash tables (shared): (g_j, j) pairs
     const uint32_t* gens;  // generators (shared)
-    const uint32_t* nt;    // nibble tables (shared, backward only)
 };
 
 __device__ __forceinline__ int rdlane(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
@@ -357,7 +356,7 @@ __device__ void decode_tokens(const DevPlan& P, const Wave& W, const float* cf)
 __device__ Wave make_wave(const DevPlan& P, unsigned char* smem, bool scoring, bool act_bf16, int wave, int lane)
 {
     const CodeLayout CL = code_layout(P, scoring, act_bf16);
-    unsigned char* b = smem + code_shared_bytes(P, scoring) + (unsigned)wave * CL.bytes;
+    unsigned char* b = smem + code_shared_bytes(P) + (unsigned)wave * CL.bytes;
     Wave W;
     W.lane = lane;
     W.t0 = 0;
@@ -379,11 +378,10 @@ __device__ Wave make_wave(const DevPlan& P, unsigned char* smem, bool scoring, b
     W.cw = (uint32_t*)(b + CL.cw);
     W.score = (float*)(b + CL.score);
     const unsigned o_gtab = align16u(P.dp * 4);
-    const unsigned o_gens = o_gtab + align16u(P.gtab_total * 8), o_nt = o_gens + align16u(P.gens_total * 4);
+    const unsigned o_gens = o_gtab + align16u(P.gtab_total * 8);
     W.mask = (const uint32_t*)smem;
     W.gtab = (const uint32_t*)(smem + o_gtab);
     W.gens = (const uint32_t*)(smem + o_gens);
-    W.nt = (const uint32_t*)(smem + o_nt);
     return W;
 }
 
@@ -421,20 +419,16 @@ __device__ void write_rows(const DevPlan& P, const Wave& W, void* out)
     }
 }
 
-__device__ void load_shared(const DevPlan& P, unsigned char* smem, bool with_nt)
+__device__ void load_shared(const DevPlan& P, unsigned char* smem)
 {
     const unsigned o_gtab = align16u(P.dp * 4);
-    const unsigned o_gens = o_gtab + align16u(P.gtab_total * 8), o_nt = o_gens + align16u(P.gens_total * 4);
+    const unsigned o_gens = o_gtab + align16u(P.gtab_total * 8);
     uint32_t* s_mask = (uint32_t*)smem;
     uint32_t* s_gtab = (uint32_t*)(smem + o_gtab);
     uint32_t* s_gens = (uint32_t*)(smem + o_gens);
     for (int i = threadIdx.x; i < P.dp; i += kThreads) s_mask[i] = P.masks[i];
     for (int i = threadIdx.x; i < 2 * P.gtab_total; i += kThreads) s_gtab[i] = P.gtab[i];
     for (int i = threadIdx.x; i < P.gens_total; i += kThreads) s_gens[i] = P.gens[i];
-    if (with_nt) {
-        uint32_t* s_nt = (uint32_t*)(smem + o_nt);
-        for (int i = threadIdx.x; i < P.nt_groups * 16 * P.nchunk; i += kThreads) s_nt[i] = P.nt[i];
-    }
     __syncthreads();
 }
 
@@ -458,7 +452,7 @@ __global__ __launch_bounds__(kThreads) void decode2_kernel(DevPlan P, const int3
                                                            void* __restrict__ y)
 {
     extern __shared__ __align__(16) unsigned char smem[];
-    load_shared(P, smem, false);
+    load_shared(P, smem);
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, TPW = P.wave_tokens;
     Wave W = make_wave(P, smem, false, true, wave, lane);
     const int64_t ngroups = (T + TPW - 1) / TPW;
@@ -497,7 +491,7 @@ __device__ void score_level(const DevPlan& P, const Wave& W, int l)
     const ActTile A{W.pairs, W.gf};
     const int col = lane & 15, kq = lane >> 4;
     for (int nb = 0; nb < NB; ++nb) {
-        column_bitmaps(P, lane, W.ntok, csh, nb, W.idx + sbp, k, Kp, W.nt, W.cw);
+        column_bitmaps(P, lane, W.ntok, csh, nb, W.idx + sbp, k, Kp, P.nt, W.cw);
         wave_sync();
         const int r = nb * 16 + col, tt = r >> csh, q = r & (CPT - 1);
         const bool valid = r < ncol && tt < W.ntok && q < Kp && W.idx[tt * k + sbp + q] >= 0;
@@ -527,7 +521,7 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
                                                                void* __restrict__ grad_x)
 {
     extern __shared__ __align__(16) unsigned char smem[];
-    load_shared(P, smem, true);
+    load_shared(P, smem);
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, TPW = P.wave_tokens, k = P.k_tot;
     const int d = P.d, dp = P.dp;
     Wave W = make_wave(P, smem, true, G_BF16, wave, lane);
@@ -594,7 +588,7 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
 
 size_t code_lds_bytes(const DevPlan& P, bool scoring, bool act_bf16)
 {
-    return code_shared_bytes(P, scoring) + (size_t)kCodeWaves * code_layout(P, scoring, act_bf16).bytes;
+    return code_shared_bytes(P) + (size_t)kCodeWaves * code_layout(P, scoring, act_bf16).bytes;
 }
 
 int device_cus()

@@ -125,11 +125,10 @@ __host__ __device__ inline CodeLayout code_layout(const DevPlan& P, bool with_sc
 constexpr int kCodeWaves = 4;  // waves per workgroup in the code kernels
 
 // Shared (per-workgroup) LDS of the code kernels: row masks, generator hash
-// tables and generators, then (backward only) nibble tables.
-__host__ __device__ inline unsigned code_shared_bytes(const DevPlan& P, bool with_nt)
+// tables and generators.  (The nibble tables are read through the cache.)
+__host__ __device__ inline unsigned code_shared_bytes(const DevPlan& P)
 {
-    const unsigned b = align16u(P.dp * 4) + align16u(P.gtab_total * 8) + align16u(P.gens_total * 4) +
-                       (with_nt ? align16u(P.nt_groups * 16 * P.nchunk * 4) : 0u);
+    const unsigned b = align16u(P.dp * 4) + align16u(P.gtab_total * 8) + align16u(P.gens_total * 4);
     return (b + 255u) & ~255u;
 }
 

@@ -68,6 +68,7 @@ __host__ __device__ inline EncLayout enc_layout(const DevPlan& P, bool act_bf16)
     return L;
 }
 
+// Shared LDS of an encoder workgroup: nibble tables and generators.
 __host__ __device__ inline unsigned enc_shared_bytes(const DevPlan& P)
 {
     return align16u(P.nt_groups * 16 * P.nchunk * 4) + align16u(P.gens_total * 4);
