@@ -32,6 +32,8 @@ from paper_2607_20652_amd import inputs  # noqa: E402
 
 METRIC = "DPB fwd+bwd tokens/sec at d=768,N=2^20,k=64; % of HBM/VALU roofline"
 HBM_PEAK_GBS = 8000.0
+VALU_PEAK_TFLOPS = 157.3    # fp32 vector, 256 CUs at 2.4 GHz
+MFMA_BF16_PEAK_TFLOPS = 2500.0
 CSRC = os.path.join(ROOT, "paper_2607_20652_amd", "csrc")
 COPY_BYTES = 256 << 20      # size of the plain copy that calibrates the HBM byte counters
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
@@ -95,6 +97,19 @@ def algorithmic_bytes_per_token(w, k_tot: int) -> dict:
         "decode": k_tot * 8 + w.d * xb,                    # read (idx, coef), write y
         "decode_bwd": k_tot * 4 + w.d * xb + k_tot * 4 + w.d * xb,  # read idx, g; write grad_coef, grad_x
     }
+
+
+def algorithmic_flops_per_token(w, plan_k_tot: int, hier) -> dict:
+    """Arithmetic the method must do per token, 2 flops per multiply-add.
+
+    encode: child scoring, sum over levels l >= 1 of K_{l-1} Delta_l d +-1 products
+    (a dense contraction, on the matrix cores); decode: one signed add per hashed
+    slot and coordinate; decode_bwd: the same for grad_coef and again for grad_x.
+    """
+    nbits, delta, active = hier
+    hashed = plan_k_tot - active[0]
+    score = sum(active[l - 1] * delta[l] for l in range(1, len(active))) * w.d
+    return {"encode": 2 * score, "decode": 2 * hashed * w.d, "decode_bwd": 4 * hashed * w.d}
 
 
 def load_traffic(kernel: str, tokens: int):
@@ -243,21 +258,35 @@ def main() -> int:
                      for j, n in enumerate(names)}
 
     bpt = algorithmic_bytes_per_token(w, k)
+    fpt = algorithmic_flops_per_token(w, k, dpb.hierarchy(w.d, w.n, w.levels, w.branching, w.beam, w.k))
     timed = [n for n in names if run[n]]
     dom = max(timed, key=lambda n: per_kernel_ms[n])
-    achieved = bpt[dom] * T / (per_kernel_ms[dom] * 1e-3) / 1e9
-    traffic = load_traffic(dom, T)
+    per_kernel = {}
+    for n in timed:
+        sec = per_kernel_ms[n] * 1e-3
+        hbm = bpt[n] * T / sec / 1e9
+        tfl = fpt[n] * T / sec / 1e12
+        peak = MFMA_BF16_PEAK_TFLOPS if n == "encode" else VALU_PEAK_TFLOPS
+        per_kernel[n] = {"ms": round(per_kernel_ms[n], 4), "hbm_GBps": round(hbm, 1),
+                         "hbm_frac": round(hbm / HBM_PEAK_GBS, 4), "tflops": round(tfl, 2),
+                         "compute_peak_tflops": peak, "compute_frac": round(tfl / peak, 4)}
+    # decode and decode-backward are bound by the vector ALU (sign generation and
+    # signed accumulation); the encoder's contraction runs on the matrix cores
+    bound = "mfma" if dom == "encode" else "alu"
     roofline = {
         "kernel": dom,
-        "bound": "hbm",
-        "achieved": round(achieved, 2),
-        "peak": HBM_PEAK_GBS,
-        "unit": "GB/s",
-        "frac": round(achieved / HBM_PEAK_GBS, 4),
-        "traffic": traffic,
+        "bound": bound,
+        "achieved": per_kernel[dom]["tflops"],
+        "peak": per_kernel[dom]["compute_peak_tflops"],
+        "unit": "TFLOP/s",
+        "frac": per_kernel[dom]["compute_frac"],
+        "traffic": load_traffic(dom, T),
+        "algorithmic_flops_per_launch": fpt[dom] * T,
         "algorithmic_bytes_per_launch": bpt[dom] * T,
+        "hbm_achieved_GBps": per_kernel[dom]["hbm_GBps"],
+        "hbm_frac": per_kernel[dom]["hbm_frac"],
         "avg_launch_ms": round(per_kernel_ms[dom], 4),
-        "per_kernel_ms": {n: round(v, 4) for n, v in per_kernel_ms.items() if run[n]},
+        "per_kernel": per_kernel,
     }
 
     out = {
