@@ -172,6 +172,7 @@ __device__ void fr_chunk(const DevPlan& P, const Wave& W, int tt, int n, bool fi
     float* yt = W.y + tt * dp;
     const int w0 = pbpos >> 5, sh = pbpos & 31;
     const uint32_t pmask = pbn >= 32 ? ~0u : ((1u << pbn) - 1u);
+#pragma unroll 2
     for (int iota = lane; iota < dp; iota += 64) {
         // 4 x nibble g of the row mask: even groups in s0, odd groups in s1, byte g / 2
         const uint32_t M = W.mask[iota];
@@ -189,7 +190,7 @@ __device__ void fr_chunk(const DevPlan& P, const Wave& W, int tt, int n, bool fi
             for (int i8 = 0; i8 < 8; ++i8) {
                 // frt is 64-byte aligned: the nibble goes in with one and-or
                 const uint32_t sh4 = i8 == 0 ? (U << 2) : (U >> (4 * i8 - 2));
-                acc += lds_ldf((sh4 & 0x3Cu) | tb + (uint32_t)(i8 * 64));
+                acc += lds_ldf(((sh4 & 0x3Cu) | tb) + (uint32_t)(i8 * 64));
             }
             lo = w == w0 ? U : lo;
             hi = w == w0 + 1 ? U : hi;
