@@ -59,6 +59,10 @@ def _load():
         "oracle_decode": (None, [i32, P, i32, P, P, i64, P]),
         "oracle_decode_bwd": (None, [i32, P, i32, P, P, i64, P, P]),
         "oracle_walsh_spectrum": (i32, [i32, P, i32, P]),
+        "oracle_normalize": (None, [i32, i64, P, P, P, P]),
+        "oracle_normalize_bwd": (None, [i32, i64, P, P, P, P, P]),
+        "oracle_edit_codes": (None, [i64, i32, P, P, i32, P, P, P, P]),
+        "oracle_variance_loss": (dbl, [i64, i32, P, P, i32, P]),
         "oracle_num_threads": (i32, []),
     }
     for name, (res, args) in sig.items():
@@ -216,6 +220,61 @@ def decode_bwd(d: int, m: np.ndarray, idx: np.ndarray, g: np.ndarray):
     gx = np.zeros((T, d), dtype=np.float64)
     _load().oracle_decode_bwd(d, _ptr(m), k, _ptr(idx), _ptr(g), T, _ptr(gc), _ptr(gx))
     return gc, gx
+
+
+def normalize(u: np.ndarray, ref: np.ndarray):
+    """Normalized reconstruction (§2.2): y = u ||ref|| / ||u|| per row (0 when
+    ||u|| = 0), fp64.  Returns y and norms [T, 2] = (||ref||, ||u||)."""
+    u = np.ascontiguousarray(u, dtype=np.float64)
+    ref = np.ascontiguousarray(ref, dtype=np.float64)
+    T, d = u.shape
+    y = np.zeros_like(u)
+    norms = np.zeros((T, 2), dtype=np.float64)
+    _load().oracle_normalize(d, T, _ptr(u), _ptr(ref), _ptr(y), _ptr(norms))
+    return y, norms
+
+
+def normalize_bwd(g: np.ndarray, u: np.ndarray, ref: np.ndarray):
+    """Backward of `normalize` for dL/dy = g: returns (dL/du, dL/dref), fp64."""
+    g = np.ascontiguousarray(g, dtype=np.float64)
+    u = np.ascontiguousarray(u, dtype=np.float64)
+    ref = np.ascontiguousarray(ref, dtype=np.float64)
+    T, d = u.shape
+    gu = np.zeros_like(u)
+    gr = np.zeros_like(u)
+    _load().oracle_normalize_bwd(d, T, _ptr(g), _ptr(u), _ptr(ref), _ptr(gu), _ptr(gr))
+    return gu, gr
+
+
+def edit_codes(idx: np.ndarray, coef: np.ndarray, edits):
+    """Applies edits [(feature, op, value, new_index)] in order to every slot
+    holding `feature` (op 0 zero, 1 rescale, 2 set, 3 replace index).
+    Returns edited copies (idx int32, coef fp64)."""
+    idx = np.array(idx, dtype=np.int32, order="C")
+    coef = np.array(coef, dtype=np.float64, order="C")
+    T, k = idx.shape
+    n = len(edits)
+    feat = np.array([e[0] for e in edits] or [0], dtype=np.int32)
+    op = np.array([e[1] for e in edits] or [0], dtype=np.int32)
+    val = np.array([e[2] for e in edits] or [0.0], dtype=np.float64)
+    new = np.array([e[3] for e in edits] or [0], dtype=np.int32)
+    _load().oracle_edit_codes(T, k, _ptr(idx), _ptr(coef), n, _ptr(feat), _ptr(op), _ptr(val), _ptr(new))
+    return idx, coef
+
+
+def variance_loss(idx: np.ndarray, coef: np.ndarray, n_min: int):
+    """Variance auxiliary loss (§2.2) and its gradient with respect to coef.
+
+    Population variance per feature over the slots holding it; features with
+    fewer than n_min samples are left out (the variance estimator and the
+    treatment of a feature repeated within one token are readings).
+    """
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    coef = np.ascontiguousarray(coef, dtype=np.float64)
+    T, k = idx.shape
+    grad = np.zeros((T, k), dtype=np.float64)
+    loss = _load().oracle_variance_loss(T, k, _ptr(idx), _ptr(coef), int(n_min), _ptr(grad))
+    return float(loss), grad
 
 
 def num_threads() -> int:

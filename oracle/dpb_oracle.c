@@ -493,6 +493,131 @@ int oracle_walsh_spectrum(int d, const uint32_t* masks, int r, int64_t* S)
     return 0;
 }
 
+/* ------------------------------------------------------------------ */
+/* Normalized reconstruction (§2.2 "Normalized Reconstruction"): the    */
+/* decoder output u of each row is rescaled to the norm of the          */
+/* bottleneck input ref of that row,  y = u ||ref|| / ||u||  (y = 0 when */
+/* ||u|| = 0).  norms[t] = (||ref_t||, ||u_t||).                         */
+/* ------------------------------------------------------------------ */
+void oracle_normalize(int d, int64_t T, const double* u, const double* ref, double* y, double* norms)
+{
+    for (int64_t t = 0; t < T; ++t) {
+        double su = 0.0, sr = 0.0;
+        for (int i = 0; i < d; ++i) {
+            su += u[t * d + i] * u[t * d + i];
+            sr += ref[t * d + i] * ref[t * d + i];
+        }
+        const double nu = sqrt(su), nr = sqrt(sr);
+        norms[2 * t] = nr;
+        norms[2 * t + 1] = nu;
+        for (int i = 0; i < d; ++i) y[t * d + i] = nu > 0.0 ? u[t * d + i] * (nr / nu) : 0.0;
+    }
+}
+
+/* Backward of the row normalization for dL/dy = g:
+ *   dL/du   = (||ref|| / ||u||) (g - (<g, u> / ||u||^2) u)
+ *   dL/dref = (<g, u> / (||u|| ||ref||)) ref
+ * both 0 where ||u|| = 0, and dL/dref = 0 where ||ref|| = 0. */
+void oracle_normalize_bwd(int d, int64_t T, const double* g, const double* u, const double* ref, double* gu,
+                          double* gref)
+{
+    for (int64_t t = 0; t < T; ++t) {
+        double su = 0.0, sr = 0.0, gdu = 0.0;
+        for (int i = 0; i < d; ++i) {
+            su += u[t * d + i] * u[t * d + i];
+            sr += ref[t * d + i] * ref[t * d + i];
+            gdu += g[t * d + i] * u[t * d + i];
+        }
+        const double nu = sqrt(su), nr = sqrt(sr);
+        for (int i = 0; i < d; ++i) {
+            gu[t * d + i] = nu > 0.0 ? (nr / nu) * (g[t * d + i] - (gdu / su) * u[t * d + i]) : 0.0;
+            gref[t * d + i] = (nu > 0.0 && nr > 0.0) ? gdu / (nu * nr) * ref[t * d + i] : 0.0;
+        }
+    }
+}
+
+/* Code edits (App. feature-edit experiments: zero, rescale, set or
+ * replace a feature in place).  Edits apply in order to every slot whose
+ * index equals the edit's feature: op 0 sets the coefficient to 0, op 1
+ * multiplies it by value, op 2 sets it to value, op 3 replaces the index
+ * by new_index and keeps the coefficient. */
+void oracle_edit_codes(int64_t T, int k, int32_t* idx, double* coef, int n, const int32_t* feat, const int32_t* op,
+                       const double* val, const int32_t* newidx)
+{
+    for (int64_t s = 0; s < T * (int64_t)k; ++s)
+        for (int e = 0; e < n; ++e) {
+            if (idx[s] != feat[e]) continue;
+            if (op[e] == 0) coef[s] = 0.0;
+            else if (op[e] == 1) coef[s] = coef[s] * val[e];
+            else if (op[e] == 2) coef[s] = val[e];
+            else if (op[e] == 3) idx[s] = newidx[e];
+        }
+}
+
+/* Variance auxiliary loss (§2.2 "Auxillary losses" equation): for each
+ * feature i, the coefficients a_i^(t) of the slots holding i across the
+ * batch form a sample; F = features with at least n_min samples;
+ *     L = -(1/|F|) sum_{i in F} Var_i,   Var_i = mean(a^2) - mean(a)^2,
+ * and L = 0 when F is empty.  grad[s] = dL/dcoef[s]
+ *     = -(2 / |F|) (a_s - mean_i) / count_i   for the slots of i in F, else 0.
+ * Padding slots (index < 0) are not samples. */
+typedef struct {
+    int32_t i;
+    int64_t s;
+} oracle_slot;
+
+static int slot_cmp(const void* a, const void* b)
+{
+    const oracle_slot* x = (const oracle_slot*)a;
+    const oracle_slot* y = (const oracle_slot*)b;
+    if (x->i != y->i) return x->i < y->i ? -1 : 1;
+    return x->s < y->s ? -1 : (x->s > y->s);
+}
+
+double oracle_variance_loss(int64_t T, int k, const int32_t* idx, const double* coef, int n_min, double* grad)
+{
+    const int64_t n = T * (int64_t)k;
+    oracle_slot* v = (oracle_slot*)malloc((size_t)(n > 0 ? n : 1) * sizeof(oracle_slot));
+    int64_t m = 0;
+    for (int64_t s = 0; s < n; ++s) {
+        grad[s] = 0.0;
+        if (idx[s] >= 0) {
+            v[m].i = idx[s];
+            v[m].s = s;
+            ++m;
+        }
+    }
+    qsort(v, (size_t)m, sizeof(oracle_slot), slot_cmp);
+    /* pass 1: |F|;  pass 2: sum of variances and gradients */
+    int64_t nF = 0;
+    for (int64_t a = 0; a < m;) {
+        int64_t b = a;
+        while (b < m && v[b].i == v[a].i) ++b;
+        if (b - a >= n_min) ++nF;
+        a = b;
+    }
+    double total = 0.0;
+    for (int64_t a = 0; a < m;) {
+        int64_t b = a;
+        while (b < m && v[b].i == v[a].i) ++b;
+        const int64_t c = b - a;
+        if (c >= n_min && nF > 0) {
+            double s1 = 0.0, s2 = 0.0;
+            for (int64_t q = a; q < b; ++q) {
+                s1 += coef[v[q].s];
+                s2 += coef[v[q].s] * coef[v[q].s];
+            }
+            const double mean = s1 / (double)c;
+            total += s2 / (double)c - mean * mean;
+            for (int64_t q = a; q < b; ++q)
+                grad[v[q].s] = -2.0 / (double)nF * (coef[v[q].s] - mean) / (double)c;
+        }
+        a = b;
+    }
+    free(v);
+    return nF > 0 ? -total / (double)nF : 0.0;
+}
+
 /* Threads the OpenMP loops above use (reported next to timings). */
 #include <omp.h>
 int oracle_num_threads(void)
