@@ -133,6 +133,106 @@ dpb_status dpb_decode_bwd(const dpb_plan* plan, const int32_t* idx, const void* 
                           dpb_dtype g_dtype, int64_t T, float* grad_coef, void* grad_x,
                           dpb_dtype gx_dtype, void* stream);
 
+/* DECODE BACKWARD with extra gradient terms, for a layer whose loss also
+ * depends on the coefficients directly (the variance auxiliary loss of §2.2,
+ * "Auxillary losses") and on the bottleneck input through a path other than
+ * the code (the norm of the normalized reconstruction, §2.2 "Normalized
+ * Reconstruction"):
+ *   grad_coef[s] = <phi_{idx_s}, g> + add_grad_coef[s]
+ *   grad_x       = sum_s grad_coef[s] * phi_{idx_s} + add_grad_x
+ *   add_grad_coef : device [T, k_tot] fp32, or NULL for none (read)
+ *   add_grad_x    : device [T, d] in gx_dtype, or NULL for none (read); may
+ *                   be the same buffer as grad_x (each element is read
+ *                   before it is written, by the same thread).
+ * Every other argument as in dpb_decode_bwd; with both extras NULL the
+ * results equal dpb_decode_bwd's. */
+dpb_status dpb_decode_bwd_ex(const dpb_plan* plan, const int32_t* idx, const void* grad_y,
+                             dpb_dtype g_dtype, int64_t T, const float* add_grad_coef,
+                             const void* add_grad_x, float* grad_coef, void* grad_x,
+                             dpb_dtype gx_dtype, void* stream);
+
+/* NORMALIZED RECONSTRUCTION (§2.2 "Normalized Reconstruction"): each row of
+ * the decoder output u is rescaled to the norm of the bottleneck input,
+ *   y_t = u_t * ||ref_{r(t)}|| / ||u_t||,   y_t = 0 where ||u_t|| = 0,
+ * with r(t) = ref_rows[t] if ref_rows is given, else t (the greedy feature
+ * editing of App. C.3 rescales edited codes to their source row's norm).
+ *   u        : device [T, d], u_dtype (read)
+ *   ref      : device [T_ref, d], ref_dtype (read)
+ *   ref_rows : device [T] int32, or NULL (then T_ref must equal T); a row
+ *              index outside [0, T_ref) counts as a reference of norm 0
+ *   y        : device [T, d], y_dtype (written; may be the same buffer as u
+ *              when u_dtype == y_dtype)
+ *   norms    : device [T, 2] fp32 (||ref_{r(t)}||, ||u_t||), or NULL
+ * Sums of squares accumulate in fp32.  d comes from the plan. */
+dpb_status dpb_normalize(const dpb_plan* plan, const void* u, dpb_dtype u_dtype, const void* ref,
+                         dpb_dtype ref_dtype, const int32_t* ref_rows, int64_t T_ref, int64_t T,
+                         void* y, dpb_dtype y_dtype, float* norms, void* stream);
+
+/* Backward of dpb_normalize (ref_rows = NULL) for upstream gradient g of y:
+ *   grad_u   = (||ref|| / ||u||) (g - (<g,u> / ||u||^2) u)
+ *   grad_ref = (<g,u> / (||u|| ||ref||)) ref        (added to grad_ref when
+ *                                                    accumulate != 0)
+ * both 0 where ||u|| = 0, and grad_ref = 0 where ||ref|| = 0.
+ *   g, u, ref        : device [T, d] in their dtypes (read)
+ *   grad_u, grad_ref : device [T, d] in their dtypes (written; must not
+ *                      overlap each other or the inputs) */
+dpb_status dpb_normalize_bwd(const dpb_plan* plan, const void* g, dpb_dtype g_dtype, const void* u,
+                             dpb_dtype u_dtype, const void* ref, dpb_dtype ref_dtype, int64_t T,
+                             void* grad_u, dpb_dtype gu_dtype, void* grad_ref, dpb_dtype gr_dtype,
+                             int accumulate, void* stream);
+
+/* Operations of the greedy feature editing of App. C.3 (fine-grained causal
+ * intervention); each edits one slot position of a source code using a
+ * target code. */
+typedef enum {
+    DPB_EDIT_ZERO = 0,    /* coefficient := 0 */
+    DPB_EDIT_REPLACE = 1, /* index and coefficient := the target's at the same position */
+    DPB_EDIT_RESCALE = 2, /* coefficient := the target's at the same position; index kept */
+    DPB_EDIT_NONE = 3     /* unchanged copy of the source row */
+} dpb_edit_op;
+
+/* CODE EDITS: one output code per edit e, equal to source row rows[e] with
+ * the slot at position slots[e] (a column of the level-major code) changed by
+ * ops[e].  Slots at the same position belong to the same level, so a
+ * replaced index stays in that level's index range.
+ *   idx, coef         : device [T, k_tot] source code (read)
+ *   tgt_idx, tgt_coef : device [T, k_tot] target code (read), or both NULL
+ *                       (then only ZERO and NONE are valid)
+ *   rows, slots, ops  : device [E] int32 (read)
+ *   out_idx, out_coef : device [E, k_tot] (written; must not overlap the
+ *                       inputs)
+ * An edit whose row, slot or op is out of range (or needs the missing
+ * target) yields an all-padding output row (idx -1, coef 0): edit lists live
+ * on the device and are not inspected by the host. */
+dpb_status dpb_edit_codes(const dpb_plan* plan, const int32_t* idx, const float* coef,
+                          const int32_t* tgt_idx, const float* tgt_coef, int64_t T,
+                          const int32_t* rows, const int32_t* slots, const int32_t* ops, int64_t E,
+                          int32_t* out_idx, float* out_coef, void* stream);
+
+/* Bytes of device workspace dpb_variance_loss needs: 12 * 2^n_last + 32,
+ * where 2^n_last is the number of features N; 0 for a NULL plan. */
+size_t dpb_variance_workspace_bytes(const dpb_plan* plan);
+
+/* VARIANCE AUXILIARY LOSS (§2.2 "Auxillary losses" equation) over a batch of
+ * codes: the coefficients of the slots holding feature i form its sample;
+ * F = features with at least n_min samples;
+ *   loss = -(1/|F|) sum_{i in F} Var_i      (population variance; 0 if F is empty)
+ *   grad_coef[s] = d loss / d coef[s] = -(2/|F|) (coef[s] - mean_i) / count_i
+ *                  for slots of features in F, else 0.
+ * Slots whose index is outside [0, N) (padding) are not samples.
+ *   idx, coef : device [T, k_tot] (read)
+ *   workspace : device, >= dpb_variance_workspace_bytes(plan), 16-B aligned;
+ *               caller-owned scratch, overwritten (cleared by the call itself)
+ *   loss       : device fp32 scalar (written)
+ *   grad_coef  : device [T, k_tot] fp32 (written), or NULL for the loss only
+ *   grad_scale : device fp32 scalar multiplying grad_coef (the upstream
+ *                gradient of the loss in a backward pass), or NULL for 1
+ * Per-feature sums accumulate with fp32 atomics (their order, and so the last
+ * bits, vary from run to run); the sum over features in fp64. */
+dpb_status dpb_variance_loss(const dpb_plan* plan, const int32_t* idx, const float* coef, int64_t T,
+                             int n_min, void* workspace, size_t ws_bytes, float* loss, float* grad_coef,
+                             const float* grad_scale, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

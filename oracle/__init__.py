@@ -25,8 +25,10 @@ _lib = None
 
 
 def build(force: bool = False) -> str:
-    """Compile the oracle with gcc -O2 -fopenmp into oracle/liboracle.so."""
-    if force or not os.path.exists(_LIB_PATH):
+    """Compile the oracle with gcc -O2 -fopenmp into oracle/liboracle.so
+    (again whenever the C source is newer than the library)."""
+    stale = not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC)
+    if force or stale:
         tmp = _LIB_PATH + ".tmp"
         cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", _SRC, "-o", tmp, "-lm"]
         subprocess.run(cmd, check=True)
@@ -61,7 +63,7 @@ def _load():
         "oracle_walsh_spectrum": (i32, [i32, P, i32, P]),
         "oracle_normalize": (None, [i32, i64, P, P, P, P]),
         "oracle_normalize_bwd": (None, [i32, i64, P, P, P, P, P]),
-        "oracle_edit_codes": (None, [i64, i32, P, P, i32, P, P, P, P]),
+        "oracle_edit_codes": (None, [i64, i32, P, P, P, P, i64, P, P, P, P, P]),
         "oracle_variance_loss": (dbl, [i64, i32, P, P, i32, P]),
         "oracle_num_threads": (i32, []),
     }
@@ -246,20 +248,30 @@ def normalize_bwd(g: np.ndarray, u: np.ndarray, ref: np.ndarray):
     return gu, gr
 
 
-def edit_codes(idx: np.ndarray, coef: np.ndarray, edits):
-    """Applies edits [(feature, op, value, new_index)] in order to every slot
-    holding `feature` (op 0 zero, 1 rescale, 2 set, 3 replace index).
-    Returns edited copies (idx int32, coef fp64)."""
-    idx = np.array(idx, dtype=np.int32, order="C")
-    coef = np.array(coef, dtype=np.float64, order="C")
+def edit_codes(idx: np.ndarray, coef: np.ndarray, tidx: np.ndarray, tcoef: np.ndarray, edits):
+    """Edit candidates of the greedy feature editing (App. C.3).
+
+    idx/coef is the source code [T, k], tidx/tcoef the target code of the same
+    shape; edits is a list of (row, slot, op).  Output row e is source row
+    `row` with slot `slot` edited: op 0 zero the coefficient, 1 replace index
+    and coefficient by the target's at that position, 2 rescale (take the
+    target's coefficient, keep the index), 3 no change.  Out-of-range edits
+    give an all-padding row.  Returns (idx int32 [E, k], coef fp64 [E, k])."""
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    coef = np.ascontiguousarray(coef, dtype=np.float64)
+    tidx = np.ascontiguousarray(tidx, dtype=np.int32)
+    tcoef = np.ascontiguousarray(tcoef, dtype=np.float64)
     T, k = idx.shape
-    n = len(edits)
-    feat = np.array([e[0] for e in edits] or [0], dtype=np.int32)
-    op = np.array([e[1] for e in edits] or [0], dtype=np.int32)
-    val = np.array([e[2] for e in edits] or [0.0], dtype=np.float64)
-    new = np.array([e[3] for e in edits] or [0], dtype=np.int32)
-    _load().oracle_edit_codes(T, k, _ptr(idx), _ptr(coef), n, _ptr(feat), _ptr(op), _ptr(val), _ptr(new))
-    return idx, coef
+    assert tidx.shape == (T, k) and tcoef.shape == (T, k)
+    E = len(edits)
+    rows = np.array([e[0] for e in edits] or [0], dtype=np.int32)
+    slots = np.array([e[1] for e in edits] or [0], dtype=np.int32)
+    ops = np.array([e[2] for e in edits] or [0], dtype=np.int32)
+    out_idx = np.zeros((max(E, 1), k), dtype=np.int32)
+    out_coef = np.zeros((max(E, 1), k), dtype=np.float64)
+    _load().oracle_edit_codes(T, k, _ptr(idx), _ptr(coef), _ptr(tidx), _ptr(tcoef), E, _ptr(rows), _ptr(slots),
+                              _ptr(ops), _ptr(out_idx), _ptr(out_coef))
+    return out_idx[:E], out_coef[:E]
 
 
 def variance_loss(idx: np.ndarray, coef: np.ndarray, n_min: int):
@@ -275,6 +287,28 @@ def variance_loss(idx: np.ndarray, coef: np.ndarray, n_min: int):
     grad = np.zeros((T, k), dtype=np.float64)
     loss = _load().oracle_variance_loss(T, k, _ptr(idx), _ptr(coef), int(n_min), _ptr(grad))
     return float(loss), grad
+
+
+def layer_backward(d: int, m: np.ndarray, idx: np.ndarray, coef: np.ndarray, x: np.ndarray, gy: np.ndarray,
+                   gloss: float, n_min: int, normalized: bool = True):
+    """Gradients of a DPB layer with the indices held fixed (coef = Phi_S x,
+    u = Phi_S^T coef, y = u ||x|| / ||u|| when normalized, else y = u) under
+    the loss <gy, y> + gloss * L_var(coef), composed from the oracle's parts:
+        gu, gref  = normalize_bwd(gy, u, x)            (gu = gy, gref = 0 if not normalized)
+        grad_coef = Phi_S^T gu + gloss * dL_var/dcoef
+        grad_x    = Phi_S grad_coef + gref
+    Returns (grad_coef [T, k], grad_x [T, d]) in fp64."""
+    x = np.asarray(x, dtype=np.float64)
+    gy = np.asarray(gy, dtype=np.float64)
+    u = decode(d, m, idx, coef)
+    if normalized:
+        gu, gref = normalize_bwd(gy, u, x)
+    else:
+        gu, gref = gy, np.zeros_like(x)
+    gc, gx = decode_bwd(d, m, idx, gu)
+    _, vg = variance_loss(idx, coef, n_min)
+    extra = gloss * vg
+    return gc + extra, gx + decode(d, m, idx, extra) + gref
 
 
 def num_threads() -> int:

@@ -536,22 +536,37 @@ void oracle_normalize_bwd(int d, int64_t T, const double* g, const double* u, co
     }
 }
 
-/* Code edits (App. feature-edit experiments: zero, rescale, set or
- * replace a feature in place).  Edits apply in order to every slot whose
- * index equals the edit's feature: op 0 sets the coefficient to 0, op 1
- * multiplies it by value, op 2 sets it to value, op 3 replaces the index
- * by new_index and keeps the coefficient. */
-void oracle_edit_codes(int64_t T, int k, int32_t* idx, double* coef, int n, const int32_t* feat, const int32_t* op,
-                       const double* val, const int32_t* newidx)
+/* Code edits of the greedy feature editing (App. C.3): a source code and a
+ * target code of the same shape; each edit names a source row, a slot
+ * position (level and rank within the level, i.e. a column of the code) and
+ * an operation, and yields one output row: the source row with that one slot
+ * changed.  op 0 (zero) sets the slot's coefficient to 0; op 1 (replace)
+ * takes both index and coefficient from the target at the same position;
+ * op 2 (rescale) keeps the index and takes the target's coefficient; op 3
+ * changes nothing.  An edit whose row, slot or op is out of range yields an
+ * all-padding row (index -1, coefficient 0). */
+void oracle_edit_codes(int64_t T, int k, const int32_t* idx, const double* coef, const int32_t* tidx,
+                       const double* tcoef, int64_t E, const int32_t* rows, const int32_t* slots, const int32_t* ops,
+                       int32_t* out_idx, double* out_coef)
 {
-    for (int64_t s = 0; s < T * (int64_t)k; ++s)
-        for (int e = 0; e < n; ++e) {
-            if (idx[s] != feat[e]) continue;
-            if (op[e] == 0) coef[s] = 0.0;
-            else if (op[e] == 1) coef[s] = coef[s] * val[e];
-            else if (op[e] == 2) coef[s] = val[e];
-            else if (op[e] == 3) idx[s] = newidx[e];
+    for (int64_t e = 0; e < E; ++e) {
+        const int64_t r = rows[e];
+        const int p = slots[e], op = ops[e];
+        const int ok = r >= 0 && r < T && p >= 0 && p < k && op >= 0 && op <= 3;
+        for (int s = 0; s < k; ++s) {
+            int32_t i = ok ? idx[r * k + s] : -1;
+            double c = ok ? coef[r * k + s] : 0.0;
+            if (ok && s == p) {
+                if (op == 0) c = 0.0;
+                else if (op == 1) {
+                    i = tidx[r * k + s];
+                    c = tcoef[r * k + s];
+                } else if (op == 2) c = tcoef[r * k + s];
+            }
+            out_idx[e * k + s] = i;
+            out_coef[e * k + s] = c;
         }
+    }
 }
 
 /* Variance auxiliary loss (§2.2 "Auxillary losses" equation): for each

@@ -16,6 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 lib_path = os.path.join(_HERE, "libdpb.so")
 
 DPB_F32, DPB_BF16 = 0, 1
+EDIT_ZERO, EDIT_REPLACE, EDIT_RESCALE, EDIT_NONE = 0, 1, 2, 3
 _STATUS = {0: "DPB_OK", -1: "DPB_EINVAL", -2: "DPB_EUNSUPPORTED", -3: "DPB_EHIP", -4: "DPB_ENOMEM"}
 MAX_LEVELS = 8
 
@@ -49,6 +50,12 @@ def load():
         "dpb_encode": (i32, [P, P, i32, i64, P, P, P]),
         "dpb_decode": (i32, [P, P, P, i64, P, i32, P]),
         "dpb_decode_bwd": (i32, [P, P, P, i32, i64, P, P, i32, P]),
+        "dpb_decode_bwd_ex": (i32, [P, P, P, i32, i64, P, P, P, P, i32, P]),
+        "dpb_normalize": (i32, [P, P, i32, P, i32, P, i64, i64, P, i32, P, P]),
+        "dpb_normalize_bwd": (i32, [P, P, i32, P, i32, P, i32, i64, P, i32, P, i32, i32, P]),
+        "dpb_edit_codes": (i32, [P, P, P, P, P, i64, P, P, P, i64, P, P, P]),
+        "dpb_variance_workspace_bytes": (ctypes.c_size_t, [P]),
+        "dpb_variance_loss": (i32, [P, P, P, i64, i32, P, ctypes.c_size_t, P, P, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -212,3 +219,108 @@ def forward(plan: Plan, x: torch.Tensor, out_dtype: torch.dtype | None = None):
     """encode then decode: x -> (idx, coef, y)."""
     idx, coef = encode(plan, x)
     return idx, coef, decode(plan, idx, coef, out_dtype or x.dtype)
+
+
+def _opt(t: torch.Tensor | None, name: str):
+    return None if t is None else _dev(t, name)
+
+
+def decode_bwd_ex(plan: Plan, idx: torch.Tensor, grad_y: torch.Tensor, add_grad_coef: torch.Tensor | None = None,
+                  add_grad_x: torch.Tensor | None = None, gx_dtype: torch.dtype | None = None,
+                  grad_coef: torch.Tensor | None = None, grad_x: torch.Tensor | None = None):
+    """decode_bwd plus extra terms: grad_coef = Phi^T g + add_grad_coef,
+    grad_x = Phi grad_coef + add_grad_x (add_grad_x in grad_x's dtype; it may
+    be grad_x itself)."""
+    T = idx.shape[0]
+    assert idx.dtype == torch.int32 and idx.shape[1] == plan.k_tot and grad_y.shape == (T, plan.d)
+    if grad_coef is None:
+        grad_coef = torch.empty((T, plan.k_tot), dtype=torch.float32, device=idx.device)
+    if grad_x is None:
+        grad_x = torch.empty((T, plan.d), dtype=gx_dtype or grad_y.dtype, device=idx.device)
+    if add_grad_coef is not None:
+        assert add_grad_coef.dtype == torch.float32 and add_grad_coef.shape == (T, plan.k_tot)
+    if add_grad_x is not None:
+        assert add_grad_x.dtype == grad_x.dtype and add_grad_x.shape == (T, plan.d)
+    _check("dpb_decode_bwd_ex", load().dpb_decode_bwd_ex(
+        plan._handle, _dev(idx, "idx"), _dev(grad_y, "grad_y"), _dtype_code(grad_y), T,
+        _opt(add_grad_coef, "add_grad_coef"), _opt(add_grad_x, "add_grad_x"), _dev(grad_coef, "grad_coef"),
+        _dev(grad_x, "grad_x"), _dtype_code(grad_x), _stream(idx)))
+    return grad_coef, grad_x
+
+
+def normalize(plan: Plan, u: torch.Tensor, ref: torch.Tensor, ref_rows: torch.Tensor | None = None,
+              out_dtype: torch.dtype | None = None, y: torch.Tensor | None = None, with_norms: bool = False):
+    """y = u ||ref_r|| / ||u|| per row (r = ref_rows[t] or t); optionally the
+    (||ref_r||, ||u||) pairs [T, 2]."""
+    T = u.shape[0]
+    assert u.shape == (T, plan.d) and ref.dim() == 2 and ref.shape[1] == plan.d
+    if ref_rows is not None:
+        assert ref_rows.dtype == torch.int32 and ref_rows.shape == (T,)
+    else:
+        assert ref.shape[0] == T
+    if y is None:
+        y = torch.empty((T, plan.d), dtype=out_dtype or u.dtype, device=u.device)
+    norms = torch.empty((T, 2), dtype=torch.float32, device=u.device) if with_norms else None
+    _check("dpb_normalize", load().dpb_normalize(
+        plan._handle, _dev(u, "u"), _dtype_code(u), _dev(ref, "ref"), _dtype_code(ref), _opt(ref_rows, "ref_rows"),
+        ref.shape[0], T, _dev(y, "y"), _dtype_code(y), _opt(norms, "norms"), _stream(u)))
+    return (y, norms) if with_norms else y
+
+
+def normalize_bwd(plan: Plan, g: torch.Tensor, u: torch.Tensor, ref: torch.Tensor,
+                  gu_dtype: torch.dtype | None = None, grad_ref: torch.Tensor | None = None,
+                  accumulate: bool = False, gr_dtype: torch.dtype | None = None):
+    """(grad_u, grad_ref) of normalize for upstream g; grad_ref is added to
+    the given buffer when accumulate is True."""
+    T = u.shape[0]
+    assert g.shape == u.shape == ref.shape == (T, plan.d)
+    grad_u = torch.empty((T, plan.d), dtype=gu_dtype or g.dtype, device=u.device)
+    if grad_ref is None:
+        assert not accumulate
+        grad_ref = torch.empty((T, plan.d), dtype=gr_dtype or ref.dtype, device=u.device)
+    _check("dpb_normalize_bwd", load().dpb_normalize_bwd(
+        plan._handle, _dev(g, "g"), _dtype_code(g), _dev(u, "u"), _dtype_code(u), _dev(ref, "ref"),
+        _dtype_code(ref), T, _dev(grad_u, "grad_u"), _dtype_code(grad_u), _dev(grad_ref, "grad_ref"),
+        _dtype_code(grad_ref), int(bool(accumulate)), _stream(u)))
+    return grad_u, grad_ref
+
+
+def edit_codes(plan: Plan, idx: torch.Tensor, coef: torch.Tensor, rows: torch.Tensor, slots: torch.Tensor,
+               ops: torch.Tensor, tgt_idx: torch.Tensor | None = None, tgt_coef: torch.Tensor | None = None):
+    """One edited copy of source row rows[e] per edit (slot slots[e], op
+    ops[e]: EDIT_ZERO, EDIT_REPLACE, EDIT_RESCALE, EDIT_NONE) -> (idx, coef) [E, k_tot]."""
+    T, E = idx.shape[0], rows.shape[0]
+    assert idx.shape == coef.shape == (T, plan.k_tot) and idx.dtype == torch.int32 and coef.dtype == torch.float32
+    for t in (rows, slots, ops):
+        assert t.dtype == torch.int32 and t.shape == (E,)
+    out_idx = torch.empty((E, plan.k_tot), dtype=torch.int32, device=idx.device)
+    out_coef = torch.empty((E, plan.k_tot), dtype=torch.float32, device=idx.device)
+    _check("dpb_edit_codes", load().dpb_edit_codes(
+        plan._handle, _dev(idx, "idx"), _dev(coef, "coef"), _opt(tgt_idx, "tgt_idx"), _opt(tgt_coef, "tgt_coef"), T,
+        _dev(rows, "rows"), _dev(slots, "slots"), _dev(ops, "ops"), E, _dev(out_idx, "out_idx"),
+        _dev(out_coef, "out_coef"), _stream(idx)))
+    return out_idx, out_coef
+
+
+def variance_workspace_bytes(plan: Plan) -> int:
+    return int(load().dpb_variance_workspace_bytes(plan._handle))
+
+
+def variance_loss(plan: Plan, idx: torch.Tensor, coef: torch.Tensor, n_min: int, with_grad: bool = True,
+                  workspace: torch.Tensor | None = None, grad_scale: torch.Tensor | None = None):
+    """Variance auxiliary loss of a batch of codes -> (loss [] fp32, grad_coef
+    [T, k_tot] fp32 or None); grad_coef is multiplied by the device scalar
+    grad_scale when given."""
+    T = idx.shape[0]
+    assert idx.shape == coef.shape == (T, plan.k_tot) and idx.dtype == torch.int32 and coef.dtype == torch.float32
+    nbytes = variance_workspace_bytes(plan)
+    if workspace is None:
+        workspace = torch.empty((nbytes + 15) // 16 * 4, dtype=torch.float32, device=idx.device)
+    assert workspace.numel() * workspace.element_size() >= nbytes
+    loss = torch.empty((), dtype=torch.float32, device=idx.device)
+    grad = torch.empty((T, plan.k_tot), dtype=torch.float32, device=idx.device) if with_grad else None
+    _check("dpb_variance_loss", load().dpb_variance_loss(
+        plan._handle, _dev(idx, "idx"), _dev(coef, "coef"), T, int(n_min), _dev(workspace, "workspace"),
+        workspace.numel() * workspace.element_size(), _dev(loss, "loss"), _opt(grad, "grad_coef"),
+        _opt(grad_scale, "grad_scale"), _stream(idx)))
+    return loss, grad

@@ -11,7 +11,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libdpb.so")
-SOURCES = ["api.cpp", "tables.cpp", "kernels.hip", "codes.hip", "encode.hip"]
+SOURCES = ["api.cpp", "tables.cpp", "kernels.hip", "codes.hip", "encode.hip", "extras.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

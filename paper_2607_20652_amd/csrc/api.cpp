@@ -521,4 +521,96 @@ dpb_status dpb_decode_bwd(const dpb_plan* plan, const int32_t* idx, const void* 
                                            gx_dtype == DPB_BF16, (hipStream_t)stream));
 }
 
+dpb_status dpb_decode_bwd_ex(const dpb_plan* plan, const int32_t* idx, const void* grad_y, dpb_dtype g_dtype,
+                             int64_t T, const float* add_grad_coef, const void* add_grad_x, float* grad_coef,
+                             void* grad_x, dpb_dtype gx_dtype, void* stream)
+{
+    dpb_status s = check_call(plan, T);
+    if (s) return s;
+    if (!dtype_ok(g_dtype) || !dtype_ok(gx_dtype)) return DPB_EINVAL;
+    if (T == 0) return DPB_OK;
+    if (!idx || !grad_y || !grad_coef || !grad_x || !aligned16(idx) || !aligned16(grad_y) ||
+        !aligned16(grad_coef) || !aligned16(grad_x) || !aligned16(add_grad_coef) || !aligned16(add_grad_x))
+        return DPB_EINVAL;
+    return launched(dpb::launch_decode_bwd2(plan->dev, idx, grad_y, g_dtype == DPB_BF16, T, grad_coef, grad_x,
+                                           gx_dtype == DPB_BF16, (hipStream_t)stream, add_grad_coef, add_grad_x));
+}
+
+dpb_status dpb_normalize(const dpb_plan* plan, const void* u, dpb_dtype u_dtype, const void* ref, dpb_dtype ref_dtype,
+                         const int32_t* ref_rows, int64_t T_ref, int64_t T, void* y, dpb_dtype y_dtype, float* norms,
+                         void* stream)
+{
+    dpb_status s = check_call(plan, T);
+    if (s) return s;
+    if (!dtype_ok(u_dtype) || !dtype_ok(ref_dtype) || !dtype_ok(y_dtype) || T_ref < 0) return DPB_EINVAL;
+    if (!ref_rows && T_ref != T) return DPB_EINVAL;
+    if (T == 0) return DPB_OK;
+    if (!u || !ref || !y || !aligned16(u) || !aligned16(ref) || !aligned16(y) || !aligned16(norms) ||
+        !aligned16(ref_rows))
+        return DPB_EINVAL;
+    if (u == y && u_dtype != y_dtype) return DPB_EINVAL;
+    return launched(dpb::launch_normalize(plan->dev.d, T, u, u_dtype == DPB_BF16, ref, ref_dtype == DPB_BF16, ref_rows,
+                                          T_ref, y, y_dtype == DPB_BF16, norms, (hipStream_t)stream));
+}
+
+dpb_status dpb_normalize_bwd(const dpb_plan* plan, const void* g, dpb_dtype g_dtype, const void* u, dpb_dtype u_dtype,
+                             const void* ref, dpb_dtype ref_dtype, int64_t T, void* grad_u, dpb_dtype gu_dtype,
+                             void* grad_ref, dpb_dtype gr_dtype, int accumulate, void* stream)
+{
+    dpb_status s = check_call(plan, T);
+    if (s) return s;
+    if (!dtype_ok(g_dtype) || !dtype_ok(u_dtype) || !dtype_ok(ref_dtype) || !dtype_ok(gu_dtype) ||
+        !dtype_ok(gr_dtype))
+        return DPB_EINVAL;
+    if (T == 0) return DPB_OK;
+    const void* all[5] = {g, u, ref, grad_u, grad_ref};
+    for (const void* p : all)
+        if (!p || !aligned16(p)) return DPB_EINVAL;
+    if (grad_u == grad_ref || grad_u == g || grad_u == u || grad_u == ref || grad_ref == g || grad_ref == u ||
+        grad_ref == ref)
+        return DPB_EINVAL;
+    return launched(dpb::launch_normalize_bwd(plan->dev.d, T, g, g_dtype == DPB_BF16, u, u_dtype == DPB_BF16, ref,
+                                              ref_dtype == DPB_BF16, grad_u, gu_dtype == DPB_BF16, grad_ref,
+                                              gr_dtype == DPB_BF16, accumulate, (hipStream_t)stream));
+}
+
+dpb_status dpb_edit_codes(const dpb_plan* plan, const int32_t* idx, const float* coef, const int32_t* tgt_idx,
+                          const float* tgt_coef, int64_t T, const int32_t* rows, const int32_t* slots,
+                          const int32_t* ops, int64_t E, int32_t* out_idx, float* out_coef, void* stream)
+{
+    dpb_status s = check_call(plan, E);
+    if (s) return s;
+    if (T < 0 || (!tgt_idx) != (!tgt_coef)) return DPB_EINVAL;
+    if (E == 0) return DPB_OK;
+    if (!idx || !coef || !rows || !slots || !ops || !out_idx || !out_coef) return DPB_EINVAL;
+    const void* all[9] = {idx, coef, tgt_idx, tgt_coef, rows, slots, ops, out_idx, out_coef};
+    for (const void* p : all)
+        if (!aligned16(p)) return DPB_EINVAL;
+    if ((const void*)out_idx == (const void*)idx || (const void*)out_coef == (const void*)coef ||
+        (tgt_idx && ((const void*)out_idx == (const void*)tgt_idx || (const void*)out_coef == (const void*)tgt_coef)))
+        return DPB_EINVAL;
+    return launched(dpb::launch_edit_codes(idx, coef, tgt_idx, tgt_coef, T, plan->dev.k_tot, rows, slots, ops, E,
+                                           out_idx, out_coef, (hipStream_t)stream));
+}
+
+size_t dpb_variance_workspace_bytes(const dpb_plan* plan)
+{
+    if (!plan) return 0;
+    return dpb::variance_workspace_bytes((int64_t)1 << plan->dev.level_bits[plan->dev.levels - 1]);
+}
+
+dpb_status dpb_variance_loss(const dpb_plan* plan, const int32_t* idx, const float* coef, int64_t T, int n_min,
+                             void* workspace, size_t ws_bytes, float* loss, float* grad_coef,
+                             const float* grad_scale, void* stream)
+{
+    dpb_status s = check_call(plan, T);
+    if (s) return s;
+    if (!loss || !workspace || !aligned16(workspace) || ws_bytes < dpb_variance_workspace_bytes(plan))
+        return DPB_EINVAL;
+    if (T > 0 && (!idx || !coef || !aligned16(idx) || !aligned16(coef) || !aligned16(grad_coef))) return DPB_EINVAL;
+    const int64_t nfeat = (int64_t)1 << plan->dev.level_bits[plan->dev.levels - 1];
+    return launched(dpb::launch_variance_loss(idx, coef, T * plan->dev.k_tot, nfeat, n_min, workspace, loss,
+                                              T > 0 ? grad_coef : nullptr, grad_scale, (hipStream_t)stream));
+}
+
 }  // extern "C"

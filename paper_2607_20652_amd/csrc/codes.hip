@@ -386,10 +386,38 @@ __device__ Wave make_wave(const DevPlan& P, unsigned char* smem, bool scoring, b
     return W;
 }
 
+// a, b += the 8 elements of `add` at i (fewer when rem < 8, vec false).
+template <bool BF16>
+__device__ __forceinline__ void add_row8(const void* add, int64_t i, int rem, bool vec, float4& a, float4& b)
+{
+    float v[8];
+    if (vec) {
+        if constexpr (BF16) {
+            const u32x4 q = *(const u32x4*)((const uint16_t*)add + i);
+            const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                v[2 * e] = bf16_bits_to_f32(w[e] & 0xFFFFu);
+                v[2 * e + 1] = bf16_bits_to_f32(w[e] >> 16);
+            }
+        } else {
+            const float4 p = *(const float4*)((const float*)add + i), q = *(const float4*)((const float*)add + i + 4);
+            v[0] = p.x; v[1] = p.y; v[2] = p.z; v[3] = p.w;
+            v[4] = q.x; v[5] = q.y; v[6] = q.z; v[7] = q.w;
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = e < rem ? load_act<BF16>(add, i + e) : 0.f;
+    }
+    a.x += v[0]; a.y += v[1]; a.z += v[2]; a.w += v[3];
+    b.x += v[4]; b.y += v[5]; b.z += v[6]; b.w += v[7];
+}
+
 // Converts the wave's fp32 rows to the output type, 8 coordinates per lane
-// (16- or 32-byte stores when d is a multiple of 8).
+// (16- or 32-byte stores when d is a multiple of 8).  A non-null `add`
+// (same type and shape as out) is added first; it may alias out.
 template <bool OUT_BF16>
-__device__ void write_rows(const DevPlan& P, const Wave& W, void* out)
+__device__ void write_rows(const DevPlan& P, const Wave& W, void* out, const void* add = nullptr)
 {
     const int d = P.d, dp = P.dp;
     const bool vec = (d & 7) == 0;
@@ -397,7 +425,8 @@ __device__ void write_rows(const DevPlan& P, const Wave& W, void* out)
         const float* yt = W.y + tt * dp;
         const int64_t r0 = (W.t0 + tt) * d;
         for (int o = W.lane * 8; o < d; o += 512) {
-            const float4 a = *(const float4*)(yt + o), b = *(const float4*)(yt + o + 4);
+            float4 a = *(const float4*)(yt + o), b = *(const float4*)(yt + o + 4);
+            if (add) add_row8<OUT_BF16>(add, r0 + o, d - o, vec, a, b);
             if (vec) {
                 if constexpr (OUT_BF16) {
                     u32x4 v;
@@ -519,7 +548,8 @@ template <bool G_BF16, bool GX_BF16, int NG, bool PB16>
 __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const int32_t* __restrict__ idx,
                                                                const void* __restrict__ g, int64_t T,
                                                                float* __restrict__ grad_coef,
-                                                               void* __restrict__ grad_x)
+                                                               void* grad_x, const float* __restrict__ add_gc,
+                                                               const void* add_gx)
 {
     extern __shared__ __align__(16) unsigned char smem[];
     load_shared(P, smem);
@@ -578,11 +608,15 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
                 }
             }
         wave_sync();
+        if (add_gc) {
+            for (int i = lane; i < W.ntok * k; i += 64) W.coef[i] += add_gc[t0 * k + i];
+            wave_sync();
+        }
         for (int i = lane; i < W.ntok * k; i += 64) grad_coef[t0 * k + i] = W.coef[i];
 
-        // grad_x = decode(idx, grad_coef); the scoring buffers are dead now
+        // grad_x = decode(idx, grad_coef) (+ add_gx); the scoring buffers are dead now
         decode_tokens<!GX_BF16, NG, PB16>(P, W, W.coef);
-        write_rows<GX_BF16>(P, W, grad_x);
+        write_rows<GX_BF16>(P, W, grad_x, add_gx);
         wave_sync();
     }
 }
@@ -665,45 +699,53 @@ hipError_t launch_decode2(const DevPlan& P, const int32_t* idx, const float* coe
     return hipGetLastError();
 }
 
+struct BwdExtra {
+    const float* gc;
+    const void* gx;
+};
+
 template <bool GB, bool XB, int NG, bool PB>
 static void launch_bwd_v(const DevPlan& P, dim3 grid, size_t lds, hipStream_t stream, const int32_t* idx,
-                         const void* g, int64_t T, float* gc, void* gx)
+                         const void* g, int64_t T, float* gc, void* gx, BwdExtra ex)
 {
     allow_lds(decode_bwd2_kernel<GB, XB, NG, PB>, lds);
-    hipLaunchKernelGGL((decode_bwd2_kernel<GB, XB, NG, PB>), grid, dim3(kThreads), lds, stream, P, idx, g, T, gc, gx);
+    hipLaunchKernelGGL((decode_bwd2_kernel<GB, XB, NG, PB>), grid, dim3(kThreads), lds, stream, P, idx, g, T, gc, gx,
+                       ex.gc, ex.gx);
 }
 
 template <bool GB, bool XB, bool PB>
 static void launch_bwd_ng(const DevPlan& P, dim3 grid, size_t lds, hipStream_t stream, const int32_t* idx,
-                          const void* g, int64_t T, float* gc, void* gx)
+                          const void* g, int64_t T, float* gc, void* gx, BwdExtra ex)
 {
     switch (ng_variant(P)) {
-    case 3: launch_bwd_v<GB, XB, 3, PB>(P, grid, lds, stream, idx, g, T, gc, gx); break;
-    case 4: launch_bwd_v<GB, XB, 4, PB>(P, grid, lds, stream, idx, g, T, gc, gx); break;
-    case 5: launch_bwd_v<GB, XB, 5, PB>(P, grid, lds, stream, idx, g, T, gc, gx); break;
-    case 6: launch_bwd_v<GB, XB, 6, PB>(P, grid, lds, stream, idx, g, T, gc, gx); break;
-    default: launch_bwd_v<GB, XB, 8, PB>(P, grid, lds, stream, idx, g, T, gc, gx); break;
+    case 3: launch_bwd_v<GB, XB, 3, PB>(P, grid, lds, stream, idx, g, T, gc, gx, ex); break;
+    case 4: launch_bwd_v<GB, XB, 4, PB>(P, grid, lds, stream, idx, g, T, gc, gx, ex); break;
+    case 5: launch_bwd_v<GB, XB, 5, PB>(P, grid, lds, stream, idx, g, T, gc, gx, ex); break;
+    case 6: launch_bwd_v<GB, XB, 6, PB>(P, grid, lds, stream, idx, g, T, gc, gx, ex); break;
+    default: launch_bwd_v<GB, XB, 8, PB>(P, grid, lds, stream, idx, g, T, gc, gx, ex); break;
     }
 }
 
 template <bool GB, bool XB>
 static void launch_bwd_ub(const DevPlan& P, dim3 grid, size_t lds, hipStream_t stream, const int32_t* idx,
-                          const void* g, int64_t T, float* gc, void* gx)
+                          const void* g, int64_t T, float* gc, void* gx, BwdExtra ex)
 {
-    if (P.pb_bytes == 2) launch_bwd_ng<GB, XB, true>(P, grid, lds, stream, idx, g, T, gc, gx);
-    else launch_bwd_ng<GB, XB, false>(P, grid, lds, stream, idx, g, T, gc, gx);
+    if (P.pb_bytes == 2) launch_bwd_ng<GB, XB, true>(P, grid, lds, stream, idx, g, T, gc, gx, ex);
+    else launch_bwd_ng<GB, XB, false>(P, grid, lds, stream, idx, g, T, gc, gx, ex);
 }
 
 hipError_t launch_decode_bwd2(const DevPlan& P, const int32_t* idx, const void* g, bool g_bf16, int64_t T,
-                              float* grad_coef, void* grad_x, bool gx_bf16, hipStream_t stream)
+                              float* grad_coef, void* grad_x, bool gx_bf16, hipStream_t stream,
+                              const float* add_grad_coef, const void* add_grad_x)
 {
     const size_t lds = code_lds_bytes(P, true, g_bf16);
     if (lds > (size_t)kLdsBudget) return hipErrorInvalidValue;
     const dim3 grid = code_grid(P, T, lds);
-    if (g_bf16 && gx_bf16) launch_bwd_ub<true, true>(P, grid, lds, stream, idx, g, T, grad_coef, grad_x);
-    else if (g_bf16) launch_bwd_ub<true, false>(P, grid, lds, stream, idx, g, T, grad_coef, grad_x);
-    else if (gx_bf16) launch_bwd_ub<false, true>(P, grid, lds, stream, idx, g, T, grad_coef, grad_x);
-    else launch_bwd_ub<false, false>(P, grid, lds, stream, idx, g, T, grad_coef, grad_x);
+    const BwdExtra ex{add_grad_coef, add_grad_x};
+    if (g_bf16 && gx_bf16) launch_bwd_ub<true, true>(P, grid, lds, stream, idx, g, T, grad_coef, grad_x, ex);
+    else if (g_bf16) launch_bwd_ub<true, false>(P, grid, lds, stream, idx, g, T, grad_coef, grad_x, ex);
+    else if (gx_bf16) launch_bwd_ub<false, true>(P, grid, lds, stream, idx, g, T, grad_coef, grad_x, ex);
+    else launch_bwd_ub<false, false>(P, grid, lds, stream, idx, g, T, grad_coef, grad_x, ex);
     return hipGetLastError();
 }
 

@@ -172,11 +172,26 @@ bool plan_fits(const DevPlan& P);
 hipError_t launch_decode2(const DevPlan& P, const int32_t* idx, const float* coef, int64_t T, void* y,
                           bool y_bf16, hipStream_t stream);
 hipError_t launch_decode_bwd2(const DevPlan& P, const int32_t* idx, const void* g, bool g_bf16, int64_t T,
-                              float* grad_coef, void* grad_x, bool gx_bf16, hipStream_t stream);
+                              float* grad_coef, void* grad_x, bool gx_bf16, hipStream_t stream,
+                              const float* add_grad_coef = nullptr, const void* add_grad_x = nullptr);
 bool code_kernels_fit(const DevPlan& P);
 bool encode2_supported(const DevPlan& P);
 hipError_t launch_encode2(const DevPlan& P, const void* x, bool x_bf16, int64_t T, int32_t* idx, float* coef,
                           hipStream_t stream);
+
+// Row epilogues, code edits and the variance loss (extras.hip).
+hipError_t launch_normalize(int d, int64_t T, const void* u, bool u16, const void* ref, bool r16,
+                            const int32_t* ref_rows, int64_t T_ref, void* y, bool y16, float* norms,
+                            hipStream_t stream);
+hipError_t launch_normalize_bwd(int d, int64_t T, const void* g, bool g16, const void* u, bool u16, const void* ref,
+                                bool r16, void* gu, bool gu16, void* gr, bool gr16, int accumulate,
+                                hipStream_t stream);
+hipError_t launch_edit_codes(const int32_t* idx, const float* coef, const int32_t* tidx, const float* tcoef,
+                             int64_t T, int k, const int32_t* rows, const int32_t* slots, const int32_t* ops,
+                             int64_t E, int32_t* out_idx, float* out_coef, hipStream_t stream);
+size_t variance_workspace_bytes(int64_t nfeat);
+hipError_t launch_variance_loss(const int32_t* idx, const float* coef, int64_t n, int64_t nfeat, int n_min,
+                                void* ws, float* loss, float* grad, const float* grad_scale, hipStream_t stream);
 
 hipError_t launch_encode(const DevPlan& P, const void* x, bool x_bf16, int64_t T, int32_t* idx,
                          float* coef, hipStream_t stream);

@@ -1,0 +1,293 @@
+"""GPU parity of the layer epilogues and code utilities (through the C ABI)
+against the CPU oracle: normalized reconstruction and its backward (§2.2
+"Normalized Reconstruction"), the code edits of the greedy feature editing
+(App. C.3), the variance auxiliary loss (§2.2 "Auxillary losses"), the
+backward with extra gradient terms, and the DPB layer as an autograd Function.
+
+Index and edit results are compared bit for bit; floating-point results with
+the rules of parity_util (1e-5 for fp32 outputs, 2e-2 for bf16 outputs,
+relative to max(|ref|, rms of the row)).
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_20652_amd import autograd as dpb_autograd
+from paper_2607_20652_amd import binding as dpb
+from paper_2607_20652_amd import inputs
+from parity_util import TOL_BF16, TOL_F32, compare_dense
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+_PLANS = {}
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    dpb.load()
+
+
+def plan_for(name):
+    if name not in _PLANS:
+        w = inputs.workload(name)
+        _PLANS[name] = dpb.Plan(w.d, w.n, w.levels, w.branching, w.beam, w.k, 0)
+    return _PLANS[name]
+
+
+def _tol(dt):
+    return TOL_F32 if dt == torch.float32 else TOL_BF16
+
+
+# ---------------------------------------------------------------- normalize
+
+@pytest.mark.parametrize("name,T,dt", [("tiny", 37, torch.float32), ("train", 1000, torch.bfloat16),
+                                       ("train", 333, torch.float32), ("very_wide", 70, torch.bfloat16)])
+def test_normalize_matches_oracle(name, T, dt):
+    say(f"[normalize] {name} T={T} {dt}")
+    plan = plan_for(name)
+    w = inputs.workload(name)
+    u = inputs.normal((T, w.d), 51, "bf16" if dt == torch.bfloat16 else "f32")
+    r = inputs.normal((T, w.d), 52, "bf16" if dt == torch.bfloat16 else "f32") * 3
+    u[2] = 0                                   # a zero decoder output
+    r[4] = 0                                   # a zero reference
+    y, norms = dpb.normalize(plan, u.to(DEV), r.to(DEV), with_norms=True)
+    torch.cuda.synchronize()
+    ry, rn = oracle.normalize(u.double().numpy(), r.double().numpy())
+    compare_dense(y.float().cpu().numpy(), ry, _tol(dt))
+    compare_dense(norms.cpu().numpy(), rn, TOL_F32)
+    assert torch.all(y[2] == 0) and torch.all(y[4] == 0)
+
+
+def test_normalize_ref_rows_and_in_place():
+    say("[normalize ref_rows] train")
+    plan = plan_for("train")
+    w = inputs.workload("train")
+    T, Tr = 50, 7
+    u = inputs.normal((T, w.d), 53).to(DEV)
+    r = inputs.normal((Tr, w.d), 54).to(DEV)
+    rows = torch.from_numpy(np.random.default_rng(5).integers(0, Tr, T).astype(np.int32))
+    rows[3] = Tr                                # out of range: a reference of norm 0
+    rows[9] = -1
+    y = dpb.normalize(plan, u, r, ref_rows=rows.to(DEV))
+    u2 = u.clone()
+    dpb.normalize(plan, u2, r, ref_rows=rows.to(DEV), y=u2)   # in place
+    torch.cuda.synchronize()
+    rr = r.double().cpu().numpy()[np.clip(rows.numpy(), 0, Tr - 1)]
+    rr[3] = 0
+    rr[9] = 0
+    ry, _ = oracle.normalize(u.double().cpu().numpy(), rr)
+    compare_dense(y.cpu().numpy(), ry, TOL_F32)
+    assert torch.equal(u2, y)
+
+
+@pytest.mark.parametrize("name,T,dt,acc", [("tiny", 41, torch.float32, False), ("train", 700, torch.bfloat16, True),
+                                           ("train", 129, torch.float32, True)])
+def test_normalize_bwd_matches_oracle(name, T, dt, acc):
+    say(f"[normalize bwd] {name} T={T} {dt} acc={acc}")
+    plan = plan_for(name)
+    w = inputs.workload(name)
+    tag = "bf16" if dt == torch.bfloat16 else "f32"
+    g, u, r = (inputs.normal((T, w.d), s, tag) for s in (61, 62, 63))
+    u[1] = 0
+    r[3] = 0
+    base = inputs.normal((T, w.d), 64, tag)
+    gref = base.clone().to(DEV) if acc else None
+    gu, gr = dpb.normalize_bwd(plan, g.to(DEV), u.to(DEV), r.to(DEV), grad_ref=gref, accumulate=acc)
+    torch.cuda.synchronize()
+    rgu, rgr = oracle.normalize_bwd(g.double().numpy(), u.double().numpy(), r.double().numpy())
+    if acc:
+        rgr = rgr + base.double().numpy()
+    compare_dense(gu.float().cpu().numpy(), rgu, _tol(dt))
+    compare_dense(gr.float().cpu().numpy(), rgr, _tol(dt))
+
+
+# ---------------------------------------------------------------- edits
+
+@pytest.mark.parametrize("name", ["tiny", "train"])
+def test_edit_codes_bit_exact(name):
+    say(f"[edit] {name}")
+    plan = plan_for(name)
+    w = inputs.workload(name)
+    T = 40
+    x = inputs.activations(name, T).to(DEV)
+    xt = inputs.normal((T, w.d), 71, w.dtype).to(DEV)
+    si, sc = dpb.encode(plan, x)
+    ti, tc = dpb.encode(plan, xt)
+    k = plan.k_tot
+    rng = np.random.default_rng(7)
+    E = 3 * k + 9
+    rows = rng.integers(0, T, E).astype(np.int32)
+    slots = rng.integers(0, k, E).astype(np.int32)
+    ops = rng.integers(0, 4, E).astype(np.int32)
+    rows[:3], slots[3:6], ops[6:9] = [T, -1, 2 * T], [k, -1, k + 5], [4, -1, 9]   # invalid edits
+    args = [torch.from_numpy(a).to(DEV) for a in (rows, slots, ops)]
+    oi, oc = dpb.edit_codes(plan, si, sc, *args, tgt_idx=ti, tgt_coef=tc)
+    zi, zc = dpb.edit_codes(plan, si, sc, *args)            # no target: only zero / none are valid
+    torch.cuda.synchronize()
+    edits = list(zip(rows.tolist(), slots.tolist(), ops.tolist()))
+    ri, rc = oracle.edit_codes(si.cpu().numpy(), sc.cpu().numpy(), ti.cpu().numpy(), tc.cpu().numpy(), edits)
+    assert np.array_equal(oi.cpu().numpy(), ri)
+    assert np.array_equal(oc.cpu().numpy().astype(np.float64), rc)
+    zedits = [(r_, s_, o_ if o_ in (0, 3) else 9) for r_, s_, o_ in edits]
+    ri, rc = oracle.edit_codes(si.cpu().numpy(), sc.cpu().numpy(), ti.cpu().numpy(), tc.cpu().numpy(), zedits)
+    assert np.array_equal(zi.cpu().numpy(), ri)
+    assert np.array_equal(zc.cpu().numpy().astype(np.float64), rc)
+
+
+def test_greedy_edit_step_matches_oracle():
+    """One step of the greedy feature editing (App. C.3): every (position,
+    operation) candidate is decoded, rescaled to the source norm, and scored
+    by its distance to the target activation."""
+    say("[edit step] train")
+    name = "train"
+    plan = plan_for(name)
+    w = inputs.workload(name)
+    xs = inputs.activations(name, 2)
+    xt = inputs.normal((2, w.d), 72, "bf16")
+    si, sc = dpb.encode(plan, xs.to(DEV))
+    ti, tc = dpb.encode(plan, xt.to(DEV))
+    k = plan.k_tot
+    rows = np.repeat(np.arange(2), 3 * k).astype(np.int32)
+    slots = np.tile(np.repeat(np.arange(k), 3), 2).astype(np.int32)
+    ops = np.tile(np.array([0, 1, 2], np.int32), 2 * k)
+    dr = torch.from_numpy(rows).to(DEV)
+    ei, ec = dpb.edit_codes(plan, si, sc, dr, torch.from_numpy(slots).to(DEV), torch.from_numpy(ops).to(DEV),
+                            tgt_idx=ti, tgt_coef=tc)
+    u = dpb.decode(plan, ei, ec)
+    y = dpb.normalize(plan, u, xs.to(DEV), ref_rows=dr)
+    dist = ((y - xt.float().to(DEV)[dr.long()]) ** 2).sum(1).cpu().numpy()
+    m = oracle.masks(w.d, w.n)
+    ri, rcf = oracle.edit_codes(si.cpu().numpy(), sc.cpu().numpy(), ti.cpu().numpy(), tc.cpu().numpy(),
+                                list(zip(rows, slots, ops)))
+    ry, _ = oracle.normalize(oracle.decode(w.d, m, ri, rcf), xs.double().numpy()[rows])
+    rdist = ((ry - xt.double().numpy()[rows]) ** 2).sum(1)
+    compare_dense(y.cpu().numpy(), ry, TOL_F32)
+    assert np.allclose(dist, rdist, rtol=1e-4, atol=1e-4 * rdist.mean())
+
+
+# ---------------------------------------------------------------- variance loss
+
+@pytest.mark.parametrize("name,T,n_min", [("tiny", 256, 3), ("tiny", 5, 1), ("train", 2048, 4),
+                                          ("very_wide", 300, 2), ("tiny", 64, 10 ** 6)])
+def test_variance_loss_matches_oracle(name, T, n_min):
+    say(f"[variance] {name} T={T} n_min={n_min}")
+    plan = plan_for(name)
+    x = inputs.activations(name, T).to(DEV)
+    idx, coef = dpb.encode(plan, x)
+    idx[::7, -1] = -1                        # padding is not a sample
+    coef[::7, -1] = 0
+    scale = torch.tensor(0.37, device=DEV)
+    loss, grad = dpb.variance_loss(plan, idx, coef, n_min)
+    loss2, grad2 = dpb.variance_loss(plan, idx, coef, n_min, grad_scale=scale)
+    torch.cuda.synchronize()
+    rl, rg = oracle.variance_loss(idx.cpu().numpy(), coef.cpu().numpy().astype(np.float64), n_min)
+    say(f"  loss {loss.item():.6g} oracle {rl:.6g}")
+    assert abs(loss.item() - rl) <= TOL_F32 * max(abs(rl), 1e-30)
+    assert loss2.item() == loss.item()
+    compare_dense(grad.cpu().numpy(), rg, TOL_F32)
+    compare_dense(grad2.cpu().numpy(), 0.37 * rg, TOL_F32)
+
+
+def test_variance_loss_empty_batch():
+    plan = plan_for("tiny")
+    idx = torch.empty((0, plan.k_tot), dtype=torch.int32, device=DEV)
+    coef = torch.empty((0, plan.k_tot), dtype=torch.float32, device=DEV)
+    loss, grad = dpb.variance_loss(plan, idx, coef, 1)
+    torch.cuda.synchronize()
+    assert loss.item() == 0.0 and grad.numel() == 0
+
+
+# ---------------------------------------------------------------- backward with extra terms
+
+@pytest.mark.parametrize("name,T,gdt", [("tiny", 77, torch.float32), ("train", 500, torch.bfloat16)])
+def test_decode_bwd_ex_adds_terms(name, T, gdt):
+    say(f"[bwd ex] {name} T={T} {gdt}")
+    plan = plan_for(name)
+    w = inputs.workload(name)
+    m = oracle.masks(w.d, w.n)
+    x = inputs.activations(name, T).to(DEV)
+    idx, _ = dpb.encode(plan, x)
+    g = inputs.upstream_grad(name, T).to(gdt).to(DEV)
+    agc = inputs.normal((T, plan.k_tot), 81).to(DEV)
+    agx = inputs.normal((T, w.d), 82, "bf16" if gdt == torch.bfloat16 else "f32").to(DEV)
+    gc, gx = dpb.decode_bwd_ex(plan, idx, g, add_grad_coef=agc, add_grad_x=agx)
+    gc0, gx0 = dpb.decode_bwd(plan, idx, g)
+    gc1, gx1 = dpb.decode_bwd_ex(plan, idx, g)                       # no extras: identical to decode_bwd
+    agx2 = agx.clone()
+    _, gx2 = dpb.decode_bwd_ex(plan, idx, g, add_grad_coef=agc, add_grad_x=agx2, grad_x=agx2)   # in place
+    torch.cuda.synchronize()
+    assert torch.equal(gc1, gc0) and torch.equal(gx1, gx0)
+    assert torch.equal(gx2, gx)
+    ii = idx.cpu().numpy()
+    rgc, rgx = oracle.decode_bwd(w.d, m, ii, g.double().cpu().numpy())
+    a = agc.double().cpu().numpy()
+    rgc = rgc + a
+    rgx = rgx + oracle.decode(w.d, m, ii, a) + agx.double().cpu().numpy()
+    compare_dense(gc.cpu().numpy(), rgc, TOL_F32)
+    compare_dense(gx.float().cpu().numpy(), rgx, _tol(gdt))
+
+
+# ---------------------------------------------------------------- the layer
+
+@pytest.mark.parametrize("name,T,normalized,n_min", [("tiny", 200, True, 3), ("gpt2", 512, True, 2),
+                                                     ("train", 300, False, 2), ("train", 256, True, None)])
+def test_layer_forward_backward_matches_oracle(name, T, normalized, n_min):
+    say(f"[layer] {name} T={T} normalized={normalized} n_min={n_min}")
+    plan = plan_for(name)
+    w = inputs.workload(name)
+    m = oracle.masks(w.d, w.n)
+    x = inputs.activations(name, T).to(DEV).requires_grad_(True)
+    gy = inputs.upstream_grad(name, T).to(DEV)
+    y, lv = dpb_autograd.dpb_layer(x, plan, normalized, n_min)
+    gloss = 0.61
+    torch.autograd.backward([y, lv], [gy, torch.tensor(gloss, device=DEV)])
+    idx, coef = dpb.encode(plan, x.detach())
+    torch.cuda.synchronize()
+    ii, cc = idx.cpu().numpy(), coef.cpu().numpy().astype(np.float64)
+    xd = x.detach().double().cpu().numpy()
+    u = oracle.decode(w.d, m, ii, cc)
+    ry = oracle.normalize(u, xd)[0] if normalized else u
+    compare_dense(y.detach().float().cpu().numpy(), ry, _tol(x.dtype))
+    if n_min is not None:
+        rl, _ = oracle.variance_loss(ii, cc, n_min)
+        assert abs(lv.item() - rl) <= TOL_F32 * max(abs(rl), 1e-30)
+    else:
+        assert lv.item() == 0.0
+    _, rgx = oracle.layer_backward(w.d, m, ii, cc, xd, gy.double().cpu().numpy(),
+                                   gloss if n_min is not None else 0.0, n_min or 1, normalized)
+    compare_dense(x.grad.float().cpu().numpy(), rgx, _tol(x.dtype))
+
+
+def test_mlp_block_trains():
+    """The DPB MLP block runs forward and backward in bf16; a few SGD steps on
+    a fixed synthetic batch lower the block's regression loss."""
+    say("[mlp block] gpt2")
+    torch.manual_seed(0)
+    plan = plan_for("gpt2")
+    blk = dpb_autograd.DPBMLP(plan, 4 * plan.d, normalized=True, n_min=2, dtype=torch.bfloat16, device=DEV)
+    h = inputs.activations("gpt2", 256).to(DEV).reshape(4, 64, plan.d)
+    target = inputs.normal((4, 64, plan.d), 91, "bf16").to(DEV)
+    opt = torch.optim.SGD(blk.parameters(), lr=0.05)
+    losses = []
+    for _ in range(6):
+        out, lv = blk(h)
+        loss = ((out.float() - target.float()) ** 2).mean() + 0.05 * lv
+        opt.zero_grad()
+        loss.backward()
+        opt.step()
+        losses.append(loss.item())
+    torch.cuda.synchronize()
+    say(f"  losses {losses}")
+    assert all(np.isfinite(losses)) and losses[-1] < losses[0]
+    assert all(p.grad is not None and torch.isfinite(p.grad).all() for p in blk.parameters())

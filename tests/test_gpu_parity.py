@@ -83,6 +83,21 @@ def test_encode_matches_oracle(name, T):
     assert st["exempt_tokens"] <= max(2, 0.02 * T)
 
 
+@pytest.mark.parametrize("name,T", [("gpt2", 300), ("wide", 257), ("very_wide", 90)])
+def test_encode_f32_input_matches_oracle(name, T):
+    """fp32 activations at the bf16 workloads' shapes (the fp32 scoring path)."""
+    say(f"[encode f32] {name} T={T}")
+    plan = plan_for(name)
+    w, nb, dl, K, m, gens = oracle_setup(name)
+    x = inputs.normal((T, w.d), 300 + w.index)
+    idx, coef = dpb.encode(plan, x.to(DEV))
+    torch.cuda.synchronize()
+    oi, oc, om, oo = oracle.encode(w.d, m, nb, K, dl, gens, x.double().numpy())
+    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32)
+    say(f"  {st}")
+    assert st["exempt_tokens"] <= max(2, 0.02 * T)
+
+
 @pytest.mark.parametrize("name,rows", [("gpt2", 384), ("wide", 256), ("very_wide", 160)])
 def test_encode_full_size_sampled(name, rows):
     w = inputs.workload(name)

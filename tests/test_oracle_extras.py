@@ -1,12 +1,13 @@
 """Pins for the oracle's normalized reconstruction, code edits and variance
 auxiliary loss (§2.2 "Normalized Reconstruction", "Auxillary losses"; the
-feature-edit experiments of the appendix).
+greedy feature editing of App. C.3).
 
 Normalization: output norm equals the reference norm, the direction is the
 decoder's, positive rescaling of the decoder output changes nothing, and the
 hand-derived backward equals float64 autograd of the forward definition.
-Edits: each edit changes the decode by exactly the removed / added terms
-(decode is linear in the code).  Variance loss: a hand-worked example
+Edits: each candidate changes the decode by exactly the removed / added
+terms (decode is linear in the code), and replacing every position in turn
+reaches the target code.  Variance loss: a hand-worked example
 (tests/golden), finite differences of the loss for the gradient, invariance
 to a per-feature shift, quadratic scaling, and the n_min cut.
 """
@@ -67,42 +68,52 @@ def tiny_code():
     T, k = 6, 10
     idx = rng.integers(0, 1 << n, size=(T, k)).astype(np.int32)
     idx[:, 0] = 7           # a basis feature everywhere
-    idx[::2, 3] = 1234      # a hashed feature on even tokens
     idx[1, 5] = -1          # padding
     coef = rng.standard_normal((T, k))
-    return d, m, idx, coef
+    tidx = rng.integers(0, 1 << n, size=(T, k)).astype(np.int32)
+    tcoef = rng.standard_normal((T, k))
+    return d, m, idx, coef, tidx, tcoef
 
 
-def test_edit_zero_rescale_set_remove_exact_terms(tiny_code):
-    d, m, idx, coef = tiny_code
+def test_edit_candidates_change_decode_by_exact_terms(tiny_code):
+    """Decode is linear in the code, so each candidate's decode differs from
+    its source row's by exactly the terms the edit removes and adds."""
+    d, m, idx, coef, tidx, tcoef = tiny_code
+    T, k = idx.shape
     base = oracle.decode(d, m, idx, coef)
-    contrib = lambda f, c: np.stack([sum(c[t, s] * oracle.phi(d, m, f) for s in range(idx.shape[1]) if idx[t, s] == f)
-                                     if np.any(idx[t] == f) else np.zeros(d) for t in range(idx.shape[0])])
-    for f in (7, 1234):
-        i2, c2 = oracle.edit_codes(idx, coef, [(f, 0, 0.0, 0)])
-        assert np.array_equal(i2, idx)
-        assert np.allclose(oracle.decode(d, m, i2, c2), base - contrib(f, coef), atol=1e-12)
-        i3, c3 = oracle.edit_codes(idx, coef, [(f, 1, 2.5, 0)])
-        assert np.allclose(oracle.decode(d, m, i3, c3), base + 1.5 * contrib(f, coef), atol=1e-12)
-        i4, c4 = oracle.edit_codes(idx, coef, [(f, 2, 0.75, 0)])
-        ones = np.where(idx == f, 0.75, 0.0)
-        assert np.allclose(oracle.decode(d, m, i4, c4), base - contrib(f, coef) + contrib(f, ones), atol=1e-12)
+    edits = [(r, p, op) for r in range(T) for p in (0, 3, 9) for op in range(4)]
+    oi, oc = oracle.edit_codes(idx, coef, tidx, tcoef, edits)
+    dec = oracle.decode(d, m, oi, oc)
+    phi = lambda i: oracle.phi(d, m, int(i)) if i >= 0 else np.zeros(d)
+    for e, (r, p, op) in enumerate(edits):
+        old = coef[r, p] * phi(idx[r, p])
+        if op == 0:
+            expect = base[r] - old
+        elif op == 1:
+            expect = base[r] - old + tcoef[r, p] * phi(tidx[r, p])
+        elif op == 2:
+            expect = base[r] - old + tcoef[r, p] * phi(idx[r, p])
+        else:
+            expect = base[r]
+        assert np.allclose(dec[e], expect, atol=1e-12), (r, p, op)
+        other = np.arange(k) != p
+        assert np.array_equal(oi[e, other], idx[r, other]) and np.array_equal(oc[e, other], coef[r, other])
 
 
-def test_edit_replace_moves_the_terms(tiny_code):
-    d, m, idx, coef = tiny_code
-    base = oracle.decode(d, m, idx, coef)
-    i2, c2 = oracle.edit_codes(idx, coef, [(1234, 3, 0.0, 2048)])
-    assert np.array_equal(c2, coef) and not np.any(i2 == 1234)
-    w = np.where(idx == 1234, coef, 0.0).sum(axis=1, keepdims=True)
-    expect = base + w * (oracle.phi(d, m, 2048) - oracle.phi(d, m, 1234))[None, :]
-    assert np.allclose(oracle.decode(d, m, i2, c2), expect, atol=1e-12)
+def test_edit_out_of_range_gives_padding(tiny_code):
+    _, _, idx, coef, tidx, tcoef = tiny_code
+    T, k = idx.shape
+    oi, oc = oracle.edit_codes(idx, coef, tidx, tcoef, [(T, 0, 0), (-1, 0, 0), (0, k, 0), (0, 0, 4), (0, 0, -1)])
+    assert np.all(oi == -1) and np.all(oc == 0.0)
 
 
-def test_edits_apply_in_order(tiny_code):
-    _, _, idx, coef = tiny_code
-    i2, c2 = oracle.edit_codes(idx, coef, [(1234, 3, 0.0, 99), (99, 1, -2.0, 0)])
-    assert np.allclose(c2[idx == 1234], -2.0 * coef[idx == 1234])
+def test_edit_chain_reaches_target(tiny_code):
+    """Replacing every position in turn turns the source code into the target."""
+    _, _, idx, coef, tidx, tcoef = tiny_code
+    ci, cc = idx[2:3].copy(), coef[2:3].copy()
+    for p in range(idx.shape[1]):
+        ci, cc = oracle.edit_codes(ci, cc, tidx[2:3], tcoef[2:3], [(0, p, 1)])
+    assert np.array_equal(ci[0], tidx[2]) and np.array_equal(cc[0], tcoef[2])
 
 
 def test_variance_loss_hand_example():
