@@ -10,7 +10,10 @@ default workload) exceeds the 256 MB Infinity Cache.
 
 Prints ONE JSON line.  `roofline` describes the kernel with the largest average
 launch time, timed with HIP events on the stream the kernels run on;
-`cpu_baseline` times the CPU oracle on a bounded sample of the same workload.
+`extras` times the layer epilogues (normalization and its backward), the code
+edits, the variance auxiliary loss and the whole autograd layer at the same
+shape, after the timed steps; `cpu_baseline` times the CPU oracle on a bounded
+sample of the same workload.
 """
 from __future__ import annotations
 
@@ -40,10 +43,12 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 
 
 def kernel_source_digest() -> str:
-    """Digest of every source the kernels and their plan tables are built from."""
+    """Digest of every source the encode / decode / backward kernels and their
+    plan tables are built from (the row epilogues and code utilities in
+    extras.hip do not affect them)."""
     h = hashlib.sha256()
     for f in sorted(os.listdir(CSRC)):
-        if f.endswith((".hip", ".hpp", ".cpp")):
+        if f.endswith((".hip", ".hpp", ".cpp")) and f != "extras.hip":
             h.update(f.encode())
             h.update(open(os.path.join(CSRC, f), "rb").read())
     return h.hexdigest()[:16]
@@ -127,6 +132,68 @@ def load_traffic(kernel: str, tokens: int):
     return k.get("hbm_bytes_per_launch")
 
 
+def time_extras(plan, w, sets, act, steps: int) -> dict:
+    """Times the layer epilogues and code utilities at the workload's shape
+    (inputs resident in HBM, HIP events on the current stream) and the whole
+    DPB layer (encode, decode, normalization, variance loss and their
+    backward) as an autograd Function.  Bytes are what each kernel must move:
+    every input read once, every output written once."""
+    from paper_2607_20652_amd import autograd as dpb_autograd
+
+    T, d, k = w.tokens, w.d, plan.k_tot
+    xb = 2 if act == torch.bfloat16 else 4
+    dev = sets[0][0].device
+    x, g = sets[0]
+    idx, coef = dpb.encode(plan, x)
+    u = dpb.decode(plan, idx, coef, act)
+    y = torch.empty_like(u)
+    gref = torch.empty_like(u)
+    ws = dpb.variance_workspace(plan, T, dev)
+    gen = torch.Generator().manual_seed(5)
+    rows = torch.arange(T, dtype=torch.int32).to(dev)
+    slots = torch.randint(0, k, (T,), generator=gen, dtype=torch.int32).to(dev)
+    ops = torch.randint(0, 3, (T,), generator=gen, dtype=torch.int32).to(dev)
+    tidx, tcoef = dpb.encode(plan, sets[1][0])
+    n_min = 2
+    xg = x.detach().clone().requires_grad_(True)
+
+    def layer():
+        yy, lv = dpb_autograd.dpb_layer(xg, plan, True, n_min)
+        torch.autograd.backward([yy, lv], [g, torch.ones((), device=dev)])
+        xg.grad = None
+
+    cases = {
+        "normalize": (lambda: dpb.normalize(plan, u, x, y=y), 3 * d * xb),
+        "normalize_bwd": (lambda: dpb.normalize_bwd(plan, g, u, x, grad_ref=gref), 5 * d * xb),
+        "variance_loss": (lambda: dpb.variance_loss(plan, idx, coef, n_min, workspace=ws), 12 * k),
+        "edit_codes": (lambda: dpb.edit_codes(plan, idx, coef, rows, slots, ops, tidx, tcoef), 16 * k),
+        "layer_fwd_bwd": (layer, None),
+    }
+    res = {}
+    for name, (fn, bpt) in cases.items():
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(steps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / steps
+        rec = {"ms": round(ms, 4)}
+        if bpt is not None:
+            gbs = bpt * T / (ms * 1e-3) / 1e9
+            rec.update({"bytes_per_launch": bpt * T, "hbm_GBps": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)})
+        else:
+            rec["tokens_per_s"] = round(T / (ms * 1e-3), 1)
+        res[name] = rec
+    res["variance_loss"]["n_min"] = n_min
+    res["edit_codes"]["edits"] = T
+    res["layer_fwd_bwd"]["what"] = "autograd DPB layer: encode, decode, normalization, variance loss and backward"
+    return res
+
+
 def cpu_baseline(name: str, target_s: float = 12.0) -> dict:
     """The oracle (fp64 C, OpenMP over tokens) on a bounded sample of the workload."""
     import oracle
@@ -165,6 +232,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="train")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip timing the normalization, edit and variance-loss kernels and the autograd layer")
     ap.add_argument("--only", choices=["encode", "decode", "decode_bwd"], default=None,
                     help="time a single kernel (for counter runs)")
     ap.add_argument("--with-copy", action="store_true",
@@ -310,6 +379,8 @@ def main() -> int:
         },
         "roofline": roofline,
     }
+    if args.only is None and not args.no_extras:
+        out["extras"] = time_extras(plan, w, sets, act, args.steps)
     if not args.no_cpu_baseline and args.only is None:
         out["cpu_baseline"] = cpu_baseline(args.workload)
     print(json.dumps(out), flush=True)

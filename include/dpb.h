@@ -209,9 +209,13 @@ dpb_status dpb_edit_codes(const dpb_plan* plan, const int32_t* idx, const float*
                           const int32_t* rows, const int32_t* slots, const int32_t* ops, int64_t E,
                           int32_t* out_idx, float* out_coef, void* stream);
 
-/* Bytes of device workspace dpb_variance_loss needs: 12 * 2^n_last + 32,
- * where 2^n_last is the number of features N; 0 for a NULL plan. */
-size_t dpb_variance_workspace_bytes(const dpb_plan* plan);
+/* Bytes of device workspace dpb_variance_loss needs for a batch of T tokens
+ * (0 for a NULL plan or T < 0): 16 bytes per slot (T * k_tot), 2 KiB per
+ * feature of the low levels (the S <= 4096 smallest indices, counted per
+ * workgroup), and about 1 KiB per bucket of 1024 to 4096 other features;
+ * each part 256-byte aligned.  About 105 MiB for 65536 tokens at N = 2^20,
+ * k_tot = 96. */
+size_t dpb_variance_workspace_bytes(const dpb_plan* plan, int64_t T);
 
 /* VARIANCE AUXILIARY LOSS (§2.2 "Auxillary losses" equation) over a batch of
  * codes: the coefficients of the slots holding feature i form its sample;
@@ -220,18 +224,32 @@ size_t dpb_variance_workspace_bytes(const dpb_plan* plan);
  *   grad_coef[s] = d loss / d coef[s] = -(2/|F|) (coef[s] - mean_i) / count_i
  *                  for slots of features in F, else 0.
  * Slots whose index is outside [0, N) (padding) are not samples.
- *   idx, coef : device [T, k_tot] (read)
- *   workspace : device, >= dpb_variance_workspace_bytes(plan), 16-B aligned;
- *               caller-owned scratch, overwritten (cleared by the call itself)
+ *   idx, coef  : device [T, k_tot] (read)
+ *   workspace  : device, >= dpb_variance_workspace_bytes(plan, T) bytes,
+ *                16-B aligned; caller-owned scratch, overwritten (nothing in it
+ *                needs to be cleared); afterwards it holds what
+ *                dpb_variance_grad reads
  *   loss       : device fp32 scalar (written)
  *   grad_coef  : device [T, k_tot] fp32 (written), or NULL for the loss only
  *   grad_scale : device fp32 scalar multiplying grad_coef (the upstream
  *                gradient of the loss in a backward pass), or NULL for 1
- * Per-feature sums accumulate with fp32 atomics (their order, and so the last
- * bits, vary from run to run); the sum over features in fp64. */
+ * Features of the low levels accumulate sums, then squared deviations about
+ * the mean, in fp32; the others sums of a and a^2 in fp64.  Both use LDS
+ * atomics, whose order (and so the last bits) may vary from run to run; the
+ * sum over features is taken in fp64 in a fixed order.  T = 0 still writes
+ * loss = 0.  DPB_EUNSUPPORTED when N exceeds 2^24 + 4096 or T * k_tot
+ * reaches 2^31. */
 dpb_status dpb_variance_loss(const dpb_plan* plan, const int32_t* idx, const float* coef, int64_t T,
                              int n_min, void* workspace, size_t ws_bytes, float* loss, float* grad_coef,
                              const float* grad_scale, void* stream);
+
+/* Gradient of the variance auxiliary loss alone (a backward pass after a
+ * forward that computed the loss): from what a dpb_variance_loss call over T
+ * tokens left in `workspace`, writes grad_coef [T, k_tot] exactly as that
+ * call would have, times *grad_scale (NULL: 1).  The workspace must not have
+ * been used by another call in between; it is only read. */
+dpb_status dpb_variance_grad(const dpb_plan* plan, int64_t T, const void* workspace, size_t ws_bytes,
+                             float* grad_coef, const float* grad_scale, void* stream);
 
 #ifdef __cplusplus
 }

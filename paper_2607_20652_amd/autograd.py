@@ -4,7 +4,8 @@
   * forward: encode (§2.2 beam search), decode (§2.1), and, when `normalized`,
     the rescaling of the decoder output to ||x|| (§2.2 "Normalized
     Reconstruction"); loss_var is the variance auxiliary loss of the code
-    (§2.2 "Auxillary losses"), or 0 when n_min is None;
+    (§2.2 "Auxillary losses"), or 0 when n_min is None; its per-slot
+    pre-gradients stay in a workspace for the backward;
   * backward: the indices are held fixed and coef = Phi_S x, so
         grad_u    = backward of the normalization (dpb_normalize_bwd),
         grad_coef = Phi_S^T grad_u + g_loss * dL_var/dcoef,
@@ -32,19 +33,21 @@ class DPBLayer(torch.autograd.Function):
         idx, coef = B.encode(plan, x)
         u = B.decode(plan, idx, coef, x.dtype)
         y = B.normalize(plan, u, x) if normalized else u
+        ws = None
         if n_min is not None:
-            loss, _ = B.variance_loss(plan, idx, coef, n_min, with_grad=False)
+            ws = B.variance_workspace(plan, x.shape[0], x.device)
+            loss, _ = B.variance_loss(plan, idx, coef, n_min, with_grad=False, workspace=ws)
         else:
             loss = torch.zeros((), dtype=torch.float32, device=x.device)
         ctx.plan, ctx.normalized, ctx.n_min = plan, normalized, n_min
-        ctx.save_for_backward(x, idx, coef, u)
+        ctx.save_for_backward(x, idx, coef, u, ws)
         ctx.set_materialize_grads(False)
         return y, loss
 
     @staticmethod
     def backward(ctx, gy: torch.Tensor | None, gloss: torch.Tensor | None):
         plan = ctx.plan
-        x, idx, coef, u = ctx.saved_tensors
+        x, idx, coef, u, ws = ctx.saved_tensors
         if gy is None:
             gy = torch.zeros_like(x)
         gy = gy.contiguous()
@@ -54,8 +57,8 @@ class DPBLayer(torch.autograd.Function):
             gu, gx = gy, None
         add_gc = None
         if gloss is not None and ctx.n_min is not None:
-            _, add_gc = B.variance_loss(plan, idx, coef, ctx.n_min, with_grad=True,
-                                        grad_scale=gloss.to(torch.float32).contiguous())
+            # the forward left the per-slot pre-gradients in ws
+            add_gc = B.variance_grad(plan, x.shape[0], ws, grad_scale=gloss.to(torch.float32).contiguous())
         _, gx = B.decode_bwd_ex(plan, idx, gu, add_grad_coef=add_gc, add_grad_x=gx, gx_dtype=x.dtype, grad_x=gx)
         return gx, None, None, None
 

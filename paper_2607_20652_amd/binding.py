@@ -54,8 +54,9 @@ def load():
         "dpb_normalize": (i32, [P, P, i32, P, i32, P, i64, i64, P, i32, P, P]),
         "dpb_normalize_bwd": (i32, [P, P, i32, P, i32, P, i32, i64, P, i32, P, i32, i32, P]),
         "dpb_edit_codes": (i32, [P, P, P, P, P, i64, P, P, P, i64, P, P, P]),
-        "dpb_variance_workspace_bytes": (ctypes.c_size_t, [P]),
+        "dpb_variance_workspace_bytes": (ctypes.c_size_t, [P, i64]),
         "dpb_variance_loss": (i32, [P, P, P, i64, i32, P, ctypes.c_size_t, P, P, P, P]),
+        "dpb_variance_grad": (i32, [P, i64, P, ctypes.c_size_t, P, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -302,8 +303,13 @@ def edit_codes(plan: Plan, idx: torch.Tensor, coef: torch.Tensor, rows: torch.Te
     return out_idx, out_coef
 
 
-def variance_workspace_bytes(plan: Plan) -> int:
-    return int(load().dpb_variance_workspace_bytes(plan._handle))
+def variance_workspace_bytes(plan: Plan, T: int) -> int:
+    return int(load().dpb_variance_workspace_bytes(plan._handle, int(T)))
+
+
+def variance_workspace(plan: Plan, T: int, device) -> torch.Tensor:
+    """A device buffer of dpb_variance_workspace_bytes(plan, T) bytes."""
+    return torch.empty((variance_workspace_bytes(plan, T) + 15) // 16 * 4, dtype=torch.float32, device=device)
 
 
 def variance_loss(plan: Plan, idx: torch.Tensor, coef: torch.Tensor, n_min: int, with_grad: bool = True,
@@ -313,10 +319,8 @@ def variance_loss(plan: Plan, idx: torch.Tensor, coef: torch.Tensor, n_min: int,
     grad_scale when given."""
     T = idx.shape[0]
     assert idx.shape == coef.shape == (T, plan.k_tot) and idx.dtype == torch.int32 and coef.dtype == torch.float32
-    nbytes = variance_workspace_bytes(plan)
     if workspace is None:
-        workspace = torch.empty((nbytes + 15) // 16 * 4, dtype=torch.float32, device=idx.device)
-    assert workspace.numel() * workspace.element_size() >= nbytes
+        workspace = variance_workspace(plan, T, idx.device)
     loss = torch.empty((), dtype=torch.float32, device=idx.device)
     grad = torch.empty((T, plan.k_tot), dtype=torch.float32, device=idx.device) if with_grad else None
     _check("dpb_variance_loss", load().dpb_variance_loss(
@@ -324,3 +328,15 @@ def variance_loss(plan: Plan, idx: torch.Tensor, coef: torch.Tensor, n_min: int,
         workspace.numel() * workspace.element_size(), _dev(loss, "loss"), _opt(grad, "grad_coef"),
         _opt(grad_scale, "grad_scale"), _stream(idx)))
     return loss, grad
+
+
+def variance_grad(plan: Plan, T: int, workspace: torch.Tensor, grad_scale: torch.Tensor | None = None,
+                  grad: torch.Tensor | None = None):
+    """Gradient of the variance loss from what a variance_loss call over T
+    tokens left in `workspace`."""
+    if grad is None:
+        grad = torch.empty((T, plan.k_tot), dtype=torch.float32, device=workspace.device)
+    _check("dpb_variance_grad", load().dpb_variance_grad(
+        plan._handle, int(T), _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
+        _dev(grad, "grad_coef"), _opt(grad_scale, "grad_scale"), _stream(workspace)))
+    return grad

@@ -593,10 +593,12 @@ dpb_status dpb_edit_codes(const dpb_plan* plan, const int32_t* idx, const float*
                                            out_idx, out_coef, (hipStream_t)stream));
 }
 
-size_t dpb_variance_workspace_bytes(const dpb_plan* plan)
+size_t dpb_variance_workspace_bytes(const dpb_plan* plan, int64_t T)
 {
-    if (!plan) return 0;
-    return dpb::variance_workspace_bytes((int64_t)1 << plan->dev.level_bits[plan->dev.levels - 1]);
+    if (!plan || T < 0) return 0;
+    const DevPlan& P = plan->dev;
+    return dpb::variance_workspace_bytes((int64_t)1 << P.level_bits[P.levels - 1],
+                                         dpb::variance_small_range(P.level_bits, P.levels), T * P.k_tot);
 }
 
 dpb_status dpb_variance_loss(const dpb_plan* plan, const int32_t* idx, const float* coef, int64_t T, int n_min,
@@ -605,12 +607,31 @@ dpb_status dpb_variance_loss(const dpb_plan* plan, const int32_t* idx, const flo
 {
     dpb_status s = check_call(plan, T);
     if (s) return s;
-    if (!loss || !workspace || !aligned16(workspace) || ws_bytes < dpb_variance_workspace_bytes(plan))
+    if (!loss || !workspace || !aligned16(workspace) || ws_bytes < dpb_variance_workspace_bytes(plan, T))
         return DPB_EINVAL;
     if (T > 0 && (!idx || !coef || !aligned16(idx) || !aligned16(coef) || !aligned16(grad_coef))) return DPB_EINVAL;
-    const int64_t nfeat = (int64_t)1 << plan->dev.level_bits[plan->dev.levels - 1];
-    return launched(dpb::launch_variance_loss(idx, coef, T * plan->dev.k_tot, nfeat, n_min, workspace, loss,
+    const DevPlan& P = plan->dev;
+    const int64_t nfeat = (int64_t)1 << P.level_bits[P.levels - 1];
+    const int S = dpb::variance_small_range(P.level_bits, P.levels);
+    if (!dpb::variance_supported(nfeat, S, T * P.k_tot)) return DPB_EUNSUPPORTED;
+    return launched(dpb::launch_variance_loss(idx, coef, T, P.k_tot, nfeat, S, n_min, workspace, loss,
                                               T > 0 ? grad_coef : nullptr, grad_scale, (hipStream_t)stream));
+}
+
+dpb_status dpb_variance_grad(const dpb_plan* plan, int64_t T, const void* workspace, size_t ws_bytes,
+                             float* grad_coef, const float* grad_scale, void* stream)
+{
+    dpb_status s = check_call(plan, T);
+    if (s) return s;
+    if (!workspace || !aligned16(workspace) || ws_bytes < dpb_variance_workspace_bytes(plan, T)) return DPB_EINVAL;
+    if (T == 0) return DPB_OK;
+    if (!grad_coef || !aligned16(grad_coef)) return DPB_EINVAL;
+    const DevPlan& P = plan->dev;
+    const int64_t nfeat = (int64_t)1 << P.level_bits[P.levels - 1];
+    const int S = dpb::variance_small_range(P.level_bits, P.levels);
+    if (!dpb::variance_supported(nfeat, S, T * P.k_tot)) return DPB_EUNSUPPORTED;
+    return launched(dpb::launch_variance_grad(T, P.k_tot, nfeat, S, const_cast<void*>(workspace), grad_coef,
+                                              grad_scale, (hipStream_t)stream));
 }
 
 }  // extern "C"

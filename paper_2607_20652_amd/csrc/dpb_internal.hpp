@@ -189,9 +189,14 @@ hipError_t launch_normalize_bwd(int d, int64_t T, const void* g, bool g16, const
 hipError_t launch_edit_codes(const int32_t* idx, const float* coef, const int32_t* tidx, const float* tcoef,
                              int64_t T, int k, const int32_t* rows, const int32_t* slots, const int32_t* ops,
                              int64_t E, int32_t* out_idx, float* out_coef, hipStream_t stream);
-size_t variance_workspace_bytes(int64_t nfeat);
-hipError_t launch_variance_loss(const int32_t* idx, const float* coef, int64_t n, int64_t nfeat, int n_min,
-                                void* ws, float* loss, float* grad, const float* grad_scale, hipStream_t stream);
+int variance_small_range(const int* level_bits, int levels);
+bool variance_supported(int64_t nfeat, int S, int64_t nslots);
+size_t variance_workspace_bytes(int64_t nfeat, int S, int64_t nslots);
+hipError_t launch_variance_loss(const int32_t* idx, const float* coef, int64_t T, int k, int64_t nfeat, int S,
+                                int n_min, void* ws, float* loss, float* grad, const float* grad_scale,
+                                hipStream_t stream);
+hipError_t launch_variance_grad(int64_t T, int k, int64_t nfeat, int S, void* ws, float* grad,
+                                const float* grad_scale, hipStream_t stream);
 
 hipError_t launch_encode(const DevPlan& P, const void* x, bool x_bf16, int64_t T, int32_t* idx,
                          float* coef, hipStream_t stream);

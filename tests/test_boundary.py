@@ -92,7 +92,8 @@ def test_compute_calls_reject_null_plan(lib):
     assert lib.dpb_normalize_bwd(None, P(16), 0, P(16), 0, P(16), 0, 4, P(32), 0, P(48), 0, 0, None) == -1
     assert lib.dpb_edit_codes(None, P(16), P(16), None, None, 4, P(16), P(32), P(48), 2, P(64), P(80), None) == -1
     assert lib.dpb_variance_loss(None, P(16), P(16), 4, 1, P(16), 1 << 20, P(16), None, None, None) == -1
-    assert lib.dpb_variance_workspace_bytes(None) == 0
+    assert lib.dpb_variance_grad(None, 4, P(16), 1 << 20, P(16), None, None) == -1
+    assert lib.dpb_variance_workspace_bytes(None, 4) == 0
     assert lib.dpb_plan_code_width(None) == 0
     lib.dpb_plan_destroy(None)
 

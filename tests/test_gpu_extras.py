@@ -199,6 +199,25 @@ def test_variance_loss_matches_oracle(name, T, n_min):
     compare_dense(grad2.cpu().numpy(), 0.37 * rg, TOL_F32)
 
 
+@pytest.mark.parametrize("name,T", [("tiny", 256), ("train", 1024)])
+def test_variance_grad_from_forward_statistics(name, T):
+    """dpb_variance_grad after dpb_variance_loss equals the gradient the loss
+    call computes itself, and the loss of a repeated call is identical."""
+    say(f"[variance grad] {name} T={T}")
+    plan = plan_for(name)
+    idx, coef = dpb.encode(plan, inputs.activations(name, T).to(DEV))
+    ws = dpb.variance_workspace(plan, T, DEV)
+    scale = torch.tensor(-1.7, device=DEV)
+    loss, grad = dpb.variance_loss(plan, idx, coef, 2, workspace=ws, grad_scale=scale)
+    g2 = dpb.variance_grad(plan, T, ws, grad_scale=scale)
+    loss2, _ = dpb.variance_loss(plan, idx, coef, 2, with_grad=False)
+    torch.cuda.synchronize()
+    assert torch.equal(g2, grad)
+    assert abs(loss2.item() - loss.item()) <= 1e-6 * abs(loss.item())
+    rl, rg = oracle.variance_loss(idx.cpu().numpy(), coef.cpu().numpy().astype(np.float64), 2)
+    compare_dense(g2.cpu().numpy(), -1.7 * rg, TOL_F32)
+
+
 def test_variance_loss_empty_batch():
     plan = plan_for("tiny")
     idx = torch.empty((0, plan.k_tot), dtype=torch.int32, device=DEV)
