@@ -63,6 +63,8 @@ def _load():
         "oracle_walsh_spectrum": (i32, [i32, P, i32, P]),
         "oracle_normalize": (None, [i32, i64, P, P, P, P]),
         "oracle_normalize_bwd": (None, [i32, i64, P, P, P, P, P]),
+        "oracle_encode_std": (i32, [i32, P, i32, P, P, P, P, P, i64, P, P, P, P, P, P]),
+        "oracle_std_update": (None, [i32, P, i32, P, P, P, P, P, i64, P, i32, dbl, P, P]),
         "oracle_edit_codes": (None, [i64, i32, P, P, P, P, i64, P, P, P, P, P]),
         "oracle_variance_loss": (dbl, [i64, i32, P, P, i32, P]),
         "oracle_num_threads": (i32, []),
@@ -201,6 +203,60 @@ def encode(d: int, m: np.ndarray, nbits, active, delta, gens: list[np.ndarray], 
     if rc < 0:
         raise ValueError("oracle_encode: bad arguments")
     return idx, coef, margin, order
+
+
+def _hier_arrays(nbits, active, delta, gens):
+    L = len(nbits)
+    nb = np.asarray(nbits, dtype=np.int32)
+    ac = np.asarray(active, dtype=np.int32)
+    dl = np.asarray(delta, dtype=np.int32)
+    g = np.concatenate([np.asarray(gg, dtype=np.uint32) for gg in gens[1:]]) if L > 1 else np.zeros(1, np.uint32)
+    g = np.ascontiguousarray(g if g.size else np.zeros(1, np.uint32), dtype=np.uint32)
+    return L, nb, ac, dl, g
+
+
+def encode_std(d: int, m: np.ndarray, nbits, active, delta, gens: list[np.ndarray], x: np.ndarray,
+               mu: np.ndarray, r: np.ndarray):
+    """Beam-search encoder on standardized scores z = (s - mu) r (§2.2 "Score
+    Standardization"); mu and r are fp32 per feature (2^n_last entries each).
+    Level-0 z is taken in fp32, the levels above in fp64.  Returns idx, coef
+    (= z), and the margins of |z| as in encode()."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    T = x.shape[0]
+    assert x.shape[1] == d
+    L, nb, ac, dl, g = _hier_arrays(nbits, active, delta, gens)
+    mu = np.ascontiguousarray(mu, dtype=np.float32)
+    r = np.ascontiguousarray(r, dtype=np.float32)
+    assert mu.shape == r.shape == (1 << int(nb[-1]),)
+    k_tot = int(ac.sum())
+    idx = np.zeros((T, k_tot), dtype=np.int32)
+    coef = np.zeros((T, k_tot), dtype=np.float64)
+    margin = np.zeros((T, L), dtype=np.float64)
+    order = np.zeros((T, L), dtype=np.float64)
+    rc = _load().oracle_encode_std(d, _ptr(m), L, _ptr(nb), _ptr(ac), _ptr(dl), _ptr(g), _ptr(x), T,
+                                   _ptr(mu), _ptr(r), _ptr(idx), _ptr(coef), _ptr(margin), _ptr(order))
+    if rc < 0:
+        raise ValueError("oracle_encode_std: bad arguments")
+    return idx, coef, margin, order
+
+
+def std_update(d: int, m: np.ndarray, nbits, active, delta, gens: list[np.ndarray], x: np.ndarray,
+               idx: np.ndarray, mu: np.ndarray, var: np.ndarray, beta: float, sample: int = 64):
+    """EMA update of the standardization statistics after a batch (§2.2
+    "Score Standardization"; sampling and update rule are readings).  x is
+    the batch, idx its code; mu, var fp64 [2^n_last].  Returns updated
+    copies (mu, var)."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    T = x.shape[0]
+    L, nb, ac, dl, g = _hier_arrays(nbits, active, delta, gens)
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    assert idx.shape == (T, int(ac.sum()))
+    mu = np.array(mu, dtype=np.float64, order="C")
+    var = np.array(var, dtype=np.float64, order="C")
+    assert mu.shape == var.shape == (1 << int(nb[-1]),)
+    _load().oracle_std_update(d, _ptr(m), L, _ptr(nb), _ptr(ac), _ptr(dl), _ptr(g), _ptr(x), T, _ptr(idx),
+                              int(sample), float(beta), _ptr(mu), _ptr(var))
+    return mu, var
 
 
 def decode(d: int, m: np.ndarray, idx: np.ndarray, coef: np.ndarray) -> np.ndarray:

@@ -27,8 +27,10 @@
  *   R8  AbsTopK key: |score| descending, then index ascending; coefficient is
  *       the signed score; level-0 coefficient is x_iota itself (Eq. 2).
  *   R9  every level is emitted, level-major, so k_tot = sum_l K_l.
- *   R10 selection scores are the raw scores (EMA standardization with mean 0,
- *       std 1, i.e. its initial state; §2.2 "Score Standardization").
+ *   R10 without statistics, selection scores are the raw scores (EMA
+ *       standardization at its initial state, mean 0 and std 1); with them,
+ *       z = (s - mu) r, r = 1/sigma (§2.2 "Score Standardization"; the
+ *       statistics are R16-R18 in the design notes).
  *   R11 backward: grad_coef = Phi_S^T g, grad_x = Phi_S grad_coef.
  */
 #include <math.h>
@@ -343,9 +345,51 @@ static void margins_of(const cand_t* sorted, int n, int K, double* boundary, dou
  * [T, levels] (may be NULL).  gens: level-by-level generator words.
  * Returns 0, or -1 on bad arguments.
  */
+/* Standardized level-0 score (§2.2 "Score Standardization") of a basis
+ * feature: z = (x - mu) * r with r = 1/sigma, taken in fp32 -- the precision
+ * the kernel takes it in -- so that both sides select the same level-0
+ * features (x is an exact fp32 value).  Without statistics, z = x. */
+static double std_score0(double x, const float* mu, const float* r, int64_t c)
+{
+    if (!mu) return x;
+    const float t = (float)x - mu[c];
+    const float z = t * r[c];
+    return (double)z;
+}
+
+/* Standardized score of a hashed feature, in fp64. */
+static double std_score(double s, const float* mu, const float* r, int64_t c)
+{
+    return mu ? (s - (double)mu[c]) * (double)r[c] : s;
+}
+
+static int encode_impl(int d, const uint32_t* masks, int levels, const int* nbits, const int* active,
+                       const int* delta, const uint32_t* gens, const double* x, int64_t T, const float* mu,
+                       const float* r, int32_t* idx, double* coef, double* margin, double* order_margin);
+
 int oracle_encode(int d, const uint32_t* masks, int levels, const int* nbits, const int* active,
                   const int* delta, const uint32_t* gens, const double* x, int64_t T,
                   int32_t* idx, double* coef, double* margin, double* order_margin)
+{
+    return encode_impl(d, masks, levels, nbits, active, delta, gens, x, T, NULL, NULL, idx, coef, margin,
+                       order_margin);
+}
+
+/* The encoder on standardized scores z_c = (s_c - mu_c) r_c (§2.2 "Score
+ * Standardization"): AbsTopK on |z|, and z is the coefficient passed to the
+ * decoder.  mu, r: fp32 per feature, N = 2^nbits[levels-1] entries each. */
+int oracle_encode_std(int d, const uint32_t* masks, int levels, const int* nbits, const int* active,
+                      const int* delta, const uint32_t* gens, const double* x, int64_t T, const float* mu,
+                      const float* r, int32_t* idx, double* coef, double* margin, double* order_margin)
+{
+    if (!mu || !r) return -1;
+    return encode_impl(d, masks, levels, nbits, active, delta, gens, x, T, mu, r, idx, coef, margin,
+                       order_margin);
+}
+
+static int encode_impl(int d, const uint32_t* masks, int levels, const int* nbits, const int* active,
+                       const int* delta, const uint32_t* gens, const double* x, int64_t T, const float* mu,
+                       const float* r, int32_t* idx, double* coef, double* margin, double* order_margin)
 {
     int k_tot = 0;
     int max_cand = d;
@@ -370,7 +414,7 @@ int oracle_encode(int d, const uint32_t* masks, int levels, const int* nbits, co
 
             /* Level 0: basis features, score = x_iota (a coordinate read). */
             for (int iota = 0; iota < d; ++iota) {
-                cand[iota].score = xt[iota];
+                cand[iota].score = std_score0(xt[iota], mu, r, iota);
                 cand[iota].index = iota;
             }
             qsort(cand, (size_t)d, sizeof(cand_t), cand_cmp);
@@ -393,7 +437,7 @@ int oracle_encode(int d, const uint32_t* masks, int levels, const int* nbits, co
                 for (int i = 0; i < n_ids; ++i) {
                     if (i > 0 && ids[i] == ids[i - 1]) continue; /* reading R7 */
                     cand[n_cand].index = ids[i];
-                    cand[n_cand].score = dense_score(d, masks, ids[i], xt);
+                    cand[n_cand].score = std_score(dense_score(d, masks, ids[i], xt), mu, r, ids[i]);
                     ++n_cand;
                 }
                 qsort(cand, (size_t)n_cand, sizeof(cand_t), cand_cmp);
@@ -491,6 +535,89 @@ int oracle_walsh_spectrum(int d, const uint32_t* masks, int r, int64_t* S)
         }
     }
     return 0;
+}
+
+/* EMA update of the standardization statistics (§2.2 "Score
+ * Standardization") after a batch encoded with them.  The statistics of a
+ * feature are taken over the tokens where it was a candidate: a basis
+ * feature (level 0) is a candidate at every token, so its sample is the
+ * column x[:, iota] of the whole batch; a feature of level l >= 1 is a
+ * candidate where it is a child p XOR g_j of an active parent p (a level
+ * l-1 entry of the token's code), and its sample is taken on the `sample`
+ * tokens t_j = floor(j T / m), j < m = min(sample, T) (the paper's 64-token
+ * sub-samples), one raw score <phi_c, x_t> per token even when several
+ * parents reach it.  For every feature with n >= 1 samples, mean m1 and
+ * population variance v:
+ *     mu <- (1 - beta) mu + beta m1,   var <- (1 - beta) var + beta v.
+ * Features with no sample keep their state.  mu, var: fp64 [N]. */
+void oracle_std_update(int d, const uint32_t* masks, int levels, const int* nbits, const int* active,
+                       const int* delta, const uint32_t* gens, const double* x, int64_t T, const int32_t* idx,
+                       int sample, double beta, double* mu, double* var)
+{
+    const int64_t N = (int64_t)1 << nbits[levels - 1];
+    int k_tot = 0, max_ids = 1;
+    for (int l = 0; l < levels; ++l) {
+        k_tot += active[l];
+        if (l > 0 && active[l - 1] * delta[l] > max_ids) max_ids = active[l - 1] * delta[l];
+    }
+    double* cnt = (double*)calloc((size_t)N, sizeof(double));
+    double* s1 = (double*)calloc((size_t)N, sizeof(double));
+    double* s2 = (double*)calloc((size_t)N, sizeof(double));
+    int64_t* ids = (int64_t*)malloc(sizeof(int64_t) * (size_t)max_ids);
+    const int64_t m = T < sample ? T : sample;
+    /* pass 1: counts and sums; pass 2: squared deviations about the mean */
+    for (int pass = 0; pass < 2; ++pass) {
+        for (int64_t t = 0; t < T; ++t)
+            for (int iota = 0; iota < d; ++iota) {
+                const double v = x[t * d + iota];
+                if (pass == 0) {
+                    cnt[iota] += 1.0;
+                    s1[iota] += v;
+                } else {
+                    const double dv = v - s1[iota] / cnt[iota];
+                    s2[iota] += dv * dv;
+                }
+            }
+        for (int64_t j = 0; j < m; ++j) {
+            const int64_t t = (j * T) / m;
+            const int32_t* code = idx + t * k_tot;
+            const uint32_t* g = gens;
+            int slot = 0;
+            for (int l = 1; l < levels; ++l) {
+                const int pb = slot;          /* the parents: level l-1 entries */
+                slot += active[l - 1];
+                int n_ids = 0;
+                for (int q = pb; q < slot; ++q) {
+                    if (code[q] < 0) continue;
+                    for (int jj = 0; jj < delta[l]; ++jj) ids[n_ids++] = (int64_t)code[q] ^ (int64_t)g[jj];
+                }
+                qsort(ids, (size_t)n_ids, sizeof(int64_t), idx_cmp);
+                for (int i = 0; i < n_ids; ++i) {
+                    if (i > 0 && ids[i] == ids[i - 1]) continue;
+                    const int64_t c = ids[i];
+                    const double v = dense_score(d, masks, c, x + t * d);
+                    if (pass == 0) {
+                        cnt[c] += 1.0;
+                        s1[c] += v;
+                    } else {
+                        const double dv = v - s1[c] / cnt[c];
+                        s2[c] += dv * dv;
+                    }
+                }
+                g += delta[l];
+            }
+        }
+    }
+    for (int64_t c = 0; c < N; ++c) {
+        if (cnt[c] == 0.0) continue;
+        const double m1 = s1[c] / cnt[c], v = s2[c] / cnt[c];
+        mu[c] = (1.0 - beta) * mu[c] + beta * m1;
+        var[c] = (1.0 - beta) * var[c] + beta * v;
+    }
+    free(cnt);
+    free(s1);
+    free(s2);
+    free(ids);
 }
 
 /* ------------------------------------------------------------------ */
