@@ -144,12 +144,60 @@ dpb_status dpb_decode_bwd(const dpb_plan* plan, const int32_t* idx, const void* 
  *   add_grad_x    : device [T, d] in gx_dtype, or NULL for none (read); may
  *                   be the same buffer as grad_x (each element is read
  *                   before it is written, by the same thread).
- * Every other argument as in dpb_decode_bwd; with both extras NULL the
+ *   stats         : the standardization statistics the code was encoded
+ *                   with (see dpb_encode_std), or NULL.  A standardized
+ *                   coefficient z = (s - mu) r moves with x as r phi, so
+ *                   grad_x = sum_s grad_coef[s] r_{idx_s} phi_{idx_s} + add_grad_x
+ *                   (grad_coef itself is unchanged).
+ * Every other argument as in dpb_decode_bwd; with all three extras NULL the
  * results equal dpb_decode_bwd's. */
 dpb_status dpb_decode_bwd_ex(const dpb_plan* plan, const int32_t* idx, const void* grad_y,
                              dpb_dtype g_dtype, int64_t T, const float* add_grad_coef,
-                             const void* add_grad_x, float* grad_coef, void* grad_x,
-                             dpb_dtype gx_dtype, void* stream);
+                             const void* add_grad_x, const float* stats, float* grad_coef,
+                             void* grad_x, dpb_dtype gx_dtype, void* stream);
+
+/* SCORE STANDARDIZATION (§2.2 "Score Standardization").  The state is two
+ * caller-owned device arrays over all N = 2^n_last features:
+ *   stats : fp32 [N][2] = (mu, r): the EMA mean of the feature's raw score and
+ *           r = 1 / sigma, sigma^2 = var + eps at the last update
+ *   var   : fp32 [N], the EMA of the variance
+ * Initial state (dpb_std_init): mu = 0, r = 1, var = 1 -- with it the
+ * standardized encoder equals dpb_encode. */
+#define DPB_STD_SAMPLE 64   /* tokens per batch for the moments of levels >= 1 */
+
+dpb_status dpb_std_init(const dpb_plan* plan, float* stats, float* var, void* stream);
+
+/* ENCODE on standardized scores: every candidate's raw score s_c becomes
+ * z_c = (s_c - mu_c) r_c; AbsTopK runs on |z| (ties to the lower index) and
+ * z is the coefficient written to the code.  Level-0 z is computed in fp32
+ * as (x - mu) * r.  Arguments as dpb_encode, plus
+ *   stats : device fp32 [N][2] (read).
+ * DPB_EUNSUPPORTED for plans outside the fast encoder's limits. */
+dpb_status dpb_encode_std(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T,
+                          const float* stats, int32_t* idx, float* coef, void* stream);
+
+/* Bytes of device workspace dpb_std_update needs (0 for a NULL plan):
+ * 32 bytes per feature, 4 KiB per coordinate, and 8 bytes per candidate of
+ * the sampled tokens. */
+size_t dpb_std_workspace_bytes(const dpb_plan* plan);
+
+/* EMA UPDATE after a batch encoded with dpb_encode_std (x, T, and its code
+ * idx).  Each feature's sample is its raw scores on the tokens where it was
+ * a candidate: every token for a basis feature (s = x_iota); for a feature
+ * of level l >= 1, the tokens t_j = floor(j T / m), j < m = min(T, 64), at
+ * which it is a child p XOR g_j of an active parent p (a level l-1 entry of
+ * that token's code), counted once per token, s = <phi_c, x_t>.  A feature
+ * with n samples, mean m1 and population variance v gets
+ *   mu <- (1 - momentum) mu + momentum m1,  var <- (1 - momentum) var + momentum v,
+ *   r = 1 / sqrt(var + eps);
+ * other features keep their state.  Moments accumulate in fp64.
+ *   momentum in [0, 1], eps >= 0
+ *   stats, var : device (read and written)
+ *   workspace  : device, >= dpb_std_workspace_bytes(plan), 16-B aligned;
+ *                caller-owned scratch, overwritten, no clearing needed */
+dpb_status dpb_std_update(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T,
+                          const int32_t* idx, float momentum, float eps, float* stats, float* var,
+                          void* workspace, size_t ws_bytes, void* stream);
 
 /* NORMALIZED RECONSTRUCTION (§2.2 "Normalized Reconstruction"): each row of
  * the decoder output u is rescaled to the norm of the bottleneck input,

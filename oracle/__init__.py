@@ -346,13 +346,14 @@ def variance_loss(idx: np.ndarray, coef: np.ndarray, n_min: int):
 
 
 def layer_backward(d: int, m: np.ndarray, idx: np.ndarray, coef: np.ndarray, x: np.ndarray, gy: np.ndarray,
-                   gloss: float, n_min: int, normalized: bool = True):
+                   gloss: float, n_min: int, normalized: bool = True, r_slot: np.ndarray | None = None):
     """Gradients of a DPB layer with the indices held fixed (coef = Phi_S x,
-    u = Phi_S^T coef, y = u ||x|| / ||u|| when normalized, else y = u) under
-    the loss <gy, y> + gloss * L_var(coef), composed from the oracle's parts:
+    or with standardization coef = (Phi_S x - mu) r; u = Phi_S^T coef,
+    y = u ||x|| / ||u|| when normalized, else y = u) under the loss
+    <gy, y> + gloss * L_var(coef), composed from the oracle's parts:
         gu, gref  = normalize_bwd(gy, u, x)            (gu = gy, gref = 0 if not normalized)
         grad_coef = Phi_S^T gu + gloss * dL_var/dcoef
-        grad_x    = Phi_S grad_coef + gref
+        grad_x    = Phi_S (r grad_coef) + gref         (r = r_slot [T, k], else 1)
     Returns (grad_coef [T, k], grad_x [T, d]) in fp64."""
     x = np.asarray(x, dtype=np.float64)
     gy = np.asarray(gy, dtype=np.float64)
@@ -361,10 +362,11 @@ def layer_backward(d: int, m: np.ndarray, idx: np.ndarray, coef: np.ndarray, x: 
         gu, gref = normalize_bwd(gy, u, x)
     else:
         gu, gref = gy, np.zeros_like(x)
-    gc, gx = decode_bwd(d, m, idx, gu)
+    gc, _ = decode_bwd(d, m, idx, gu)
     _, vg = variance_loss(idx, coef, n_min)
-    extra = gloss * vg
-    return gc + extra, gx + decode(d, m, idx, extra) + gref
+    gc = gc + gloss * vg
+    scaled = gc if r_slot is None else gc * np.asarray(r_slot, dtype=np.float64)
+    return gc, decode(d, m, idx, scaled) + gref
 
 
 def num_threads() -> int:

@@ -50,7 +50,11 @@ def load():
         "dpb_encode": (i32, [P, P, i32, i64, P, P, P]),
         "dpb_decode": (i32, [P, P, P, i64, P, i32, P]),
         "dpb_decode_bwd": (i32, [P, P, P, i32, i64, P, P, i32, P]),
-        "dpb_decode_bwd_ex": (i32, [P, P, P, i32, i64, P, P, P, P, i32, P]),
+        "dpb_decode_bwd_ex": (i32, [P, P, P, i32, i64, P, P, P, P, P, i32, P]),
+        "dpb_encode_std": (i32, [P, P, i32, i64, P, P, P, P]),
+        "dpb_std_init": (i32, [P, P, P, P]),
+        "dpb_std_workspace_bytes": (ctypes.c_size_t, [P]),
+        "dpb_std_update": (i32, [P, P, i32, i64, P, ctypes.c_float, ctypes.c_float, P, P, P, ctypes.c_size_t, P]),
         "dpb_normalize": (i32, [P, P, i32, P, i32, P, i64, i64, P, i32, P, P]),
         "dpb_normalize_bwd": (i32, [P, P, i32, P, i32, P, i32, i64, P, i32, P, i32, i32, P]),
         "dpb_edit_codes": (i32, [P, P, P, P, P, i64, P, P, P, i64, P, P, P]),
@@ -228,10 +232,12 @@ def _opt(t: torch.Tensor | None, name: str):
 
 def decode_bwd_ex(plan: Plan, idx: torch.Tensor, grad_y: torch.Tensor, add_grad_coef: torch.Tensor | None = None,
                   add_grad_x: torch.Tensor | None = None, gx_dtype: torch.dtype | None = None,
-                  grad_coef: torch.Tensor | None = None, grad_x: torch.Tensor | None = None):
+                  grad_coef: torch.Tensor | None = None, grad_x: torch.Tensor | None = None,
+                  stats: torch.Tensor | None = None):
     """decode_bwd plus extra terms: grad_coef = Phi^T g + add_grad_coef,
-    grad_x = Phi grad_coef + add_grad_x (add_grad_x in grad_x's dtype; it may
-    be grad_x itself)."""
+    grad_x = Phi (r * grad_coef) + add_grad_x, r from the standardization
+    statistics when given (else 1); add_grad_x is in grad_x's dtype and may
+    be grad_x itself."""
     T = idx.shape[0]
     assert idx.dtype == torch.int32 and idx.shape[1] == plan.k_tot and grad_y.shape == (T, plan.d)
     if grad_coef is None:
@@ -244,8 +250,8 @@ def decode_bwd_ex(plan: Plan, idx: torch.Tensor, grad_y: torch.Tensor, add_grad_
         assert add_grad_x.dtype == grad_x.dtype and add_grad_x.shape == (T, plan.d)
     _check("dpb_decode_bwd_ex", load().dpb_decode_bwd_ex(
         plan._handle, _dev(idx, "idx"), _dev(grad_y, "grad_y"), _dtype_code(grad_y), T,
-        _opt(add_grad_coef, "add_grad_coef"), _opt(add_grad_x, "add_grad_x"), _dev(grad_coef, "grad_coef"),
-        _dev(grad_x, "grad_x"), _dtype_code(grad_x), _stream(idx)))
+        _opt(add_grad_coef, "add_grad_coef"), _opt(add_grad_x, "add_grad_x"), _opt(stats, "stats"),
+        _dev(grad_coef, "grad_coef"), _dev(grad_x, "grad_x"), _dtype_code(grad_x), _stream(idx)))
     return grad_coef, grad_x
 
 
@@ -340,3 +346,53 @@ def variance_grad(plan: Plan, T: int, workspace: torch.Tensor, grad_scale: torch
         plan._handle, int(T), _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
         _dev(grad, "grad_coef"), _opt(grad_scale, "grad_scale"), _stream(workspace)))
     return grad
+
+
+STD_SAMPLE = 64
+
+
+def std_state(plan: Plan, device=None):
+    """Fresh standardization state (stats [N, 2] = (mu, r), var [N]) at its
+    initial value (mu 0, r 1, var 1)."""
+    device = device or plan.device
+    N = 1 << plan.level_bits[-1]
+    stats = torch.empty((N, 2), dtype=torch.float32, device=device)
+    var = torch.empty((N,), dtype=torch.float32, device=device)
+    _check("dpb_std_init", load().dpb_std_init(plan._handle, _dev(stats, "stats"), _dev(var, "var"),
+                                               _stream(stats)))
+    return stats, var
+
+
+def encode_std(plan: Plan, x: torch.Tensor, stats: torch.Tensor, idx: torch.Tensor | None = None,
+               coef: torch.Tensor | None = None):
+    """Encoder on standardized scores z = (s - mu) r -> (idx, coef = z)."""
+    T = x.shape[0]
+    assert x.dim() == 2 and x.shape[1] == plan.d
+    assert stats.dtype == torch.float32 and stats.shape == (1 << plan.level_bits[-1], 2)
+    if idx is None:
+        idx = torch.empty((T, plan.k_tot), dtype=torch.int32, device=x.device)
+    if coef is None:
+        coef = torch.empty((T, plan.k_tot), dtype=torch.float32, device=x.device)
+    _check("dpb_encode_std", load().dpb_encode_std(plan._handle, _dev(x, "x"), _dtype_code(x), T,
+                                                   _dev(stats, "stats"), _dev(idx, "idx"), _dev(coef, "coef"),
+                                                   _stream(x)))
+    return idx, coef
+
+
+def std_workspace(plan: Plan, device) -> torch.Tensor:
+    n = int(load().dpb_std_workspace_bytes(plan._handle))
+    return torch.empty(((n + 15) // 16) * 4, dtype=torch.float32, device=device)
+
+
+def std_update(plan: Plan, x: torch.Tensor, idx: torch.Tensor, stats: torch.Tensor, var: torch.Tensor,
+               momentum: float, eps: float = 1e-6, workspace: torch.Tensor | None = None):
+    """EMA update of (stats, var) in place from the batch x and its code idx."""
+    T = x.shape[0]
+    assert idx.shape == (T, plan.k_tot) and idx.dtype == torch.int32
+    if workspace is None:
+        workspace = std_workspace(plan, x.device)
+    _check("dpb_std_update", load().dpb_std_update(
+        plan._handle, _dev(x, "x"), _dtype_code(x), T, _dev(idx, "idx"), float(momentum), float(eps),
+        _dev(stats, "stats"), _dev(var, "var"), _dev(workspace, "workspace"),
+        workspace.numel() * workspace.element_size(), _stream(x)))
+    return stats, var

@@ -10,6 +10,8 @@
 #include "dpb_internal.hpp"
 
 using dpb::DevPlan;
+
+static_assert(dpb::kStdSample == DPB_STD_SAMPLE, "standardization sample size");
 using dpb::Hierarchy;
 
 namespace {
@@ -492,7 +494,8 @@ dpb_status dpb_encode(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, in
     if (T == 0) return DPB_OK;
     if (!x || !idx || !coef || !aligned16(x) || !aligned16(idx) || !aligned16(coef)) return DPB_EINVAL;
     if (dpb::encode2_supported(plan->dev))
-        return launched(dpb::launch_encode2(plan->dev, x, x_dtype == DPB_BF16, T, idx, coef, (hipStream_t)stream));
+        return launched(dpb::launch_encode2(plan->dev, x, x_dtype == DPB_BF16, T, nullptr, idx, coef,
+                                            (hipStream_t)stream));
     return launched(dpb::launch_encode(plan->dev, x, x_dtype == DPB_BF16, T, idx, coef, (hipStream_t)stream));
 }
 
@@ -522,8 +525,8 @@ dpb_status dpb_decode_bwd(const dpb_plan* plan, const int32_t* idx, const void* 
 }
 
 dpb_status dpb_decode_bwd_ex(const dpb_plan* plan, const int32_t* idx, const void* grad_y, dpb_dtype g_dtype,
-                             int64_t T, const float* add_grad_coef, const void* add_grad_x, float* grad_coef,
-                             void* grad_x, dpb_dtype gx_dtype, void* stream)
+                             int64_t T, const float* add_grad_coef, const void* add_grad_x, const float* stats,
+                             float* grad_coef, void* grad_x, dpb_dtype gx_dtype, void* stream)
 {
     dpb_status s = check_call(plan, T);
     if (s) return s;
@@ -532,8 +535,51 @@ dpb_status dpb_decode_bwd_ex(const dpb_plan* plan, const int32_t* idx, const voi
     if (!idx || !grad_y || !grad_coef || !grad_x || !aligned16(idx) || !aligned16(grad_y) ||
         !aligned16(grad_coef) || !aligned16(grad_x) || !aligned16(add_grad_coef) || !aligned16(add_grad_x))
         return DPB_EINVAL;
+    if (!aligned16(stats)) return DPB_EINVAL;
     return launched(dpb::launch_decode_bwd2(plan->dev, idx, grad_y, g_dtype == DPB_BF16, T, grad_coef, grad_x,
-                                           gx_dtype == DPB_BF16, (hipStream_t)stream, add_grad_coef, add_grad_x));
+                                           gx_dtype == DPB_BF16, (hipStream_t)stream, add_grad_coef, add_grad_x,
+                                           stats));
+}
+
+dpb_status dpb_encode_std(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T, const float* stats,
+                          int32_t* idx, float* coef, void* stream)
+{
+    dpb_status s = check_call(plan, T);
+    if (s) return s;
+    if (!dtype_ok(x_dtype)) return DPB_EINVAL;
+    if (!dpb::encode2_supported(plan->dev)) return DPB_EUNSUPPORTED;
+    if (T == 0) return DPB_OK;
+    if (!x || !idx || !coef || !stats || !aligned16(x) || !aligned16(idx) || !aligned16(coef) || !aligned16(stats))
+        return DPB_EINVAL;
+    return launched(dpb::launch_encode2(plan->dev, x, x_dtype == DPB_BF16, T, stats, idx, coef, (hipStream_t)stream));
+}
+
+dpb_status dpb_std_init(const dpb_plan* plan, float* stats, float* var, void* stream)
+{
+    dpb_status s = check_call(plan, 0);
+    if (s) return s;
+    if (!stats || !var || !aligned16(stats) || !aligned16(var)) return DPB_EINVAL;
+    return launched(dpb::launch_std_init(plan->dev, stats, var, (hipStream_t)stream));
+}
+
+size_t dpb_std_workspace_bytes(const dpb_plan* plan)
+{
+    return plan ? dpb::std_workspace_bytes(plan->dev) : 0;
+}
+
+dpb_status dpb_std_update(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T, const int32_t* idx,
+                          float momentum, float eps, float* stats, float* var, void* workspace, size_t ws_bytes,
+                          void* stream)
+{
+    dpb_status s = check_call(plan, T);
+    if (s) return s;
+    if (!dtype_ok(x_dtype) || !(momentum >= 0.f && momentum <= 1.f) || !(eps >= 0.f)) return DPB_EINVAL;
+    if (T == 0) return DPB_OK;
+    if (!x || !idx || !stats || !var || !workspace || !aligned16(x) || !aligned16(idx) || !aligned16(stats) ||
+        !aligned16(var) || !aligned16(workspace) || ws_bytes < dpb::std_workspace_bytes(plan->dev))
+        return DPB_EINVAL;
+    return launched(dpb::launch_std_update(plan->dev, x, x_dtype == DPB_BF16, T, idx, momentum, eps, stats, var,
+                                           workspace, (hipStream_t)stream));
 }
 
 dpb_status dpb_normalize(const dpb_plan* plan, const void* u, dpb_dtype u_dtype, const void* ref, dpb_dtype ref_dtype,

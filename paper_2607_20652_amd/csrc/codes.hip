@@ -549,7 +549,8 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
                                                                const void* __restrict__ g, int64_t T,
                                                                float* __restrict__ grad_coef,
                                                                void* grad_x, const float* __restrict__ add_gc,
-                                                               const void* add_gx)
+                                                               const void* add_gx,
+                                                               const float2* __restrict__ stats)
 {
     extern __shared__ __align__(16) unsigned char smem[];
     load_shared(P, smem);
@@ -613,6 +614,16 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
             wave_sync();
         }
         for (int i = lane; i < W.ntok * k; i += 64) grad_coef[t0 * k + i] = W.coef[i];
+        if (stats) {
+            // standardized coefficients z = (s - mu) r: dz/dx = r phi
+            wave_sync();
+            const int32_t nfeat_sh = P.level_bits[P.levels - 1];
+            for (int i = lane; i < W.ntok * k; i += 64) {
+                const int32_t c = W.idx[i];
+                if (c >= 0 && (c >> nfeat_sh) == 0) W.coef[i] *= stats[c].y;
+            }
+            wave_sync();
+        }
 
         // grad_x = decode(idx, grad_coef) (+ add_gx); the scoring buffers are dead now
         decode_tokens<!GX_BF16, NG, PB16>(P, W, W.coef);
@@ -702,6 +713,7 @@ hipError_t launch_decode2(const DevPlan& P, const int32_t* idx, const float* coe
 struct BwdExtra {
     const float* gc;
     const void* gx;
+    const float2* stats;
 };
 
 template <bool GB, bool XB, int NG, bool PB>
@@ -710,7 +722,7 @@ static void launch_bwd_v(const DevPlan& P, dim3 grid, size_t lds, hipStream_t st
 {
     allow_lds(decode_bwd2_kernel<GB, XB, NG, PB>, lds);
     hipLaunchKernelGGL((decode_bwd2_kernel<GB, XB, NG, PB>), grid, dim3(kThreads), lds, stream, P, idx, g, T, gc, gx,
-                       ex.gc, ex.gx);
+                       ex.gc, ex.gx, ex.stats);
 }
 
 template <bool GB, bool XB, bool PB>
@@ -736,12 +748,12 @@ static void launch_bwd_ub(const DevPlan& P, dim3 grid, size_t lds, hipStream_t s
 
 hipError_t launch_decode_bwd2(const DevPlan& P, const int32_t* idx, const void* g, bool g_bf16, int64_t T,
                               float* grad_coef, void* grad_x, bool gx_bf16, hipStream_t stream,
-                              const float* add_grad_coef, const void* add_grad_x)
+                              const float* add_grad_coef, const void* add_grad_x, const float* stats)
 {
     const size_t lds = code_lds_bytes(P, true, g_bf16);
     if (lds > (size_t)kLdsBudget) return hipErrorInvalidValue;
     const dim3 grid = code_grid(P, T, lds);
-    const BwdExtra ex{add_grad_coef, add_grad_x};
+    const BwdExtra ex{add_grad_coef, add_grad_x, (const float2*)stats};
     if (g_bf16 && gx_bf16) launch_bwd_ub<true, true>(P, grid, lds, stream, idx, g, T, grad_coef, grad_x, ex);
     else if (g_bf16) launch_bwd_ub<true, false>(P, grid, lds, stream, idx, g, T, grad_coef, grad_x, ex);
     else if (gx_bf16) launch_bwd_ub<false, true>(P, grid, lds, stream, idx, g, T, grad_coef, grad_x, ex);

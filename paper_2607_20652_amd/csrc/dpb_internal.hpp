@@ -173,11 +173,20 @@ hipError_t launch_decode2(const DevPlan& P, const int32_t* idx, const float* coe
                           bool y_bf16, hipStream_t stream);
 hipError_t launch_decode_bwd2(const DevPlan& P, const int32_t* idx, const void* g, bool g_bf16, int64_t T,
                               float* grad_coef, void* grad_x, bool gx_bf16, hipStream_t stream,
-                              const float* add_grad_coef = nullptr, const void* add_grad_x = nullptr);
+                              const float* add_grad_coef = nullptr, const void* add_grad_x = nullptr,
+                              const float* stats = nullptr);
 bool code_kernels_fit(const DevPlan& P);
 bool encode2_supported(const DevPlan& P);
-hipError_t launch_encode2(const DevPlan& P, const void* x, bool x_bf16, int64_t T, int32_t* idx, float* coef,
-                          hipStream_t stream);
+hipError_t launch_encode2(const DevPlan& P, const void* x, bool x_bf16, int64_t T, const float* stats, int32_t* idx,
+                          float* coef, hipStream_t stream);
+
+// EMA statistics of the score standardization (standardize.hip): tokens per
+// batch on which the candidate moments of levels >= 1 are taken.
+constexpr int kStdSample = 64;
+size_t std_workspace_bytes(const DevPlan& P);
+hipError_t launch_std_init(const DevPlan& P, float* stats, float* var, hipStream_t stream);
+hipError_t launch_std_update(const DevPlan& P, const void* x, bool x_bf16, int64_t T, const int32_t* idx,
+                             float beta, float eps, float* stats, float* var, void* ws, hipStream_t stream);
 
 // Row epilogues, code edits and the variance loss (extras.hip).
 hipError_t launch_normalize(int d, int64_t T, const void* u, bool u16, const void* ref, bool r16,

@@ -10,6 +10,10 @@
 //    largest lane maxima are distinct keys >= tau), so only the few keys >= tau
 //    are ranked exactly.  With bf16 activations a key is 32 bits: the bf16
 //    magnitude above the complemented coordinate.
+//  * With standardization statistics (mu, r = 1/sigma per feature, §2.2
+//    "Score Standardization") every score s becomes z = (s - mu) r before it
+//    is keyed: level 0 then uses 64-bit keys of fp32 z, and each child's
+//    (mu, r) is gathered from the statistics table.
 //  * Levels l >= 1: the children of every active parent are scored on the
 //    matrix cores (§2.2 child-scoring equation); the 64-bit keys (|s| desc,
 //    index asc, see device_common.hpp) are sorted by a bitonic network laid
@@ -294,8 +298,77 @@ __device__ void level0_f32(const DevPlan& P, int lane, int64_t t0, int ntok, con
     }
 }
 
+// Level 0 on standardized scores z = (x - mu) r (§2.2 "Score
+// Standardization"), in fp32: 64-bit keys over the coordinates, as level0_f32.
+// With bf16 activations lane li reads the interleaved dwords e = li + LPT m
+// (coordinates 32 (e >> 4) + (e & 15) and that + 16); coordinates past d
+// get key 0.
+template <int LPT, int LLP, bool X_BF16>
+__device__ void level0_std(const DevPlan& P, int lane, int64_t t0, int ntok, const uint32_t* pairs, const float* xf,
+                           const float2* __restrict__ stats, uint64_t* list, int listn, int* cnt, int32_t* par,
+                           int kmaxp, int32_t* out_idx, float* out_coef, int x32addr)
+{
+    const int tt = lane >> LLP, li = lane & (LPT - 1), K0 = P.active[0], d = P.d;
+    auto zkey = [&](float x, int iota) -> uint64_t {
+        if (iota >= d) return 0ull;
+        const float2 st = stats[iota];
+        return make_key((x - st.x) * st.y, (uint32_t)iota);
+    };
+    uint64_t best = 0;
+    if constexpr (X_BF16) {
+        const uint32_t* row = pairs + tt * P.prow;
+        for (int e = li; e < P.dp / 2; e += LPT) {
+            const uint32_t D = row[e];
+            const int lo = 32 * (e >> 4) + (e & 15);
+            best = max(best, max(zkey(bf16_bits_to_f32(D & 0xFFFFu), lo), zkey(bf16_bits_to_f32(D >> 16), lo + 16)));
+        }
+    } else {
+        const float* row = xf + tt * P.dp;
+        for (int iota = li; iota < d; iota += LPT) best = max(best, zkey(row[iota], iota));
+    }
+    uint64_t sv[1] = {best};
+    sort_desc<1, LLP, false>(sv, li, x32addr);
+    const uint64_t tau = shfl_u64(sv[0], (lane & ~(LPT - 1)) + K0 - 1);
+    if (li == 0) cnt[tt] = 0;
+    wave_sync();
+    uint64_t* lst = list + tt * listn;
+    if constexpr (X_BF16) {
+        const uint32_t* row = pairs + tt * P.prow;
+        for (int e = li; e < P.dp / 2; e += LPT) {
+            const uint32_t D = row[e];
+            const int lo = 32 * (e >> 4) + (e & 15);
+            const uint64_t klo = zkey(bf16_bits_to_f32(D & 0xFFFFu), lo), khi = zkey(bf16_bits_to_f32(D >> 16), lo + 16);
+            if (klo >= tau && klo != 0ull) lst[atomicAdd(&cnt[tt], 1)] = klo;
+            if (khi >= tau && khi != 0ull) lst[atomicAdd(&cnt[tt], 1)] = khi;
+        }
+    } else {
+        const float* row = xf + tt * P.dp;
+        for (int iota = li; iota < d; iota += LPT) {
+            const uint64_t kk = zkey(row[iota], iota);
+            if (kk >= tau) lst[atomicAdd(&cnt[tt], 1)] = kk;
+        }
+    }
+    wave_sync();
+    const int n = cnt[tt];
+    const bool live = tt < ntok;
+    for (int e = li; e < n; e += LPT) {
+        const uint64_t ke = lst[e];
+        int rank = 0;
+        for (int f = 0; f < n; ++f) rank += lst[f] > ke;
+        if (rank < K0) {
+            const uint32_t iota = key_index(ke);
+            par[tt * kmaxp + rank] = (int32_t)iota;
+            if (live) {
+                out_idx[(t0 + tt) * P.k_tot + rank] = (int32_t)iota;
+                out_coef[(t0 + tt) * P.k_tot + rank] = key_value(ke);
+            }
+        }
+    }
+}
+
 template <bool X_BF16, int CPT, int R>
 __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const void* __restrict__ xin, int64_t T,
+                                                              const float2* __restrict__ stats,
                                                               int32_t* __restrict__ out_idx,
                                                               float* __restrict__ out_coef)
 {
@@ -351,7 +424,10 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
         wave_sync();
 
         // ---- level 0
-        if constexpr (X_BF16)
+        if (stats)
+            level0_std<LPT, LLP, X_BF16>(P, lane, t0, ntok, pairs, xf, stats, list, EL.listn, cnt, par, EL.kmaxp,
+                                         out_idx, out_coef, x32);
+        else if constexpr (X_BF16)
             level0_bf16<LPT, LLP>(P, lane, t0, ntok, pairs, list, EL.listn, cnt, par, EL.kmaxp, out_idx,
                                   out_coef, x32);
         else
@@ -375,7 +451,14 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int j = 16 * mb + 4 * kq + i;
-                    keys[4 * mb + i] = (valid && j < Dl) ? make_key(acc[i] * P.rsd, (uint32_t)p ^ gens[j]) : 0ull;
+                    const bool ok = valid && j < Dl;
+                    const uint32_t c = ok ? (uint32_t)p ^ gens[j] : 0u;
+                    float sc = acc[i] * P.rsd;
+                    if (stats && ok) {
+                        const float2 st = stats[c];
+                        sc = (sc - st.x) * st.y;
+                    }
+                    keys[4 * mb + i] = ok ? make_key(sc, c) : 0ull;
                 }
             }
             sort_desc<R, NB, true>(keys, lanepos, x32);
@@ -399,9 +482,10 @@ bool encode2_supported(const DevPlan& P)
     return lds <= (size_t)kLdsBudget;
 }
 
-hipError_t launch_encode2(const DevPlan& P, const void* x, bool x_bf16, int64_t T, int32_t* idx, float* coef,
-                          hipStream_t stream)
+hipError_t launch_encode2(const DevPlan& P, const void* x, bool x_bf16, int64_t T, const float* stats, int32_t* idx,
+                          float* coef, hipStream_t stream)
 {
+    const float2* st = (const float2*)stats;
     const size_t lds = enc_shared_bytes(P) + (size_t)kEncWaves * enc_layout(P, x_bf16).bytes;
     const int64_t groups = (T + P.wave_tokens - 1) / P.wave_tokens;
     const int64_t need = (groups + kEncWaves - 1) / kEncWaves;
@@ -415,7 +499,8 @@ hipError_t launch_encode2(const DevPlan& P, const void* x, bool x_bf16, int64_t 
 #define DPB_ENC(XB, CV, RV)                                                                                       \
     do {                                                                                                          \
         allow_lds(encode3_kernel<XB, CV, RV>, lds);                                                               \
-        hipLaunchKernelGGL((encode3_kernel<XB, CV, RV>), grid, dim3(kEncThreads), lds, stream, P, x, T, idx, coef); \
+        hipLaunchKernelGGL((encode3_kernel<XB, CV, RV>), grid, dim3(kEncThreads), lds, stream, P, x, T, st, idx,    \
+                           coef);                                                                                 \
     } while (0)
 #define DPB_ENC_R(XB, CV)                    \
     do {                                     \

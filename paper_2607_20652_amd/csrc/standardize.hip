@@ -1,0 +1,254 @@
+// EMA statistics of the score standardization (§2.2 "Score
+// Standardization") for gfx950.
+//
+// State, owned by the caller: stats[N] = (mu, r = 1/sigma) as float2, read by
+// the encoder, and var[N] (the EMA of the variance).  After a batch encoded
+// with the state, the moments of each feature over the tokens where it was a
+// candidate update it:
+//  * level 0: a basis feature is a candidate at every token, so its sample is
+//    a column of x over the whole batch -- per-workgroup fp64 column sums over
+//    a fixed token range, folded in a fixed order;
+//  * levels l >= 1: on kStdSample evenly spaced tokens, the children
+//    p XOR g_j of the active parents (the level l-1 entries of the token's
+//    code), each child once per token, scored from the definition
+//    <phi_c, x>; one record per (token, child).  Records of one feature are
+//    combined with fp64 atomics in a per-feature accumulator that only the
+//    records themselves clear, and the record with the lowest position
+//    applies the update.
+// Update of a feature with n samples, mean m1, population variance v:
+//    mu <- (1 - beta) mu + beta m1,  var <- (1 - beta) var + beta v,
+//    r = 1 / sqrt(var + eps).
+#include <algorithm>
+
+#include "dpb_internal.hpp"
+#include "device_common.hpp"
+
+namespace dpb {
+namespace {
+
+constexpr int kStdGroups = 256;     // workgroups of the level-0 column pass
+constexpr int kStdThreads = 256;
+
+struct StdAcc {
+    uint32_t n;
+    uint32_t owner;
+    double s1;
+    double s2;
+};
+
+struct StdRec {
+    int32_t feat;      // -1: none (duplicate child or missing parent)
+    float s;
+};
+
+struct StdWs {
+    double* col;       // [kStdGroups][d][2] fp64 column sums of x and x^2
+    StdRec* rec;       // [kStdSample][cands]
+    StdAcc* acc;       // [N]
+};
+
+__host__ __device__ inline size_t std_align(size_t v) { return (v + 255) & ~(size_t)255; }
+
+__host__ __device__ inline int std_cands(const DevPlan& P)
+{
+    int c = 0;
+    for (int l = 1; l < P.levels; ++l) c += P.active[l - 1] * P.delta[l];
+    return c;
+}
+
+__host__ __device__ inline StdWs std_ws(void* ws, const DevPlan& P, size_t* total)
+{
+    unsigned char* b = (unsigned char*)ws;
+    const int64_t N = (int64_t)1 << P.level_bits[P.levels - 1];
+    const size_t o1 = std_align((size_t)kStdGroups * P.d * 16);
+    const size_t o2 = o1 + std_align((size_t)kStdSample * std_cands(P) * sizeof(StdRec));
+    const size_t o3 = o2 + std_align((size_t)N * sizeof(StdAcc));
+    if (total) *total = o3;
+    StdWs W{};
+    if (!ws) return W;
+    W.col = (double*)b;
+    W.rec = (StdRec*)(b + o1);
+    W.acc = (StdAcc*)(b + o2);
+    return W;
+}
+
+__device__ __forceinline__ void ema(float2* stats, float* var, int64_t c, double n, double s1, double s2, float beta,
+                                    float eps)
+{
+    const double m1 = s1 / n;
+    const double v = fmax(s2 / n - m1 * m1, 0.0);
+    const float mu = (1.f - beta) * stats[c].x + beta * (float)m1;
+    const float vv = (1.f - beta) * var[c] + beta * (float)v;
+    var[c] = vv;
+    stats[c] = make_float2(mu, 1.f / sqrtf(vv + eps));
+}
+
+__global__ void std_init_kernel(float2* stats, float* var, int64_t N)
+{
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N; i += (int64_t)gridDim.x * blockDim.x) {
+        stats[i] = make_float2(0.f, 1.f);
+        var[i] = 1.f;
+    }
+}
+
+// Column sums of x and x^2 over the tokens [T g / G, T (g + 1) / G) of
+// workgroup g = blockIdx.x; blockIdx.y picks 256 columns, one per thread;
+// eight rows are loaded per round.
+template <bool BF16>
+__global__ __launch_bounds__(kStdThreads) void std_col_kernel(const void* x, int d, int64_t T, StdWs W)
+{
+    const int c = blockIdx.y * kStdThreads + threadIdx.x;
+    if (c >= d) return;
+    const int64_t t0 = T * blockIdx.x / kStdGroups, t1 = T * (blockIdx.x + 1) / kStdGroups;
+    double s1 = 0.0, s2 = 0.0;
+    for (int64_t t = t0; t < t1; t += 8) {
+        float v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = t + e < t1 ? load_act<BF16>(x, (t + e) * d + c) : 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            s1 += (double)v[e];
+            s2 += (double)v[e] * (double)v[e];
+        }
+    }
+    double* o = W.col + ((int64_t)blockIdx.x * d + c) * 2;
+    o[0] = s1;
+    o[1] = s2;
+}
+
+__global__ void std_col_update_kernel(int d, int64_t T, StdWs W, float2* stats, float* var, float beta, float eps)
+{
+    const int c = blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= d || T <= 0) return;
+    double s1 = 0.0, s2 = 0.0;
+    for (int g = 0; g < kStdGroups; ++g) {
+        s1 += W.col[((int64_t)g * d + c) * 2];
+        s2 += W.col[((int64_t)g * d + c) * 2 + 1];
+    }
+    ema(stats, var, c, (double)T, s1, s2, beta, eps);
+}
+
+// One workgroup per (sample token, level l >= 1): the token's candidates at
+// level l, each child once, scored <phi_c, x_t> from the definition (one
+// wave per child, lanes over the coordinates).
+template <bool BF16>
+__global__ __launch_bounds__(kStdThreads) void std_sample_kernel(DevPlan P, const void* x, int64_t T, int m,
+                                                                 const int32_t* idx, StdWs W)
+{
+    const int j = blockIdx.x, l = blockIdx.y + 1;
+    const int64_t t = ((int64_t)j * T) / m;
+    const int Kp = P.active[l - 1], Dl = P.delta[l], d = P.d;
+    const int32_t* par = idx + t * P.k_tot + P.slot_base[l - 1];
+    const uint32_t* g = P.gens + P.gens_off[l];
+    int cbase = 0;
+    for (int ll = 1; ll < l; ++ll) cbase += P.active[ll - 1] * P.delta[ll];
+    StdRec* rec = W.rec + (int64_t)j * std_cands(P) + cbase;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    for (int e = wave; e < Kp * Dl; e += kStdThreads / 64) {
+        const int q = e / Dl, jj = e - q * Dl;
+        const int32_t p = par[q];
+        int32_t feat = -1;
+        if (p >= 0) {
+            const uint32_t c = (uint32_t)p ^ g[jj];
+            // a child reached from an earlier parent slot is that slot's record
+            bool dup = false;
+            for (int q2 = 0; q2 < q && !dup; ++q2) {
+                const int32_t p2 = par[q2];
+                if (p2 < 0) continue;
+                for (int j2 = 0; j2 < Dl; ++j2)
+                    if (((uint32_t)p2 ^ g[j2]) == c) {
+                        dup = true;
+                        break;
+                    }
+            }
+            if (!dup) feat = (int32_t)c;
+        }
+        float s = 0.f;
+        if (feat >= 0) {
+            float part = 0.f;
+            for (int iota = lane; iota < d; iota += 64)
+                part += signed_by_parity(load_act<BF16>(x, t * d + iota), P.masks[iota] & (uint32_t)feat);
+            s = wave_sum(part) * P.rsd;
+        }
+        if (lane == 0) rec[e] = StdRec{feat, s};
+    }
+}
+
+__global__ void std_rec_clear_kernel(int64_t nrec, StdWs W)
+{
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nrec; i += (int64_t)gridDim.x * blockDim.x) {
+        const StdRec r = W.rec[i];
+        if (r.feat >= 0) W.acc[r.feat] = StdAcc{0u, 0xFFFFFFFFu, 0.0, 0.0};
+    }
+}
+
+__global__ void std_rec_accum_kernel(int64_t nrec, StdWs W)
+{
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nrec; i += (int64_t)gridDim.x * blockDim.x) {
+        const StdRec r = W.rec[i];
+        if (r.feat < 0) continue;
+        StdAcc* a = W.acc + r.feat;
+        atomicAdd(&a->n, 1u);
+        atomicAdd(&a->s1, (double)r.s);
+        atomicAdd(&a->s2, (double)r.s * (double)r.s);
+        atomicMin(&a->owner, (uint32_t)i);
+    }
+}
+
+__global__ void std_rec_update_kernel(int64_t nrec, StdWs W, float2* stats, float* var, float beta, float eps)
+{
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nrec; i += (int64_t)gridDim.x * blockDim.x) {
+        const StdRec r = W.rec[i];
+        if (r.feat < 0) continue;
+        const StdAcc a = W.acc[r.feat];
+        if (a.owner == (uint32_t)i) ema(stats, var, r.feat, (double)a.n, a.s1, a.s2, beta, eps);
+    }
+}
+
+dim3 std_grid(int64_t n, int threads)
+{
+    const int64_t need = (n + threads - 1) / threads;
+    return dim3((unsigned)std::max<int64_t>(1, std::min<int64_t>(need, 4096)));
+}
+
+}  // namespace
+
+size_t std_workspace_bytes(const DevPlan& P)
+{
+    size_t total = 0;
+    (void)std_ws(nullptr, P, &total);
+    return total;
+}
+
+hipError_t launch_std_init(const DevPlan& P, float* stats, float* var, hipStream_t stream)
+{
+    const int64_t N = (int64_t)1 << P.level_bits[P.levels - 1];
+    hipLaunchKernelGGL(std_init_kernel, std_grid(N, 256), dim3(256), 0, stream, (float2*)stats, var, N);
+    return hipGetLastError();
+}
+
+hipError_t launch_std_update(const DevPlan& P, const void* x, bool x_bf16, int64_t T, const int32_t* idx,
+                             float beta, float eps, float* stats, float* var, void* ws, hipStream_t stream)
+{
+    const StdWs W = std_ws(ws, P, nullptr);
+    float2* st = (float2*)stats;
+    const dim3 gc(kStdGroups, (P.d + kStdThreads - 1) / kStdThreads);
+    if (x_bf16) hipLaunchKernelGGL(std_col_kernel<true>, gc, dim3(kStdThreads), 0, stream, x, P.d, T, W);
+    else hipLaunchKernelGGL(std_col_kernel<false>, gc, dim3(kStdThreads), 0, stream, x, P.d, T, W);
+    hipLaunchKernelGGL(std_col_update_kernel, dim3((P.d + 255) / 256), dim3(256), 0, stream, P.d, T, W, st, var, beta,
+                       eps);
+    const int m = (int)std::min<int64_t>(T, kStdSample);
+    if (P.levels > 1 && m > 0) {
+        const dim3 g2(m, P.levels - 1);
+        if (x_bf16) hipLaunchKernelGGL(std_sample_kernel<true>, g2, dim3(kStdThreads), 0, stream, P, x, T, m, idx, W);
+        else hipLaunchKernelGGL(std_sample_kernel<false>, g2, dim3(kStdThreads), 0, stream, P, x, T, m, idx, W);
+        const int64_t nrec = (int64_t)m * std_cands(P);
+        hipLaunchKernelGGL(std_rec_clear_kernel, std_grid(nrec, 256), dim3(256), 0, stream, nrec, W);
+        hipLaunchKernelGGL(std_rec_accum_kernel, std_grid(nrec, 256), dim3(256), 0, stream, nrec, W);
+        hipLaunchKernelGGL(std_rec_update_kernel, std_grid(nrec, 256), dim3(256), 0, stream, nrec, W, st, var, beta,
+                           eps);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace dpb

@@ -87,7 +87,11 @@ def test_compute_calls_reject_null_plan(lib):
     assert lib.dpb_encode(None, P(16), 0, 4, P(16), P(16), None) == -1
     assert lib.dpb_decode(None, P(16), P(16), 4, P(16), 0, None) == -1
     assert lib.dpb_decode_bwd(None, P(16), P(16), 0, 4, P(16), P(16), 0, None) == -1
-    assert lib.dpb_decode_bwd_ex(None, P(16), P(16), 0, 4, None, None, P(16), P(16), 0, None) == -1
+    assert lib.dpb_decode_bwd_ex(None, P(16), P(16), 0, 4, None, None, None, P(16), P(16), 0, None) == -1
+    assert lib.dpb_encode_std(None, P(16), 0, 4, P(16), P(16), P(16), None) == -1
+    assert lib.dpb_std_init(None, P(16), P(16), None) == -1
+    assert lib.dpb_std_update(None, P(16), 0, 4, P(16), 0.1, 1e-6, P(16), P(16), P(16), 1 << 20, None) == -1
+    assert lib.dpb_std_workspace_bytes(None) == 0
     assert lib.dpb_normalize(None, P(16), 0, P(16), 0, None, 4, 4, P(16), 0, None, None) == -1
     assert lib.dpb_normalize_bwd(None, P(16), 0, P(16), 0, P(16), 0, 4, P(32), 0, P(48), 0, 0, None) == -1
     assert lib.dpb_edit_codes(None, P(16), P(16), None, None, 4, P(16), P(32), P(48), 2, P(64), P(80), None) == -1

@@ -68,6 +68,38 @@ def test_layer_backward_equals_autograd_of_explicit_layer(normalized, gloss, n_m
     assert np.allclose(gx, xt.grad.numpy(), rtol=1e-10, atol=1e-11)
 
 
+def test_standardized_layer_backward_equals_autograd():
+    """With standardized coefficients coef = (Phi_S x - mu) r the gradient to
+    x carries r on every slot."""
+    w = inputs.workload("tiny")
+    nb, dl, K = oracle.hierarchy(w.d, w.n, w.levels, w.branching, w.beam, w.k)
+    m, gens = oracle.masks(w.d, w.n), oracle.generators(nb, dl, 0)
+    N = 1 << w.n
+    rng = np.random.default_rng(4)
+    mu = (0.3 * rng.standard_normal(N)).astype(np.float32)
+    r = rng.uniform(0.5, 2.0, N).astype(np.float32)
+    T = 20
+    x = inputs.activations("tiny", T).double().numpy()
+    gy = inputs.upstream_grad("tiny", T).double().numpy()
+    idx, coef, _, _ = oracle.encode_std(w.d, m, nb, K, dl, gens, x, mu, r)
+    Phi = _phi_stack(w.d, m, idx)
+    live = torch.tensor(idx >= 0)
+    mus = torch.tensor(np.where(idx >= 0, mu[np.maximum(idx, 0)], 0.0).astype(np.float64))
+    rs = np.where(idx >= 0, r[np.maximum(idx, 0)], 0.0).astype(np.float64)
+    xt = torch.tensor(x, requires_grad=True)
+    c = torch.where(live, (torch.einsum("tkd,td->tk", Phi, xt) - mus) * torch.tensor(rs), torch.zeros(()))
+    c.retain_grad()
+    u = torch.einsum("tkd,tk->td", Phi, c)
+    y = u * (xt.norm(dim=1, keepdim=True) / u.norm(dim=1, keepdim=True))
+    L = (torch.tensor(gy) * y).sum() + 0.8 * _torch_var_loss(idx, c, 2)
+    L.backward()
+    # level-0 coefficients are fp32 on the encoder side; the layer's are fp64
+    assert np.allclose(c.detach().numpy(), coef, rtol=1e-6, atol=1e-6)
+    gc, gx = oracle.layer_backward(w.d, m, idx, c.detach().numpy(), x, gy, 0.8, 2, True, r_slot=rs)
+    assert np.allclose(gc, c.grad.numpy(), rtol=1e-10, atol=1e-11)
+    assert np.allclose(gx, xt.grad.numpy(), rtol=1e-10, atol=1e-11)
+
+
 def test_layer_forward_pieces_agree_with_explicit_layer():
     """decode + normalize of the encoder's code equals the explicit layer."""
     w = inputs.workload("tiny")
