@@ -547,7 +547,7 @@ dpb_status dpb_encode_std(const dpb_plan* plan, const void* x, dpb_dtype x_dtype
     dpb_status s = check_call(plan, T);
     if (s) return s;
     if (!dtype_ok(x_dtype)) return DPB_EINVAL;
-    if (!dpb::encode2_supported(plan->dev)) return DPB_EUNSUPPORTED;
+    if (!dpb::encode2_std_supported(plan->dev)) return DPB_EUNSUPPORTED;
     if (T == 0) return DPB_OK;
     if (!x || !idx || !coef || !stats || !aligned16(x) || !aligned16(idx) || !aligned16(coef) || !aligned16(stats))
         return DPB_EINVAL;
@@ -574,6 +574,7 @@ dpb_status dpb_std_update(const dpb_plan* plan, const void* x, dpb_dtype x_dtype
     dpb_status s = check_call(plan, T);
     if (s) return s;
     if (!dtype_ok(x_dtype) || !(momentum >= 0.f && momentum <= 1.f) || !(eps >= 0.f)) return DPB_EINVAL;
+    if (!dpb::std_supported(plan->dev)) return DPB_EUNSUPPORTED;
     if (T == 0) return DPB_OK;
     if (!x || !idx || !stats || !var || !workspace || !aligned16(x) || !aligned16(idx) || !aligned16(stats) ||
         !aligned16(var) || !aligned16(workspace) || ws_bytes < dpb::std_workspace_bytes(plan->dev))

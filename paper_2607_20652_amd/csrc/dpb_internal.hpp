@@ -177,6 +177,7 @@ hipError_t launch_decode_bwd2(const DevPlan& P, const int32_t* idx, const void* 
                               const float* stats = nullptr);
 bool code_kernels_fit(const DevPlan& P);
 bool encode2_supported(const DevPlan& P);
+bool encode2_std_supported(const DevPlan& P);
 hipError_t launch_encode2(const DevPlan& P, const void* x, bool x_bf16, int64_t T, const float* stats, int32_t* idx,
                           float* coef, hipStream_t stream);
 
@@ -184,6 +185,7 @@ hipError_t launch_encode2(const DevPlan& P, const void* x, bool x_bf16, int64_t 
 // batch on which the candidate moments of levels >= 1 are taken.
 constexpr int kStdSample = 64;
 size_t std_workspace_bytes(const DevPlan& P);
+bool std_supported(const DevPlan& P);
 hipError_t launch_std_init(const DevPlan& P, float* stats, float* var, hipStream_t stream);
 hipError_t launch_std_update(const DevPlan& P, const void* x, bool x_bf16, int64_t T, const int32_t* idx,
                              float beta, float eps, float* stats, float* var, void* ws, hipStream_t stream);

@@ -72,10 +72,11 @@ __host__ __device__ inline EncLayout enc_layout(const DevPlan& P, bool act_bf16)
     return L;
 }
 
-// Shared LDS of an encoder workgroup: nibble tables and generators.
-__host__ __device__ inline unsigned enc_shared_bytes(const DevPlan& P)
+// Shared LDS of an encoder workgroup: nibble tables, generators and, with
+// standardization, the level-0 statistics.
+__host__ __device__ inline unsigned enc_shared_bytes(const DevPlan& P, bool std)
 {
-    return align16u(P.nt_groups * 16 * P.nchunk * 4) + align16u(P.gens_total * 4);
+    return align16u(P.nt_groups * 16 * P.nchunk * 4) + align16u(P.gens_total * 4) + (std ? align16u(P.d * 8) : 0u);
 }
 
 // Exchange with the lane whose index differs by m (a power of two): DPP for
@@ -299,19 +300,19 @@ __device__ void level0_f32(const DevPlan& P, int lane, int64_t t0, int ntok, con
 }
 
 // Level 0 on standardized scores z = (x - mu) r (§2.2 "Score
-// Standardization"), in fp32: 64-bit keys over the coordinates, as level0_f32.
-// With bf16 activations lane li reads the interleaved dwords e = li + LPT m
-// (coordinates 32 (e >> 4) + (e & 15) and that + 16); coordinates past d
-// get key 0.
+// Standardization"), in fp32: 64-bit keys over the coordinates, as level0_f32,
+// with the level-0 statistics staged in LDS (st0).  With bf16 activations lane
+// li reads the interleaved dwords e = li + LPT m (coordinates 32 (e >> 4) +
+// (e & 15) and that + 16); coordinates past d get key 0.
 template <int LPT, int LLP, bool X_BF16>
 __device__ void level0_std(const DevPlan& P, int lane, int64_t t0, int ntok, const uint32_t* pairs, const float* xf,
-                           const float2* __restrict__ stats, uint64_t* list, int listn, int* cnt, int32_t* par,
-                           int kmaxp, int32_t* out_idx, float* out_coef, int x32addr)
+                           const float2* st0, uint64_t* list, int listn, int* cnt, int32_t* par, int kmaxp,
+                           int32_t* out_idx, float* out_coef, int x32addr)
 {
     const int tt = lane >> LLP, li = lane & (LPT - 1), K0 = P.active[0], d = P.d;
     auto zkey = [&](float x, int iota) -> uint64_t {
         if (iota >= d) return 0ull;
-        const float2 st = stats[iota];
+        const float2 st = st0[iota];
         return make_key((x - st.x) * st.y, (uint32_t)iota);
     };
     uint64_t best = 0;
@@ -366,7 +367,7 @@ __device__ void level0_std(const DevPlan& P, int lane, int64_t t0, int ntok, con
     }
 }
 
-template <bool X_BF16, int CPT, int R>
+template <bool X_BF16, int CPT, int R, bool STD>
 __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const void* __restrict__ xin, int64_t T,
                                                               const float2* __restrict__ stats,
                                                               int32_t* __restrict__ out_idx,
@@ -379,15 +380,18 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
     extern __shared__ __align__(16) unsigned char smem[];
     uint32_t* s_nt = (uint32_t*)smem;
     uint32_t* s_gens = (uint32_t*)(smem + align16u(P.nt_groups * 16 * P.nchunk * 4));
+    float2* s_st0 = (float2*)(smem + enc_shared_bytes(P, false));   // level-0 statistics (STD)
     for (int i = threadIdx.x; i < P.nt_groups * 16 * P.nchunk; i += kEncThreads) s_nt[i] = P.nt[i];
     for (int i = threadIdx.x; i < P.gens_total; i += kEncThreads) s_gens[i] = P.gens[i];
+    if constexpr (STD)
+        for (int i = threadIdx.x; i < P.d; i += kEncThreads) s_st0[i] = stats[i];
     __syncthreads();
 
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int d = P.d, dp = P.dp;
     const int x32 = (lane ^ 32) << 2;
     const EncLayout EL = enc_layout(P, X_BF16);
-    unsigned char* wb = smem + enc_shared_bytes(P) + (unsigned)wave * EL.bytes;
+    unsigned char* wb = smem + enc_shared_bytes(P, STD) + (unsigned)wave * EL.bytes;
     uint32_t* pairs = (uint32_t*)(wb + EL.act);
     float* xf = (float*)(wb + EL.act);
     uint32_t* cw = (uint32_t*)(wb + EL.cw);
@@ -424,8 +428,8 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
         wave_sync();
 
         // ---- level 0
-        if (stats)
-            level0_std<LPT, LLP, X_BF16>(P, lane, t0, ntok, pairs, xf, stats, list, EL.listn, cnt, par, EL.kmaxp,
+        if constexpr (STD)
+            level0_std<LPT, LLP, X_BF16>(P, lane, t0, ntok, pairs, xf, s_st0, list, EL.listn, cnt, par, EL.kmaxp,
                                          out_idx, out_coef, x32);
         else if constexpr (X_BF16)
             level0_bf16<LPT, LLP>(P, lane, t0, ntok, pairs, list, EL.listn, cnt, par, EL.kmaxp, out_idx,
@@ -443,6 +447,16 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
             const bool valid = p >= 0;
             const int trow = valid ? ct : 0;
             const uint32_t* gens = s_gens + P.gens_off[l];
+            // standardization statistics of this lane's children, requested
+            // before the scoring so that the gathers overlap it
+            float2 stv[R];
+            if constexpr (STD) {
+#pragma unroll
+                for (int e = 0; e < R; ++e) {
+                    const int j = 16 * (e >> 2) + 4 * kq + (e & 3);
+                    stv[e] = (valid && j < Dl) ? stats[(uint32_t)p ^ gens[j]] : make_float2(0.f, 1.f);
+                }
+            }
             uint64_t keys[R];
 #pragma unroll
             for (int mb = 0; mb < R / 4; ++mb) {
@@ -454,10 +468,7 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
                     const bool ok = valid && j < Dl;
                     const uint32_t c = ok ? (uint32_t)p ^ gens[j] : 0u;
                     float sc = acc[i] * P.rsd;
-                    if (stats && ok) {
-                        const float2 st = stats[c];
-                        sc = (sc - st.x) * st.y;
-                    }
+                    if constexpr (STD) sc = (sc - stv[4 * mb + i].x) * stv[4 * mb + i].y;
                     keys[4 * mb + i] = ok ? make_key(sc, c) : 0ull;
                 }
             }
@@ -471,6 +482,13 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
 
 }  // namespace
 
+// Whether the standardized encoder's workgroup fits the LDS budget.
+bool encode2_std_supported(const DevPlan& P)
+{
+    const size_t lds = enc_shared_bytes(P, true) + (size_t)kEncWaves * enc_layout(P, false).bytes;
+    return encode2_supported(P) && lds <= (size_t)kLdsBudget;
+}
+
 bool encode2_supported(const DevPlan& P)
 {
     const int TPW = P.wave_tokens, LPT = 64 / TPW;
@@ -478,7 +496,7 @@ bool encode2_supported(const DevPlan& P)
     for (int l = 1; l < P.levels; ++l)
         if (P.cpt[l] > 16 || TPW * P.cpt[l] > 16) return false;
     if (16 / TPW != 4 && 16 / TPW != 8 && 16 / TPW != 16) return false;
-    const size_t lds = enc_shared_bytes(P) + (size_t)kEncWaves * enc_layout(P, false).bytes;
+    const size_t lds = enc_shared_bytes(P, false) + (size_t)kEncWaves * enc_layout(P, false).bytes;
     return lds <= (size_t)kLdsBudget;
 }
 
@@ -486,7 +504,7 @@ hipError_t launch_encode2(const DevPlan& P, const void* x, bool x_bf16, int64_t 
                           float* coef, hipStream_t stream)
 {
     const float2* st = (const float2*)stats;
-    const size_t lds = enc_shared_bytes(P) + (size_t)kEncWaves * enc_layout(P, x_bf16).bytes;
+    const size_t lds = enc_shared_bytes(P, stats != nullptr) + (size_t)kEncWaves * enc_layout(P, x_bf16).bytes;
     const int64_t groups = (T + P.wave_tokens - 1) / P.wave_tokens;
     const int64_t need = (groups + kEncWaves - 1) / kEncWaves;
     int cus = 256, dev = 0;
@@ -496,11 +514,17 @@ hipError_t launch_encode2(const DevPlan& P, const void* x, bool x_bf16, int64_t 
     const int per_cu = (int)std::max<size_t>(1, (160 * 1024) / std::max<size_t>(lds, 1));
     const dim3 grid((unsigned)std::max<int64_t>(1, std::min<int64_t>(need, (int64_t)cus * std::min(per_cu, 8) * 4)));
     const int R = enc_r(P), CPT = 16 / P.wave_tokens;
-#define DPB_ENC(XB, CV, RV)                                                                                       \
-    do {                                                                                                          \
-        allow_lds(encode3_kernel<XB, CV, RV>, lds);                                                               \
-        hipLaunchKernelGGL((encode3_kernel<XB, CV, RV>), grid, dim3(kEncThreads), lds, stream, P, x, T, st, idx,    \
-                           coef);                                                                                 \
+#define DPB_ENC(XB, CV, RV)                                                                                        \
+    do {                                                                                                           \
+        if (st) {                                                                                                  \
+            allow_lds(encode3_kernel<XB, CV, RV, true>, lds);                                                      \
+            hipLaunchKernelGGL((encode3_kernel<XB, CV, RV, true>), grid, dim3(kEncThreads), lds, stream, P, x, T,  \
+                               st, idx, coef);                                                                     \
+        } else {                                                                                                   \
+            allow_lds(encode3_kernel<XB, CV, RV, false>, lds);                                                     \
+            hipLaunchKernelGGL((encode3_kernel<XB, CV, RV, false>), grid, dim3(kEncThreads), lds, stream, P, x, T, \
+                               st, idx, coef);                                                                     \
+        }                                                                                                          \
     } while (0)
 #define DPB_ENC_R(XB, CV)                    \
     do {                                     \

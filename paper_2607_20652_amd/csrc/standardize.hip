@@ -92,28 +92,53 @@ __global__ void std_init_kernel(float2* stats, float* var, int64_t N)
 }
 
 // Column sums of x and x^2 over the tokens [T g / G, T (g + 1) / G) of
-// workgroup g = blockIdx.x; blockIdx.y picks 256 columns, one per thread;
-// eight rows are loaded per round.
+// workgroup g = blockIdx.x; each thread takes 4 consecutive columns of a
+// 1024-column strip (blockIdx.y), eight rows per round.
 template <bool BF16>
 __global__ __launch_bounds__(kStdThreads) void std_col_kernel(const void* x, int d, int64_t T, StdWs W)
 {
-    const int c = blockIdx.y * kStdThreads + threadIdx.x;
-    if (c >= d) return;
+    const int c0 = blockIdx.y * 4 * kStdThreads + 4 * threadIdx.x;
+    if (c0 >= d) return;
     const int64_t t0 = T * blockIdx.x / kStdGroups, t1 = T * (blockIdx.x + 1) / kStdGroups;
-    double s1 = 0.0, s2 = 0.0;
+    const bool vec = (d & 3) == 0;
+    double s1[4] = {0.0, 0.0, 0.0, 0.0}, s2[4] = {0.0, 0.0, 0.0, 0.0};
     for (int64_t t = t0; t < t1; t += 8) {
-        float v[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = t + e < t1 ? load_act<BF16>(x, (t + e) * d + c) : 0.f;
+        float v[8][4];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-            s1 += (double)v[e];
-            s2 += (double)v[e] * (double)v[e];
+            const int64_t i = (t + e) * d + c0;
+            if (t + e >= t1) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) v[e][q] = 0.f;
+            } else if (vec && BF16) {
+                const uint2 u = *(const uint2*)((const uint16_t*)x + i);
+                v[e][0] = bf16_bits_to_f32(u.x & 0xFFFFu);
+                v[e][1] = bf16_bits_to_f32(u.x >> 16);
+                v[e][2] = bf16_bits_to_f32(u.y & 0xFFFFu);
+                v[e][3] = bf16_bits_to_f32(u.y >> 16);
+            } else if (vec) {
+                const float4 f = *(const float4*)((const float*)x + i);
+                v[e][0] = f.x; v[e][1] = f.y; v[e][2] = f.z; v[e][3] = f.w;
+            } else {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) v[e][q] = c0 + q < d ? load_act<BF16>(x, i + q) : 0.f;
+            }
         }
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                s1[q] += (double)v[e][q];
+                s2[q] += (double)v[e][q] * (double)v[e][q];
+            }
     }
-    double* o = W.col + ((int64_t)blockIdx.x * d + c) * 2;
-    o[0] = s1;
-    o[1] = s2;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+        if (c0 + q < d) {
+            double* o = W.col + ((int64_t)blockIdx.x * d + c0 + q) * 2;
+            o[0] = s1[q];
+            o[1] = s2[q];
+        }
 }
 
 __global__ void std_col_update_kernel(int d, int64_t T, StdWs W, float2* stats, float* var, float beta, float eps)
@@ -129,48 +154,65 @@ __global__ void std_col_update_kernel(int d, int64_t T, StdWs W, float2* stats, 
 }
 
 // One workgroup per (sample token, level l >= 1): the token's candidates at
-// level l, each child once, scored <phi_c, x_t> from the definition (one
-// wave per child, lanes over the coordinates).
+// level l, each child once, scored <phi_c, x_t> from the definition.  The
+// candidate list and the row of x are staged in LDS; a candidate is a
+// duplicate when an earlier entry of the list holds the same child; each
+// wave scores one candidate at a time, lanes over the coordinates.
+constexpr int kStdMaxCand = 4096;
+
 template <bool BF16>
 __global__ __launch_bounds__(kStdThreads) void std_sample_kernel(DevPlan P, const void* x, int64_t T, int m,
                                                                  const int32_t* idx, StdWs W)
 {
+    __shared__ int32_t cand[kStdMaxCand];
+    extern __shared__ __align__(16) float xrow[];
     const int j = blockIdx.x, l = blockIdx.y + 1;
     const int64_t t = ((int64_t)j * T) / m;
-    const int Kp = P.active[l - 1], Dl = P.delta[l], d = P.d;
+    const int Kp = P.active[l - 1], Dl = P.delta[l], d = P.d, n = Kp * Dl;
     const int32_t* par = idx + t * P.k_tot + P.slot_base[l - 1];
     const uint32_t* g = P.gens + P.gens_off[l];
     int cbase = 0;
     for (int ll = 1; ll < l; ++ll) cbase += P.active[ll - 1] * P.delta[ll];
     StdRec* rec = W.rec + (int64_t)j * std_cands(P) + cbase;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    for (int e = wave; e < Kp * Dl; e += kStdThreads / 64) {
-        const int q = e / Dl, jj = e - q * Dl;
+    for (int e = threadIdx.x; e < n; e += kStdThreads) {
+        const int q = e / Dl;
         const int32_t p = par[q];
-        int32_t feat = -1;
-        if (p >= 0) {
-            const uint32_t c = (uint32_t)p ^ g[jj];
-            // a child reached from an earlier parent slot is that slot's record
-            bool dup = false;
-            for (int q2 = 0; q2 < q && !dup; ++q2) {
-                const int32_t p2 = par[q2];
-                if (p2 < 0) continue;
-                for (int j2 = 0; j2 < Dl; ++j2)
-                    if (((uint32_t)p2 ^ g[j2]) == c) {
-                        dup = true;
-                        break;
-                    }
-            }
-            if (!dup) feat = (int32_t)c;
-        }
+        cand[e] = p >= 0 ? (int32_t)((uint32_t)p ^ g[e - q * Dl]) : -1;
+    }
+    for (int iota = threadIdx.x; iota < d; iota += kStdThreads) xrow[iota] = load_act<BF16>(x, t * d + iota);
+    __syncthreads();
+    // a later copy of a child is marked (no later write to cand before the next barrier)
+    int32_t mine[kStdMaxCand / kStdThreads];
+#pragma unroll
+    for (int r = 0; r < kStdMaxCand / kStdThreads; ++r) {
+        const int e = threadIdx.x + r * kStdThreads;
+        int32_t c = e < n ? cand[e] : -1;
+        if (c >= 0)
+            for (int e2 = 0; e2 < e; ++e2)
+                if (cand[e2] == c) {
+                    c = -1;
+                    break;
+                }
+        mine[r] = c;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kStdMaxCand / kStdThreads; ++r) {
+        const int e = threadIdx.x + r * kStdThreads;
+        if (e < n) cand[e] = mine[r];
+    }
+    __syncthreads();
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    for (int e = wave; e < n; e += kStdThreads / 64) {
+        const int32_t c = cand[e];
         float s = 0.f;
-        if (feat >= 0) {
+        if (c >= 0) {
             float part = 0.f;
             for (int iota = lane; iota < d; iota += 64)
-                part += signed_by_parity(load_act<BF16>(x, t * d + iota), P.masks[iota] & (uint32_t)feat);
+                part += signed_by_parity(xrow[iota], P.masks[iota] & (uint32_t)c);
             s = wave_sum(part) * P.rsd;
         }
-        if (lane == 0) rec[e] = StdRec{feat, s};
+        if (lane == 0) rec[e] = StdRec{c, s};
     }
 }
 
@@ -213,6 +255,13 @@ dim3 std_grid(int64_t n, int threads)
 
 }  // namespace
 
+bool std_supported(const DevPlan& P)
+{
+    for (int l = 1; l < P.levels; ++l)
+        if (P.active[l - 1] * P.delta[l] > kStdMaxCand) return false;
+    return P.d <= 16384;
+}
+
 size_t std_workspace_bytes(const DevPlan& P)
 {
     size_t total = 0;
@@ -232,7 +281,7 @@ hipError_t launch_std_update(const DevPlan& P, const void* x, bool x_bf16, int64
 {
     const StdWs W = std_ws(ws, P, nullptr);
     float2* st = (float2*)stats;
-    const dim3 gc(kStdGroups, (P.d + kStdThreads - 1) / kStdThreads);
+    const dim3 gc(kStdGroups, (P.d + 4 * kStdThreads - 1) / (4 * kStdThreads));
     if (x_bf16) hipLaunchKernelGGL(std_col_kernel<true>, gc, dim3(kStdThreads), 0, stream, x, P.d, T, W);
     else hipLaunchKernelGGL(std_col_kernel<false>, gc, dim3(kStdThreads), 0, stream, x, P.d, T, W);
     hipLaunchKernelGGL(std_col_update_kernel, dim3((P.d + 255) / 256), dim3(256), 0, stream, P.d, T, W, st, var, beta,
@@ -240,8 +289,11 @@ hipError_t launch_std_update(const DevPlan& P, const void* x, bool x_bf16, int64
     const int m = (int)std::min<int64_t>(T, kStdSample);
     if (P.levels > 1 && m > 0) {
         const dim3 g2(m, P.levels - 1);
-        if (x_bf16) hipLaunchKernelGGL(std_sample_kernel<true>, g2, dim3(kStdThreads), 0, stream, P, x, T, m, idx, W);
-        else hipLaunchKernelGGL(std_sample_kernel<false>, g2, dim3(kStdThreads), 0, stream, P, x, T, m, idx, W);
+        const size_t xl = (size_t)P.d * 4;
+        allow_lds(std_sample_kernel<true>, xl);
+        allow_lds(std_sample_kernel<false>, xl);
+        if (x_bf16) hipLaunchKernelGGL(std_sample_kernel<true>, g2, dim3(kStdThreads), xl, stream, P, x, T, m, idx, W);
+        else hipLaunchKernelGGL(std_sample_kernel<false>, g2, dim3(kStdThreads), xl, stream, P, x, T, m, idx, W);
         const int64_t nrec = (int64_t)m * std_cands(P);
         hipLaunchKernelGGL(std_rec_clear_kernel, std_grid(nrec, 256), dim3(256), 0, stream, nrec, W);
         hipLaunchKernelGGL(std_rec_accum_kernel, std_grid(nrec, 256), dim3(256), 0, stream, nrec, W);
