@@ -8,7 +8,8 @@ The paper measures on residual-stream activations of GPT-2-style models
 trained on FineWeb-Edu (§3); those activations are not available, so these
 seeded draws stand in for them, with the shapes of the workloads below.
 
-Recipe (per workload with index c):
+Recipe (per workload with index c; the pt_* workloads use the per-level
+shapes of the paper's Table 6, with d = 1024 or 2048 and Delta = 256):
   * x  ~ N(0, 1) drawn as float32 by NumPy PCG64(seed 1000 + c), row-major, then
     rounded to bfloat16 (round-to-nearest-even) for bf16 workloads;
   * the gpt2 workload scales round(0.05 T) tokens by 4 (exact in bf16), chosen
@@ -37,6 +38,23 @@ class Workload:
     k: int              # active features on the last level
     tokens: int         # T
     dtype: str          # "f32" or "bf16" activations
+    # explicit per-level hierarchy (n_l, K_l), when it is not the even spacing
+    # of the configuration terms (the paper's own Table 6 shapes)
+    level_bits: tuple | None = None
+    active: tuple | None = None
+
+    def hierarchy(self):
+        """(level_bits, branching per level with [0] = 0, active) when explicit, else None."""
+        if self.level_bits is None:
+            return None
+        return list(self.level_bits), [0] + [self.branching] * (self.levels - 1), list(self.active)
+
+    def plan_kwargs(self) -> dict:
+        """Keyword arguments of the binding's Plan for this workload's hierarchy."""
+        h = self.hierarchy()
+        if h is None:
+            return dict(n_bits=self.n, levels=self.levels, branching=self.branching, beam=self.beam, k=self.k)
+        return dict(level_bits=h[0], branchings=h[1], active=h[2])
 
 
 WORKLOADS = {
@@ -45,6 +63,10 @@ WORKLOADS = {
     "wide": Workload("wide", 2, 768, 20, 5, 16, 8, 64, 65536, "bf16"),
     "very_wide": Workload("very_wide", 3, 1024, 24, 6, 16, 16, 64, 16384, "bf16"),
     "train": Workload("train", 4, 768, 20, 5, 16, 8, 64, 65536, "bf16"),
+    # Table 6 (App. G) hierarchies: 256 children scored per active parent
+    "pt_small_2l": Workload("pt_small_2l", 5, 1024, 15, 2, 256, 16, 32, 16384, "bf16", (10, 15), (16, 32)),
+    "pt_large_2l": Workload("pt_large_2l", 6, 2048, 15, 2, 256, 16, 32, 16384, "bf16", (11, 15), (16, 32)),
+    "pt_small_3l": Workload("pt_small_3l", 7, 1024, 17, 3, 256, 16, 64, 16384, "bf16", (10, 15, 17), (16, 32, 64)),
 }
 
 

@@ -1,0 +1,118 @@
+"""GPU parity on the paper's own hierarchies (App. G, Table 6): d = 1024 or
+2048, level bits (10|11, 15[, 17]), K = (16, 32[, 64]), 256 children scored per
+active parent.  Same rules as the other parity tests: encode against the
+oracle with near-tie exemptions above level 0, decode and backward on the
+oracle's codes; full-size runs on sampled rows.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_20652_amd import binding as dpb
+from paper_2607_20652_amd import inputs
+from parity_util import TOL_BF16, TOL_F32, compare_dense, compare_encode
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+NAMES = ["pt_small_2l", "pt_large_2l", "pt_small_3l"]
+_PLANS = {}
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    dpb.load()
+
+
+def plan_for(name):
+    if name not in _PLANS:
+        w = inputs.workload(name)
+        _PLANS[name] = dpb.Plan(w.d, seed=0, **w.plan_kwargs())
+    return _PLANS[name]
+
+
+def setup(name):
+    w = inputs.workload(name)
+    nb, dl, K = w.hierarchy()
+    return w, nb, dl, K, oracle.masks(w.d, nb[-1]), oracle.generators(nb, dl, 0)
+
+
+def test_plans_have_table6_shapes():
+    for name in NAMES:
+        w, nb, dl, K, _, _ = setup(name)
+        p = plan_for(name)
+        assert (p.level_bits, p.branching, p.active) == (nb, dl, K)
+        assert p.k_tot == sum(K)
+
+
+@pytest.mark.parametrize("name,T", [("pt_small_2l", 96), ("pt_large_2l", 37), ("pt_small_3l", 70)])
+def test_encode_matches_oracle(name, T):
+    say(f"[t6 encode] {name} T={T}")
+    plan = plan_for(name)
+    w, nb, dl, K, m, gens = setup(name)
+    x = inputs.activations(name, T)
+    idx, coef = dpb.encode(plan, x.to(DEV))
+    torch.cuda.synchronize()
+    oi, oc, om, oo = oracle.encode(w.d, m, nb, K, dl, gens, x.double().numpy())
+    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32)
+    say(f"  {st}")
+    assert st["exempt_tokens"] <= max(2, 0.02 * T)
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_encode_full_size_sampled(name):
+    w, nb, dl, K, m, gens = setup(name)
+    say(f"[t6 encode full] {name} T={w.tokens}")
+    plan = plan_for(name)
+    x = inputs.activations(name)
+    idx, coef = dpb.encode(plan, x.to(DEV))
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(w.index)
+    rows = np.unique(np.concatenate([np.arange(16), rng.choice(w.tokens, 32, replace=False),
+                                     np.arange(w.tokens - 16, w.tokens)]))
+    oi, oc, om, oo = oracle.encode(w.d, m, nb, K, dl, gens, x[rows].double().numpy())
+    st = compare_encode(K, idx.cpu().numpy()[rows], coef.cpu().numpy()[rows], oi, oc, om, oo, TOL_F32)
+    say(f"  {st}")
+    assert st["exempt_tokens"] <= max(2, 0.02 * len(rows))
+    # every emitted index is unique within its token and lies in its level
+    ii = idx.cpu().numpy()
+    lo = [0] + [1 << b for b in nb[:-1]]
+    hi = [w.d] + [1 << b for b in nb[1:]]
+    s = 0
+    for l, k in enumerate(K):
+        blk = ii[:, s:s + k]
+        assert ((blk >= lo[l]) & (blk < hi[l])).all()
+        srt = np.sort(blk, axis=1)
+        assert (srt[:, 1:] != srt[:, :-1]).all()
+        s += k
+
+
+@pytest.mark.parametrize("name,T", [("pt_small_2l", 130), ("pt_large_2l", 50), ("pt_small_3l", 90)])
+@pytest.mark.parametrize("out", ["f32", "bf16"])
+def test_decode_and_bwd_match_oracle(name, T, out):
+    say(f"[t6 decode+bwd] {name} T={T} {out}")
+    plan = plan_for(name)
+    w, nb, dl, K, m, gens = setup(name)
+    x = inputs.activations(name, T)
+    oi, oc, _, _ = oracle.encode(w.d, m, nb, K, dl, gens, x.double().numpy())
+    dt = torch.float32 if out == "f32" else torch.bfloat16
+    tol = TOL_F32 if out == "f32" else TOL_BF16
+    di = torch.from_numpy(oi).to(DEV)
+    y = dpb.decode(plan, di, torch.from_numpy(oc.astype(np.float32)).to(DEV), dt)
+    g = inputs.upstream_grad(name, T)
+    gc, gx = dpb.decode_bwd(plan, di, g.to(DEV), dt)
+    torch.cuda.synchronize()
+    compare_dense(y.float().cpu().numpy(), oracle.decode(w.d, m, oi, oc.astype(np.float32).astype(np.float64)), tol)
+    rgc, rgx = oracle.decode_bwd(w.d, m, oi, g.double().numpy())
+    compare_dense(gc.cpu().numpy(), rgc, TOL_F32)
+    compare_dense(gx.float().cpu().numpy(), rgx, tol)
