@@ -114,6 +114,30 @@ dpb_status dpb_plan_describe(const dpb_plan* plan, int* d, int* levels, int* lev
 dpb_status dpb_encode(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T,
                       int32_t* idx, float* coef, void* stream);
 
+/* Bytes of device workspace dpb_encode_ws needs for T tokens: 0 when the
+ * plan runs on the narrow encoder (at most 64 children per parent and the
+ * other limits of dpb_encode's fast path), else the child scores of up to
+ * 4096 tokens, 4 * min(T, 4096) * max_l K_{l-1} Delta_l bytes (128 MiB for
+ * the paper's 3-level hierarchy). */
+size_t dpb_encode_workspace_bytes(const dpb_plan* plan, int64_t T);
+
+/* ENCODE with a workspace: the general entry of which dpb_encode and
+ * dpb_encode_std are special cases.  For plans that score many children per
+ * parent (up to 256, as the paper's own hierarchies do, App. G Table 6) it
+ * runs each level as a matrix-core GEMM of all K_{l-1} x Delta_l child
+ * scores into the workspace, followed by the AbsTopK selection; results are
+ * the same as dpb_encode's.
+ *   stats     : device fp32 [N][2] standardization statistics, or NULL for
+ *               raw scores (see dpb_encode_std)
+ *   workspace : device, >= dpb_encode_workspace_bytes(plan, T), 16-B aligned,
+ *               caller-owned scratch (may be NULL when that is 0; with NULL,
+ *               wide plans fall back to the general encoder, and with stats
+ *               to DPB_EUNSUPPORTED)
+ * Other arguments as dpb_encode. */
+dpb_status dpb_encode_ws(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T,
+                         const float* stats, int32_t* idx, float* coef, void* workspace,
+                         size_t ws_bytes, void* stream);
+
 /* DECODE (§2.1): y = sum_slots coef * phi_idx, directions generated on chip.
  *   idx, coef : device [T, k_tot] (read; any valid code, not only encoder output)
  *   y         : device [T, d], fp32 or bf16 (y_dtype; written)

@@ -52,6 +52,8 @@ def load():
         "dpb_decode_bwd": (i32, [P, P, P, i32, i64, P, P, i32, P]),
         "dpb_decode_bwd_ex": (i32, [P, P, P, i32, i64, P, P, P, P, P, i32, P]),
         "dpb_encode_std": (i32, [P, P, i32, i64, P, P, P, P]),
+        "dpb_encode_workspace_bytes": (ctypes.c_size_t, [P, i64]),
+        "dpb_encode_ws": (i32, [P, P, i32, i64, P, P, P, P, ctypes.c_size_t, P]),
         "dpb_std_init": (i32, [P, P, P, P]),
         "dpb_std_workspace_bytes": (ctypes.c_size_t, [P]),
         "dpb_std_update": (i32, [P, P, i32, i64, P, ctypes.c_float, ctypes.c_float, P, P, P, ctypes.c_size_t, P]),
@@ -179,16 +181,29 @@ class Plan:
             pass
 
 
-def encode(plan: Plan, x: torch.Tensor, idx: torch.Tensor | None = None, coef: torch.Tensor | None = None):
-    """x [T, d] fp32/bf16 (device) -> (idx [T, k_tot] int32, coef [T, k_tot] fp32)."""
+def encode_workspace(plan: Plan, T: int, device) -> torch.Tensor | None:
+    """Workspace for encode of T tokens, or None when the plan needs none."""
+    n = int(load().dpb_encode_workspace_bytes(plan._handle, int(T)))
+    return None if n == 0 else torch.empty(((n + 15) // 16) * 4, dtype=torch.float32, device=device)
+
+
+def encode(plan: Plan, x: torch.Tensor, idx: torch.Tensor | None = None, coef: torch.Tensor | None = None,
+           stats: torch.Tensor | None = None, workspace: torch.Tensor | None = None):
+    """x [T, d] fp32/bf16 (device) -> (idx [T, k_tot] int32, coef [T, k_tot] fp32); on
+    standardized scores when stats is given.  A workspace is allocated when the
+    plan needs one (wide hierarchies) and none is given."""
     T = x.shape[0]
     assert x.dim() == 2 and x.shape[1] == plan.d
     if idx is None:
         idx = torch.empty((T, plan.k_tot), dtype=torch.int32, device=x.device)
     if coef is None:
         coef = torch.empty((T, plan.k_tot), dtype=torch.float32, device=x.device)
-    _check("dpb_encode", load().dpb_encode(plan._handle, _dev(x, "x"), _dtype_code(x), T, _dev(idx, "idx"),
-                                           _dev(coef, "coef"), _stream(x)))
+    if workspace is None:
+        workspace = encode_workspace(plan, T, x.device)
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check("dpb_encode_ws", load().dpb_encode_ws(plan._handle, _dev(x, "x"), _dtype_code(x), T,
+                                                 _opt(stats, "stats"), _dev(idx, "idx"), _dev(coef, "coef"),
+                                                 _opt(workspace, "workspace"), nbytes, _stream(x)))
     return idx, coef
 
 
@@ -364,19 +379,10 @@ def std_state(plan: Plan, device=None):
 
 
 def encode_std(plan: Plan, x: torch.Tensor, stats: torch.Tensor, idx: torch.Tensor | None = None,
-               coef: torch.Tensor | None = None):
+               coef: torch.Tensor | None = None, workspace: torch.Tensor | None = None):
     """Encoder on standardized scores z = (s - mu) r -> (idx, coef = z)."""
-    T = x.shape[0]
-    assert x.dim() == 2 and x.shape[1] == plan.d
     assert stats.dtype == torch.float32 and stats.shape == (1 << plan.level_bits[-1], 2)
-    if idx is None:
-        idx = torch.empty((T, plan.k_tot), dtype=torch.int32, device=x.device)
-    if coef is None:
-        coef = torch.empty((T, plan.k_tot), dtype=torch.float32, device=x.device)
-    _check("dpb_encode_std", load().dpb_encode_std(plan._handle, _dev(x, "x"), _dtype_code(x), T,
-                                                   _dev(stats, "stats"), _dev(idx, "idx"), _dev(coef, "coef"),
-                                                   _stream(x)))
-    return idx, coef
+    return encode(plan, x, idx, coef, stats=stats, workspace=workspace)
 
 
 def std_workspace(plan: Plan, device) -> torch.Tensor:

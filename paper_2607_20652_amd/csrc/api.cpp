@@ -80,6 +80,18 @@ dpb_status fill_plan(dpb_plan* plan, const Hierarchy& h, const uint32_t* gens, u
         P.gamma_t_off[l] = gt_off;
         if (live) gt_off += (int64_t)(P.dp / 16) * (P.dpad[l] / 16) * 64;
     }
+    {
+        int64_t gb = 0;
+        for (int l = 0; l < dpb::kMaxLevels; ++l) {
+            const bool live = l >= 1 && l < L;
+            P.gpad[l] = live ? (h.branching[l] + 31) / 32 * 32 : 0;
+            P.gbits_off[l] = gb;
+            gb += (int64_t)P.gpad[l] * P.nchunk;
+        }
+    }
+    P.bwd_direct = 0;
+    for (int l = 1; l < L; ++l)
+        if (h.branching[l] > 64) P.bwd_direct = 1;
     P.wave_tokens = maxcpt >= 16 ? 1 : 16 / maxcpt;
     P.leaf_columns = (L >= 2 && P.cpt[L - 1] >= 4 && P.cpt[L - 1] <= 16 && h.active[L - 1] >= 2 * h.active[L - 2] &&
                       P.dpad[L - 1] == 16 && P.slot_base[L - 2] + h.active[L - 2] <= dpb::kFrMax)
@@ -255,11 +267,33 @@ void build_gamma_fragments(const dpb_plan* plan, std::vector<uint16_t>* out)
     }
 }
 
+// Generator sign bitmaps (see DevPlan::gbits).
+void build_gen_bits(const dpb_plan* plan, std::vector<uint32_t>* out)
+{
+    const DevPlan& P = plan->dev;
+    int64_t total = 0;
+    for (int l = 1; l < P.levels; ++l) total += (int64_t)P.gpad[l] * P.nchunk;
+    out->assign((size_t)std::max<int64_t>(total, 1), 0);
+    for (int l = 1; l < P.levels; ++l) {
+        const uint32_t* g = plan->gens_h.data() + P.gens_off[l];
+        for (int j = 0; j < P.delta[l]; ++j)
+            for (int c = 0; c < P.nchunk; ++c) {
+                uint32_t word = 0;
+                for (int b = 0; b < 32; ++b) {
+                    const int iota = 32 * c + b;
+                    if (iota < P.d) word |= row_parity(plan->masks_h[iota], g[j]) << b;
+                }
+                (*out)[P.gbits_off[l] + (int64_t)j * P.nchunk + c] = word;
+            }
+    }
+}
+
 dpb_status upload(dpb_plan* plan)
 {
     DevPlan& P = plan->dev;
     std::vector<uint16_t> gamma, gamma_pair, gamma_t;
-    std::vector<uint32_t> nt;
+    std::vector<uint32_t> nt, gbits;
+    build_gen_bits(plan, &gbits);
     std::vector<uint32_t> gtab;
     build_gen_tables(plan, &gtab);
     build_gamma_fragments(plan, &gamma);
@@ -283,6 +317,7 @@ dpb_status upload(dpb_plan* plan)
         {gamma_t.data(), gamma_t.size() * 2, 0},
         {nt.data(), nt.size() * 4, 0},
         {gtab.data(), gtab.size() * 4, 0},
+        {gbits.data(), gbits.size() * 4, 0},
     };
     size_t total = 0;
     for (Part& p : parts) {
@@ -314,6 +349,7 @@ dpb_status upload(dpb_plan* plan)
     P.gamma_t = base + parts[4].off;
     P.nt = (const uint32_t*)(base + parts[5].off);
     P.gtab = (const uint32_t*)(base + parts[6].off);
+    P.gbits = (const uint32_t*)(base + parts[7].off);
     return DPB_OK;
 }
 
@@ -539,6 +575,38 @@ dpb_status dpb_decode_bwd_ex(const dpb_plan* plan, const int32_t* idx, const voi
     return launched(dpb::launch_decode_bwd2(plan->dev, idx, grad_y, g_dtype == DPB_BF16, T, grad_coef, grad_x,
                                            gx_dtype == DPB_BF16, (hipStream_t)stream, add_grad_coef, add_grad_x,
                                            stats));
+}
+
+size_t dpb_encode_workspace_bytes(const dpb_plan* plan, int64_t T)
+{
+    // sized for either activation type (the workspace does not depend on it)
+    if (!plan || T <= 0 || dpb::encode2_supported(plan->dev) ||
+        !(dpb::encode_wide_supported(plan->dev, true) || dpb::encode_wide_supported(plan->dev, false)))
+        return 0;
+    return dpb::encode_wide_workspace_bytes(plan->dev, T);
+}
+
+dpb_status dpb_encode_ws(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T, const float* stats,
+                         int32_t* idx, float* coef, void* workspace, size_t ws_bytes, void* stream)
+{
+    dpb_status s = check_call(plan, T);
+    if (s) return s;
+    if (!dtype_ok(x_dtype)) return DPB_EINVAL;
+    if (T == 0) return DPB_OK;
+    if (!x || !idx || !coef || !aligned16(x) || !aligned16(idx) || !aligned16(coef) || !aligned16(stats) ||
+        !aligned16(workspace))
+        return DPB_EINVAL;
+    const DevPlan& P = plan->dev;
+    const bool bf = x_dtype == DPB_BF16;
+    hipStream_t st = (hipStream_t)stream;
+    if (dpb::encode2_supported(P)) {
+        if (stats && !dpb::encode2_std_supported(P)) return DPB_EUNSUPPORTED;
+        return launched(dpb::launch_encode2(P, x, bf, T, stats, idx, coef, st));
+    }
+    if (dpb::encode_wide_supported(P, bf) && workspace && ws_bytes >= dpb::encode_wide_workspace_bytes(P, T))
+        return launched(dpb::launch_encode_wide(P, x, bf, T, stats, idx, coef, workspace, st));
+    if (stats) return DPB_EUNSUPPORTED;
+    return launched(dpb::launch_encode(P, x, bf, T, idx, coef, st));
 }
 
 dpb_status dpb_encode_std(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T, const float* stats,

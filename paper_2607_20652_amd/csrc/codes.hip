@@ -577,7 +577,8 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
         wave_sync();
 
         // route every slot of levels >= 1 to a parent slot of the previous level
-        route_slots(P, W, 1);
+        // (plans with many children per parent take every slot directly below)
+        if (!P.bwd_direct) route_slots(P, W, 1);
         // coefficients for basis slots and padding
         for (int tt = 0; tt < TPW; ++tt)
             for (int s = lane; s < k; s += 64) {
@@ -589,7 +590,8 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
         wave_sync();
 
         // grad_coef of routed slots: child scores of each parent column against g
-        for (int l = 1; l < P.levels; ++l) score_level<G_BF16>(P, W, l);
+        if (!P.bwd_direct)
+            for (int l = 1; l < P.levels; ++l) score_level<G_BF16>(P, W, l);
 
         // hashed slots that route nowhere: a direct reduction over the coordinates
         for (int tt = 0; tt < W.ntok; ++tt)

@@ -66,6 +66,15 @@ struct DevPlan {
     int gtab_shift[kMaxLevels];
     int gtab_total;             // entries over all levels (0: routing disabled)
     int gens_total;             // sum_l Delta_l
+    // Generator sign bitmaps: word (j, c) of level l at gbits_off[l] + j * nchunk + c
+    // has bit b = sign of phi~_{g_j} at coordinate 32c + b (1: negative), for
+    // j < gpad[l] = Delta_l rounded up to 32 (rows past Delta_l are zero).
+    const uint32_t* gbits;
+    int64_t gbits_off[kMaxLevels];
+    int gpad[kMaxLevels];
+    // 1: the backward takes <phi_s, g> of every slot directly instead of
+    // scoring all children of each parent column (many children per parent)
+    int bwd_direct;
 };
 
 
@@ -178,6 +187,11 @@ hipError_t launch_decode_bwd2(const DevPlan& P, const int32_t* idx, const void* 
 bool code_kernels_fit(const DevPlan& P);
 bool encode2_supported(const DevPlan& P);
 bool encode2_std_supported(const DevPlan& P);
+// Wide encoder (many children per parent): GEMM + selection per level.
+bool encode_wide_supported(const DevPlan& P, bool x_bf16);
+size_t encode_wide_workspace_bytes(const DevPlan& P, int64_t T);
+hipError_t launch_encode_wide(const DevPlan& P, const void* x, bool x_bf16, int64_t T, const float* stats,
+                              int32_t* idx, float* coef, void* ws, hipStream_t stream);
 hipError_t launch_encode2(const DevPlan& P, const void* x, bool x_bf16, int64_t T, const float* stats, int32_t* idx,
                           float* coef, hipStream_t stream);
 

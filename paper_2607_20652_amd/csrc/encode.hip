@@ -480,6 +480,412 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
     }
 }
 
+// ---------------------------------------------------------------------------
+// Wide encoder: levels that score many children per parent (the paper's own
+// hierarchies score 256, App. G Table 6).  Level 0 runs one wave per token.
+// Each level l >= 1 is then a GEMM and a selection:
+//  * wide_gemm_kernel: the scores of all K_{l-1} x Delta_l children of a
+//    chunk of tokens, S[(t, q)][j] = <gamma_j, phi~_{p_tq} (.) x_t> (§2.2
+//    child-scoring equation), as 16x16x32 bf16 MFMAs over a workgroup tile of
+//    all generator rows x 128 (token, parent) columns.  A fragments (exact
+//    +-1) are built from per-generator sign bitmaps held in LDS, B fragments
+//    from the token rows and the parents' sign bitmaps (nibble tables), as in
+//    the narrow encoder.  Scores go to a workspace, token-major.
+//  * wide_select_kernel: one wave per token; AbsTopK with deduplication (a
+//    child reached from several parents has bit-identical keys).  The K-th
+//    largest distinct key among each lane's top keys is a threshold with at
+//    least K distinct keys above it; the keys above it are collected in LDS,
+//    sorted by a bitonic network, and the first K distinct ones emitted.  If
+//    too many keys pass, an exact extraction (K rounds of a wave maximum
+//    below the previous key) takes over.
+constexpr int kWideCols = 128;     // (token, parent) columns of a GEMM workgroup
+constexpr int kWideList = 1024;    // collected keys per token
+constexpr int kWideThreads = 256;
+
+template <bool X_BF16, bool STD>
+__global__ __launch_bounds__(kWideThreads) void wide_level0_kernel(DevPlan P, const void* __restrict__ xin, int64_t T,
+                                                                   const float2* __restrict__ stats,
+                                                                   int32_t* __restrict__ out_idx,
+                                                                   float* __restrict__ out_coef)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, d = P.d, dp = P.dp;
+    const int ND = (dp / 2 + 63) / 64;
+    const int listn = P.active[0] * (X_BF16 ? 2 * ND : (d + 63) / 64);
+    const unsigned act_b = align16u(X_BF16 ? P.prow * 4 : dp * 4);
+    const unsigned per_wave = act_b + align16u(listn * 8) + align16u((P.active[0] + 1) * 4) + 16;
+    float2* st0 = (float2*)smem;
+    unsigned char* wb = smem + (STD ? align16u(d * 8) : 0u) + wave * per_wave;
+    uint32_t* pairs = (uint32_t*)wb;
+    float* xf = (float*)wb;
+    uint64_t* list = (uint64_t*)(wb + act_b);
+    int32_t* par = (int32_t*)(wb + act_b + align16u(listn * 8));
+    int* cnt = (int*)(wb + act_b + align16u(listn * 8) + align16u((P.active[0] + 1) * 4));
+    if constexpr (STD) {
+        for (int i = threadIdx.x; i < d; i += kWideThreads) st0[i] = stats[i];
+        __syncthreads();
+    }
+    const int x32 = (lane ^ 32) << 2;
+    for (int64_t t = (int64_t)blockIdx.x * 4 + wave; t < T; t += (int64_t)gridDim.x * 4) {
+        if constexpr (X_BF16) {
+            load_pairs(P, lane, 1, 1, (const uint16_t*)xin, t, pairs);
+        } else {
+            const float* xs = (const float*)xin;
+            for (int iota = lane; iota < dp; iota += 64) xf[iota] = iota < d ? xs[t * d + iota] : 0.f;
+        }
+        wave_sync();
+        if constexpr (STD)
+            level0_std<64, 6, X_BF16>(P, lane, t, 1, pairs, xf, st0, list, listn, cnt, par, 0, out_idx, out_coef, x32);
+        else if constexpr (X_BF16)
+            level0_bf16<64, 6>(P, lane, t, 1, pairs, list, listn, cnt, par, 0, out_idx, out_coef, x32);
+        else
+            level0_f32<64, 6>(P, lane, t, 1, xf, list, listn, cnt, par, 0, out_idx, out_coef, x32);
+        wave_sync();
+    }
+}
+
+// LDS of a GEMM workgroup: generator bitmaps, the tokens' rows, column bitmaps.
+__host__ __device__ inline unsigned wide_gemm_lds(const DevPlan& P, int l, bool x_bf16)
+{
+    const int TT = kWideCols / P.cpt[l];
+    return align16u(P.gpad[l] * P.cws * 4) + align16u(TT * (x_bf16 ? P.prow : P.dp) * 4) +
+           align16u(kWideCols * P.cws * 4);
+}
+
+// Scores of tokens [t0 + TT blockIdx.x, ...) of a chunk of ntok tokens at level
+// l into scores[(t - t0) K_{l-1} + q][j] (t0-relative tokens).  MT = 16-row
+// tiles per wave: waves (wr, wc) cover rows 16 MT wr .. and columns 64 wc ..
+template <bool X_BF16, int MT>
+__global__ __launch_bounds__(kWideThreads) void wide_gemm_kernel(DevPlan P, int l, const void* __restrict__ xin,
+                                                                 int64_t t0, int64_t ntok,
+                                                                 const int32_t* __restrict__ idx,
+                                                                 float* __restrict__ scores)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int KP = P.active[l - 1], KC = P.cpt[l], D = P.delta[l], nchunk = P.nchunk, d = P.d, dp = P.dp;
+    const int TT = kWideCols / KC;
+    const int64_t tb = (int64_t)blockIdx.x * TT;
+    const int nt_tok = (int)min((int64_t)TT, ntok - tb);
+    uint32_t* s_gb = (uint32_t*)smem;   // row stride cws (odd): the 16 rows of a fragment on 16 banks
+    unsigned char* p1 = smem + align16u(P.gpad[l] * P.cws * 4);
+    uint32_t* pairs = (uint32_t*)p1;
+    float* xf = (float*)p1;
+    uint32_t* cw = (uint32_t*)(p1 + align16u(TT * (X_BF16 ? P.prow : dp) * 4));
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+
+    const uint32_t* gsrc = P.gbits + P.gbits_off[l];
+    for (int i = threadIdx.x; i < P.gpad[l] * nchunk; i += kWideThreads) {
+        const int row = i / nchunk;
+        s_gb[row * P.cws + (i - row * nchunk)] = gsrc[i];
+    }
+    for (int tt = wave; tt < TT; tt += 4) {
+        if constexpr (X_BF16) {
+            load_pairs(P, lane, tt < nt_tok ? 1 : 0, 1, (const uint16_t*)xin, t0 + tb + tt, pairs + tt * P.prow);
+        } else {
+            const float* xs = (const float*)xin;
+            for (int iota = lane; iota < dp; iota += 64)
+                xf[tt * dp + iota] = (tt < nt_tok && iota < d) ? xs[(t0 + tb + tt) * d + iota] : 0.f;
+        }
+    }
+    // parents' sign bitmaps: one nibble-table word per 4-bit group of the index
+    for (int e = threadIdx.x; e < kWideCols * nchunk; e += kWideThreads) {
+        const int col = e / nchunk, w = e - col * nchunk, tt = col / KC, q = col - tt * KC;
+        const int32_t p = (tt < nt_tok && q < KP) ? idx[(t0 + tb + tt) * P.k_tot + P.slot_base[l - 1] + q] : -1;
+        uint32_t word = 0;
+        if (p >= 0)
+            for (int g = 0; g < P.nt_groups; ++g) word ^= P.nt[(g * nchunk + w) * 16 + ((p >> (4 * g)) & 15)];
+        cw[col * P.cws + w] = word;
+    }
+    __syncthreads();
+
+    const int wr = wave >> 1, wc = wave & 1, c16 = lane & 15, kq = lane >> 4;
+    f32x4 acc[MT][4];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int n = 0; n < 4; ++n) acc[mt][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int rowbase = wr * 16 * MT + c16;
+    for (int c = 0; c < nchunk; ++c) {
+        if constexpr (X_BF16) {
+            u32x4 b[4];
+#pragma unroll
+            for (int n = 0; n < 4; ++n) {
+                const int col = wc * 64 + n * 16 + c16, tt = col / KC;
+                const uint32_t R = rotl32(cw[col * P.cws + c], 15u - 4u * (uint32_t)kq);
+                const u32x4 pd = *(const u32x4*)(pairs + tt * P.prow + c * 16 + kq * 4);
+                b[n].x = pd.x ^ (R & 0x80008000u);
+                b[n].y = pd.y ^ (__builtin_amdgcn_alignbit(R, R, 1) & 0x80008000u);
+                b[n].z = pd.z ^ (__builtin_amdgcn_alignbit(R, R, 2) & 0x80008000u);
+                b[n].w = pd.w ^ (__builtin_amdgcn_alignbit(R, R, 3) & 0x80008000u);
+            }
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                const uint32_t RA = rotl32(s_gb[(rowbase + 16 * mt) * P.cws + c], 15u - 4u * (uint32_t)kq);
+                u32x4 a;
+                a.x = 0x3F803F80u | (RA & 0x80008000u);
+                a.y = 0x3F803F80u | (__builtin_amdgcn_alignbit(RA, RA, 1) & 0x80008000u);
+                a.z = 0x3F803F80u | (__builtin_amdgcn_alignbit(RA, RA, 2) & 0x80008000u);
+                a.w = 0x3F803F80u | (__builtin_amdgcn_alignbit(RA, RA, 3) & 0x80008000u);
+                const bf16x8 av = __builtin_bit_cast(bf16x8, a);
+#pragma unroll
+                for (int n = 0; n < 4; ++n)
+                    acc[mt][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, b[n]), acc[mt][n],
+                                                                         0, 0, 0);
+            }
+        } else {
+            // fp32 activations: each value split exactly into three bf16 terms
+            u32x4 bh[4], bm[4], bl[4];
+#pragma unroll
+            for (int n = 0; n < 4; ++n) {
+                const int col = wc * 64 + n * 16 + c16, tt = col / KC;
+                const uint32_t wd = cw[col * P.cws + c];
+                uint32_t hi[8], mi[8], lo[8];
+#pragma unroll
+                for (int x = 0; x < 8; ++x) {
+                    const int off = 4 * kq + (x >> 1) + 16 * (x & 1);
+                    float v = xf[tt * dp + 32 * c + off];
+                    v = __uint_as_float(__float_as_uint(v) ^ (((wd >> off) & 1u) << 31));
+                    split3(v, hi[x], mi[x], lo[x]);
+                }
+                bh[n] = u32x4{hi[0] | (hi[1] << 16), hi[2] | (hi[3] << 16), hi[4] | (hi[5] << 16), hi[6] | (hi[7] << 16)};
+                bm[n] = u32x4{mi[0] | (mi[1] << 16), mi[2] | (mi[3] << 16), mi[4] | (mi[5] << 16), mi[6] | (mi[7] << 16)};
+                bl[n] = u32x4{lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16), lo[4] | (lo[5] << 16), lo[6] | (lo[7] << 16)};
+            }
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                const uint32_t RA = rotl32(s_gb[(rowbase + 16 * mt) * P.cws + c], 15u - 4u * (uint32_t)kq);
+                u32x4 a;
+                a.x = 0x3F803F80u | (RA & 0x80008000u);
+                a.y = 0x3F803F80u | (__builtin_amdgcn_alignbit(RA, RA, 1) & 0x80008000u);
+                a.z = 0x3F803F80u | (__builtin_amdgcn_alignbit(RA, RA, 2) & 0x80008000u);
+                a.w = 0x3F803F80u | (__builtin_amdgcn_alignbit(RA, RA, 3) & 0x80008000u);
+                const bf16x8 av = __builtin_bit_cast(bf16x8, a);
+#pragma unroll
+                for (int n = 0; n < 4; ++n) {
+                    acc[mt][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, bh[n]),
+                                                                         acc[mt][n], 0, 0, 0);
+                    acc[mt][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, bm[n]),
+                                                                         acc[mt][n], 0, 0, 0);
+                    acc[mt][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, bl[n]),
+                                                                         acc[mt][n], 0, 0, 0);
+                }
+            }
+        }
+    }
+    // scores (times 1/sqrt d) of the live (token, parent) columns and generator rows
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+        const int col = wc * 64 + n * 16 + c16, tt = col / KC, q = col - tt * KC;
+        if (tt >= nt_tok || q >= KP) continue;
+        float* dst = scores + ((tb + tt) * KP + q) * D;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const int j0 = wr * 16 * MT + 16 * mt + 4 * kq;
+            if (j0 < D) {
+                const f32x4 v = acc[mt][n];
+                *(float4*)(dst + j0) = make_float4(v[0] * P.rsd, v[1] * P.rsd, v[2] * P.rsd, v[3] * P.rsd);
+            }
+        }
+    }
+}
+
+// Exclusive prefix over the wave of per-lane counts below 2^5.
+__device__ __forceinline__ int wave_prefix5(int cnt, int lane, int& total)
+{
+    const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+    int before = 0;
+    total = 0;
+#pragma unroll
+    for (int b = 0; b < 5; ++b) {
+        const uint64_t m = __ballot((cnt >> b) & 1);
+        before += (int)__popcll(m & below) << b;
+        total += (int)__popcll(m) << b;
+    }
+    return before;
+}
+
+// Sorts the n <= 64 R keys of the list (0-padded) and emits the first K
+// distinct ones of the token into slots [sb, sb + K); returns how many.
+template <int R>
+__device__ __forceinline__ int wide_emit(const DevPlan& P, const uint64_t* lst, int n, int K, int lane, int x32,
+                                         int64_t t, int sb, int32_t* out_idx, float* out_coef)
+{
+    uint64_t v[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int e = lane * R + r;
+        v[r] = e < n ? lst[e] : 0ull;
+    }
+    sort_desc<R, 6, false>(v, lane, x32);
+    uint64_t prev = shfl_u64(v[R - 1], (lane + 63) & 63);
+    if (lane == 0) prev = 0ull;
+    int kept = 0, cnt = 0;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const bool k = v[r] != 0ull && v[r] != prev;
+        kept |= (int)k << r;
+        cnt += (int)k;
+        prev = v[r];
+    }
+    int total = 0;
+    int rank = wave_prefix5(cnt, lane, total);
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        if (((kept >> r) & 1) && rank < K) {
+            out_idx[t * P.k_tot + sb + rank] = (int32_t)key_index(v[r]);
+            out_coef[t * P.k_tot + sb + rank] = key_value(v[r]);
+        }
+        rank += (kept >> r) & 1;
+    }
+    return total;
+}
+
+template <bool STD>
+__global__ __launch_bounds__(kWideThreads) void wide_select_kernel(DevPlan P, int l, int64_t t0, int64_t ntok,
+                                                                   const float* __restrict__ scores,
+                                                                   const float2* __restrict__ stats,
+                                                                   int32_t* __restrict__ out_idx,
+                                                                   float* __restrict__ out_coef)
+{
+    __shared__ uint64_t s_list[4][kWideList];
+    __shared__ int32_t s_par[4][128];
+    __shared__ uint32_t s_gen[256];
+    __shared__ int s_cnt[4];
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, x32 = (lane ^ 32) << 2;
+    const int KP = P.active[l - 1], D = P.delta[l], K = P.active[l], n = KP * D, sb = P.slot_base[l];
+    const int dsh = 31 - __builtin_clz((unsigned)D);
+    for (int j = threadIdx.x; j < D; j += kWideThreads) s_gen[j] = P.gens[P.gens_off[l] + j];
+    __syncthreads();
+    const int64_t tl = (int64_t)blockIdx.x * 4 + wave;   // chunk-relative token
+    if (tl >= ntok) return;
+    const int64_t t = t0 + tl;
+    for (int q = lane; q < KP; q += 64) s_par[wave][q] = out_idx[t * P.k_tot + P.slot_base[l - 1] + q];
+    if (lane == 0) s_cnt[wave] = 0;
+    wave_sync();
+    const float* src = scores + tl * (int64_t)n;
+
+    // keys of this lane's candidates f = 64 e + lane, eight per round
+    constexpr int B = 8;
+    auto keys8 = [&](int e0, uint64_t (&k)[B]) {
+        float v[B];
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            const int f = (e0 + b) * 64 + lane;
+            v[b] = f < n ? src[f] : 0.f;
+        }
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            const int f = (e0 + b) * 64 + lane;
+            k[b] = 0ull;
+            if (f < n) {
+                const int32_t p = s_par[wave][f >> dsh];
+                if (p >= 0) {
+                    const uint32_t c = (uint32_t)p ^ s_gen[f & (D - 1)];
+                    float z = v[b];
+                    if constexpr (STD) {
+                        const float2 st = stats[c];
+                        z = (z - st.x) * st.y;
+                    }
+                    k[b] = make_key(z, c);
+                }
+            }
+        }
+    };
+    const int rounds = (n + 64 * B - 1) / (64 * B);
+
+    // threshold: the K-th largest distinct key among the lanes' top two keys
+    constexpr int M = 2;
+    uint64_t top[M] = {0ull, 0ull};
+    for (int rd = 0; rd < rounds; ++rd) {
+        uint64_t k[B];
+        keys8(rd * B, k);
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            if (k[b] > top[0]) {
+                top[1] = top[0];
+                top[0] = k[b];
+            } else if (k[b] > top[1] && k[b] != top[0]) {
+                top[1] = k[b];
+            }
+        }
+    }
+    sort_desc<M, 6, false>(top, lane, x32);
+    uint64_t prev = shfl_u64(top[M - 1], (lane + 63) & 63);
+    if (lane == 0) prev = 0ull;
+    int kept = 0, cnt = 0;
+#pragma unroll
+    for (int r = 0; r < M; ++r) {
+        const bool kk = top[r] != 0ull && top[r] != prev;
+        kept |= (int)kk << r;
+        cnt += (int)kk;
+        prev = top[r];
+    }
+    int total = 0;
+    int rank = wave_prefix5(cnt, lane, total);
+    uint64_t tau_l = 0ull;
+#pragma unroll
+    for (int r = 0; r < M; ++r) {
+        if (((kept >> r) & 1) && rank == K - 1) tau_l = top[r];
+        rank += (kept >> r) & 1;
+    }
+    // one lane holds tau when at least K distinct keys were seen; else take every key
+    uint64_t tau = 1ull;
+    const uint64_t hb = __ballot(tau_l != 0ull);
+    if (hb) tau = shfl_u64(tau_l, __builtin_ctzll(hb));
+
+    // collect the keys >= tau
+    uint64_t* lst = s_list[wave];
+    for (int rd = 0; rd < rounds; ++rd) {
+        uint64_t k[B];
+        keys8(rd * B, k);
+#pragma unroll
+        for (int b = 0; b < B; ++b)
+            if (k[b] >= tau && k[b] != 0ull) {
+                const int pos = atomicAdd(&s_cnt[wave], 1);
+                if (pos < kWideList) lst[pos] = k[b];
+            }
+    }
+    wave_sync();
+    const int nl = s_cnt[wave];
+    int emitted;
+    if (nl <= 64) emitted = wide_emit<1>(P, lst, nl, K, lane, x32, t, sb, out_idx, out_coef);
+    else if (nl <= 128) emitted = wide_emit<2>(P, lst, nl, K, lane, x32, t, sb, out_idx, out_coef);
+    else if (nl <= 256) emitted = wide_emit<4>(P, lst, nl, K, lane, x32, t, sb, out_idx, out_coef);
+    else if (nl <= 512) emitted = wide_emit<8>(P, lst, nl, K, lane, x32, t, sb, out_idx, out_coef);
+    else if (nl <= kWideList) emitted = wide_emit<16>(P, lst, nl, K, lane, x32, t, sb, out_idx, out_coef);
+    else {
+        // exact extraction: K rounds of the largest key below the previous one
+        uint64_t last = ~0ull;
+        emitted = 0;
+        for (int r = 0; r < K; ++r) {
+            uint64_t best = 0ull;
+            for (int rd = 0; rd < rounds; ++rd) {
+                uint64_t k[B];
+                keys8(rd * B, k);
+#pragma unroll
+                for (int b = 0; b < B; ++b)
+                    if (k[b] < last && k[b] > best) best = k[b];
+            }
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1) {
+                const uint64_t o = shfl_u64(best, lane ^ off);
+                best = o > best ? o : best;
+            }
+            if (best == 0ull) break;
+            if (lane == 0) {
+                out_idx[t * P.k_tot + sb + r] = (int32_t)key_index(best);
+                out_coef[t * P.k_tot + sb + r] = key_value(best);
+            }
+            last = best;
+            ++emitted;
+        }
+    }
+    for (int r = emitted + lane; r < K; r += 64) {
+        out_idx[t * P.k_tot + sb + r] = -1;
+        out_coef[t * P.k_tot + sb + r] = 0.f;
+    }
+}
+
 }  // namespace
 
 // Whether the standardized encoder's workgroup fits the LDS budget.
@@ -543,6 +949,110 @@ hipError_t launch_encode2(const DevPlan& P, const void* x, bool x_bf16, int64_t 
     }
 #undef DPB_ENC_R
 #undef DPB_ENC
+    return hipGetLastError();
+}
+
+// Tokens per pass of the wide encoder (bounds its workspace).
+constexpr int64_t kWideChunkTokens = 4096;
+
+static int wide_max_cands(const DevPlan& P)
+{
+    int m = 0;
+    for (int l = 1; l < P.levels; ++l) m = std::max(m, P.active[l - 1] * P.delta[l]);
+    return m;
+}
+
+static unsigned wide_level0_lds(const DevPlan& P, bool x_bf16, bool std)
+{
+    const int ND = (P.dp / 2 + 63) / 64;
+    const int listn = P.active[0] * (x_bf16 ? 2 * ND : (P.d + 63) / 64);
+    const unsigned per_wave = align16u(x_bf16 ? P.prow * 4 : P.dp * 4) + align16u(listn * 8) +
+                              align16u((P.active[0] + 1) * 4) + 16;
+    return (std ? align16u(P.d * 8) : 0u) + 4 * per_wave;
+}
+
+bool encode_wide_supported(const DevPlan& P, bool x_bf16)
+{
+    if (P.levels < 2 || P.active[0] > 64 || P.d > 4096) return false;
+    if (wide_level0_lds(P, x_bf16, true) > (unsigned)kLdsBudget) return false;
+    for (int l = 1; l < P.levels; ++l) {
+        const int D = P.delta[l];
+        if (D < 16 || D > 256 || (D & (D - 1)) || P.cpt[l] > 128 || P.active[l] > 128) return false;
+        if (P.active[l - 1] * D > 64 * 128) return false;
+        if (wide_gemm_lds(P, l, x_bf16) > (unsigned)kLdsBudget) return false;
+    }
+    return true;
+}
+
+size_t encode_wide_workspace_bytes(const DevPlan& P, int64_t T)
+{
+    const int64_t ch = std::min<int64_t>(T, kWideChunkTokens);
+    return ch > 0 ? ((size_t)ch * wide_max_cands(P) * 4 + 255) & ~(size_t)255 : 0;
+}
+
+template <bool XB>
+static void launch_wide_gemm(const DevPlan& P, int l, const void* x, int64_t c0, int64_t nc, const int32_t* idx,
+                             float* scores, hipStream_t stream)
+{
+    const int TT = kWideCols / P.cpt[l];
+    const dim3 grid((unsigned)((nc + TT - 1) / TT));
+    const size_t lds = wide_gemm_lds(P, l, XB);
+    const int MT = std::max(32, P.delta[l]) / 32;
+#define DPB_WG(M)                                                                                             \
+    do {                                                                                                      \
+        allow_lds(wide_gemm_kernel<XB, M>, lds);                                                              \
+        hipLaunchKernelGGL((wide_gemm_kernel<XB, M>), grid, dim3(kWideThreads), lds, stream, P, l, x, c0, nc, idx, \
+                           scores);                                                                           \
+    } while (0)
+    if (MT == 1) DPB_WG(1);
+    else if (MT == 2) DPB_WG(2);
+    else if (MT == 4) DPB_WG(4);
+    else DPB_WG(8);
+#undef DPB_WG
+}
+
+template <bool STD>
+static void launch_wide_select(const DevPlan& P, int l, int64_t c0, int64_t nc, const float* scores,
+                               const float2* st, int32_t* idx, float* coef, hipStream_t stream)
+{
+    const dim3 grid((unsigned)((nc + 3) / 4));
+    hipLaunchKernelGGL((wide_select_kernel<STD>), grid, dim3(kWideThreads), 0, stream, P, l, c0, nc, scores, st, idx,
+                       coef);
+}
+
+hipError_t launch_encode_wide(const DevPlan& P, const void* x, bool x_bf16, int64_t T, const float* stats,
+                              int32_t* idx, float* coef, void* ws, hipStream_t stream)
+{
+    const float2* st = (const float2*)stats;
+    {
+        int cus = 256, dev = 0;
+        hipDeviceProp_t prop;
+        if (hipGetDevice(&dev) == hipSuccess && hipGetDeviceProperties(&prop, dev) == hipSuccess)
+            cus = prop.multiProcessorCount;
+        const dim3 grid((unsigned)std::max<int64_t>(1, std::min<int64_t>((T + 3) / 4, (int64_t)cus * 8)));
+        const size_t lds = wide_level0_lds(P, x_bf16, st != nullptr);
+#define DPB_W0(XB, SD)                                                                                        \
+    do {                                                                                                      \
+        allow_lds(wide_level0_kernel<XB, SD>, lds);                                                           \
+        hipLaunchKernelGGL((wide_level0_kernel<XB, SD>), grid, dim3(kWideThreads), lds, stream, P, x, T, st, idx, \
+                           coef);                                                                             \
+    } while (0)
+        if (x_bf16 && st) DPB_W0(true, true);
+        else if (x_bf16) DPB_W0(true, false);
+        else if (st) DPB_W0(false, true);
+        else DPB_W0(false, false);
+#undef DPB_W0
+    }
+    float* scores = (float*)ws;
+    for (int64_t c0 = 0; c0 < T; c0 += kWideChunkTokens) {
+        const int64_t nc = std::min<int64_t>(kWideChunkTokens, T - c0);
+        for (int l = 1; l < P.levels; ++l) {
+            if (x_bf16) launch_wide_gemm<true>(P, l, x, c0, nc, idx, scores, stream);
+            else launch_wide_gemm<false>(P, l, x, c0, nc, idx, scores, stream);
+            if (st) launch_wide_select<true>(P, l, c0, nc, scores, st, idx, coef, stream);
+            else launch_wide_select<false>(P, l, c0, nc, scores, st, idx, coef, stream);
+        }
+    }
     return hipGetLastError();
 }
 

@@ -89,6 +89,8 @@ def test_compute_calls_reject_null_plan(lib):
     assert lib.dpb_decode_bwd(None, P(16), P(16), 0, 4, P(16), P(16), 0, None) == -1
     assert lib.dpb_decode_bwd_ex(None, P(16), P(16), 0, 4, None, None, None, P(16), P(16), 0, None) == -1
     assert lib.dpb_encode_std(None, P(16), 0, 4, P(16), P(16), P(16), None) == -1
+    assert lib.dpb_encode_ws(None, P(16), 0, 4, None, P(16), P(16), None, 0, None) == -1
+    assert lib.dpb_encode_workspace_bytes(None, 4) == 0
     assert lib.dpb_std_init(None, P(16), P(16), None) == -1
     assert lib.dpb_std_update(None, P(16), 0, 4, P(16), 0.1, 1e-6, P(16), P(16), P(16), 1 << 20, None) == -1
     assert lib.dpb_std_workspace_bytes(None) == 0
