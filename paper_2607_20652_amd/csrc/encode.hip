@@ -605,14 +605,44 @@ __global__ __launch_bounds__(kWideThreads) void wide_gemm_kernel(DevPlan P, int 
 #pragma unroll
         for (int n = 0; n < 4; ++n) acc[mt][n] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int rowbase = wr * 16 * MT + c16;
-    for (int c = 0; c < nchunk; ++c) {
+    int bcol[4], btok[4];
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+        bcol[n] = wc * 64 + n * 16 + c16;
+        btok[n] = bcol[n] / KC;
+    }
+    // the LDS words of chunk c + 1 are requested before chunk c is computed
+    // (two register sets, used in turn)
+    struct Words {
+        uint32_t a[MT], b[4];
+        u32x4 pd[4];
+    };
+    auto fetch = [&](int c, Words& W) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) W.a[mt] = s_gb[(rowbase + 16 * mt) * P.cws + c];
+#pragma unroll
+        for (int n = 0; n < 4; ++n) {
+            W.b[n] = cw[bcol[n] * P.cws + c];
+            if constexpr (X_BF16) W.pd[n] = *(const u32x4*)(pairs + btok[n] * P.prow + c * 16 + kq * 4);
+        }
+    };
+    // A dword i: bf16 +-1 pair with the signs at coordinates 4kq + i and 16 + 4kq + i of the chunk
+    auto afrag = [&](uint32_t w) -> bf16x8 {
+        const uint32_t R = rotl32(w, 15u - 4u * (uint32_t)kq);
+        u32x4 a;
+        a.x = __builtin_amdgcn_bitop3_b32(R, 0x80008000u, 0x3F803F80u, 0xEA);   // (R & M) | one
+        a.y = __builtin_amdgcn_bitop3_b32(__builtin_amdgcn_alignbit(R, R, 1), 0x80008000u, 0x3F803F80u, 0xEA);
+        a.z = __builtin_amdgcn_bitop3_b32(__builtin_amdgcn_alignbit(R, R, 2), 0x80008000u, 0x3F803F80u, 0xEA);
+        a.w = __builtin_amdgcn_bitop3_b32(__builtin_amdgcn_alignbit(R, R, 3), 0x80008000u, 0x3F803F80u, 0xEA);
+        return __builtin_bit_cast(bf16x8, a);
+    };
+    auto compute = [&](int c, const Words& W) {
         if constexpr (X_BF16) {
             u32x4 b[4];
 #pragma unroll
             for (int n = 0; n < 4; ++n) {
-                const int col = wc * 64 + n * 16 + c16, tt = col / KC;
-                const uint32_t R = rotl32(cw[col * P.cws + c], 15u - 4u * (uint32_t)kq);
-                const u32x4 pd = *(const u32x4*)(pairs + tt * P.prow + c * 16 + kq * 4);
+                const uint32_t R = rotl32(W.b[n], 15u - 4u * (uint32_t)kq);
+                const u32x4 pd = W.pd[n];
                 b[n].x = pd.x ^ (R & 0x80008000u);
                 b[n].y = pd.y ^ (__builtin_amdgcn_alignbit(R, R, 1) & 0x80008000u);
                 b[n].z = pd.z ^ (__builtin_amdgcn_alignbit(R, R, 2) & 0x80008000u);
@@ -620,13 +650,7 @@ __global__ __launch_bounds__(kWideThreads) void wide_gemm_kernel(DevPlan P, int 
             }
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
-                const uint32_t RA = rotl32(s_gb[(rowbase + 16 * mt) * P.cws + c], 15u - 4u * (uint32_t)kq);
-                u32x4 a;
-                a.x = 0x3F803F80u | (RA & 0x80008000u);
-                a.y = 0x3F803F80u | (__builtin_amdgcn_alignbit(RA, RA, 1) & 0x80008000u);
-                a.z = 0x3F803F80u | (__builtin_amdgcn_alignbit(RA, RA, 2) & 0x80008000u);
-                a.w = 0x3F803F80u | (__builtin_amdgcn_alignbit(RA, RA, 3) & 0x80008000u);
-                const bf16x8 av = __builtin_bit_cast(bf16x8, a);
+                const bf16x8 av = afrag(W.a[mt]);
 #pragma unroll
                 for (int n = 0; n < 4; ++n)
                     acc[mt][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, b[n]), acc[mt][n],
@@ -637,8 +661,8 @@ __global__ __launch_bounds__(kWideThreads) void wide_gemm_kernel(DevPlan P, int 
             u32x4 bh[4], bm[4], bl[4];
 #pragma unroll
             for (int n = 0; n < 4; ++n) {
-                const int col = wc * 64 + n * 16 + c16, tt = col / KC;
-                const uint32_t wd = cw[col * P.cws + c];
+                const int tt = btok[n];
+                const uint32_t wd = W.b[n];
                 uint32_t hi[8], mi[8], lo[8];
 #pragma unroll
                 for (int x = 0; x < 8; ++x) {
@@ -653,13 +677,7 @@ __global__ __launch_bounds__(kWideThreads) void wide_gemm_kernel(DevPlan P, int 
             }
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
-                const uint32_t RA = rotl32(s_gb[(rowbase + 16 * mt) * P.cws + c], 15u - 4u * (uint32_t)kq);
-                u32x4 a;
-                a.x = 0x3F803F80u | (RA & 0x80008000u);
-                a.y = 0x3F803F80u | (__builtin_amdgcn_alignbit(RA, RA, 1) & 0x80008000u);
-                a.z = 0x3F803F80u | (__builtin_amdgcn_alignbit(RA, RA, 2) & 0x80008000u);
-                a.w = 0x3F803F80u | (__builtin_amdgcn_alignbit(RA, RA, 3) & 0x80008000u);
-                const bf16x8 av = __builtin_bit_cast(bf16x8, a);
+                const bf16x8 av = afrag(W.a[mt]);
 #pragma unroll
                 for (int n = 0; n < 4; ++n) {
                     acc[mt][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, bh[n]),
@@ -671,6 +689,14 @@ __global__ __launch_bounds__(kWideThreads) void wide_gemm_kernel(DevPlan P, int 
                 }
             }
         }
+    };
+    Words w0, w1;
+    fetch(0, w0);
+    for (int c = 0; c < nchunk; c += 2) {
+        if (c + 1 < nchunk) fetch(c + 1, w1);
+        compute(c, w0);
+        if (c + 2 < nchunk) fetch(c + 2, w0);
+        if (c + 1 < nchunk) compute(c + 1, w1);
     }
     // scores (times 1/sqrt d) of the live (token, parent) columns and generator rows
 #pragma unroll
