@@ -544,6 +544,101 @@ __device__ void score_level(const DevPlan& P, const Wave& W, int l)
     }
 }
 
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+
+// c + a.lo b.lo + a.hi b.hi for bf16 pairs.  The operands are taken as plain
+// words: a bit cast of a vector element (pq.y) reads element 0 with this
+// compiler.
+__device__ __forceinline__ float dot2u(uint32_t a, uint32_t b, float c)
+{
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2v, a), __builtin_bit_cast(bf16x2v, b), c, false);
+}
+
+// +-1 bf16 pair carrying bits 15 and 31 of R as its signs
+__device__ __forceinline__ uint32_t unit_pair(uint32_t R)
+{
+    return __builtin_amdgcn_bitop3_b32(R, 0x80008000u, 0x3F803F80u, 0xEA);   // (R & signs) | one
+}
+
+// grad_coef of the hashed slots that route nowhere: the scaled sum over the
+// coordinates of g(iota) (-1)^{parity(M_iota & c)} for slot index c, with
+// one lane per slot (2, 4 or 8 lanes per slot on the last, partial round,
+// each taking every 2nd, 4th or 8th chunk).  The slot's signs over the 32
+// coordinates of chunk w form one word, the XOR of one nibble-table word per
+// 4-bit group of c (parity is linear in the index bits).  bf16 g: dword o of
+// the chunk holds coordinates o and o + 16, which meet the +-1 pair made from
+// word bits o and o + 16 in a two-element dot product (fp32 accumulation).
+template <bool G_BF16, int NG>
+__device__ void direct_scores(const DevPlan& P, const Wave& W)
+{
+    const int k = P.k_tot, n = W.ntok * k, lane = W.lane, nchunk = P.nchunk, d = P.d, ng = P.nt_groups;
+    int32_t* list = (int32_t*)W.score;   // 256 entries
+    const uint64_t below = (1ull << lane) - 1;
+    for (int w0 = 0; w0 < n; w0 += 256) {
+        int m = 0;
+        for (int b = w0; b < min(n, w0 + 256); b += 64) {
+            const int i = b + lane;
+            const bool act = i < n && W.idx[i] >= d && W.route[i] < 0;
+            const uint64_t bal = __ballot(act);
+            if (act) list[m + __popcll(bal & below)] = i;
+            m += __popcll(bal);
+        }
+        wave_sync();
+        for (int r0 = 0; r0 < m; r0 += 64) {
+            const int mr = min(64, m - r0);
+            const int sh = mr > 32 ? 0 : mr > 16 ? 1 : mr > 8 ? 2 : 3;   // 2^sh lanes per slot
+            const int r = lane & ((64 >> sh) - 1), part = lane >> (6 - sh);
+            const bool valid = r < mr;
+            const int item = list[r0 + (valid ? r : 0)];
+            const int tt = item / k;
+            const uint32_t c = (uint32_t)W.idx[item];
+            float acc0 = 0.f, acc1 = 0.f;
+            // the nibble-table words of the next chunk are requested before
+            // this chunk is summed (groups past ng read a valid word and drop it)
+            uint32_t tw[NG];
+            auto fetch_words = [&](int w) {
+#pragma unroll
+                for (int g = 0; g < NG; ++g)
+                    tw[g] = P.nt[(min(g, ng - 1) * nchunk + w) * 16 + ((c >> (4 * g)) & 15u)];
+            };
+            auto fold_words = [&]() {
+                uint32_t v = 0;
+#pragma unroll
+                for (int g = 0; g < NG; ++g) v ^= g < ng ? tw[g] : 0u;
+                return v;
+            };
+            fetch_words(min(part, nchunk - 1));
+            for (int w = part; w < nchunk; w += 1 << sh) {
+                const uint32_t word = fold_words();
+                fetch_words(min(w + (1 << sh), nchunk - 1));
+                if constexpr (G_BF16) {
+                    const u32x4* pr = (const u32x4*)(W.pairs + tt * P.prow + w * 16);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const u32x4 pq = pr[q];
+                        const int o = 4 * q;
+                        acc0 = dot2u(pq.x, unit_pair(word << (15 - o)), acc0);
+                        acc1 = dot2u(pq.y, unit_pair(word << (14 - o)), acc1);
+                        acc0 = dot2u(pq.z, unit_pair(word << (13 - o)), acc0);
+                        acc1 = dot2u(pq.w, unit_pair(word << (12 - o)), acc1);
+                    }
+                } else {
+                    const float* gr = W.gf + tt * P.dp + 32 * w;
+#pragma unroll
+                    for (int b = 0; b < 32; b += 2) {
+                        acc0 += __uint_as_float(__float_as_uint(gr[b]) ^ ((word << (31 - b)) & 0x80000000u));
+                        acc1 += __uint_as_float(__float_as_uint(gr[b + 1]) ^ ((word << (30 - b)) & 0x80000000u));
+                    }
+                }
+            }
+            float acc = acc0 + acc1;
+            for (int off = 64 >> sh; off < 64; off <<= 1) acc += __shfl_xor(acc, off, 64);
+            if (valid && part == 0) W.coef[item] = P.rsd * acc;
+        }
+        wave_sync();   // the list is rewritten by the next window
+    }
+}
+
 template <bool G_BF16, bool GX_BF16, int NG, bool PB16>
 __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const int32_t* __restrict__ idx,
                                                                const void* __restrict__ g, int64_t T,
@@ -593,23 +688,9 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
         if (!P.bwd_direct)
             for (int l = 1; l < P.levels; ++l) score_level<G_BF16>(P, W, l);
 
-        // hashed slots that route nowhere: a direct reduction over the coordinates
-        for (int tt = 0; tt < W.ntok; ++tt)
-            for (int s0 = 0; s0 < k; s0 += 64) {
-                const int s = s0 + lane;
-                const int32_t cs = s < k ? W.idx[tt * k + s] : -1;
-                uint64_t todo = __ballot(s < k && cs >= d && W.route[tt * k + s] < 0);
-                while (todo) {
-                    const int b = __builtin_ctzll(todo);
-                    todo &= todo - 1;
-                    const uint32_t c = (uint32_t)rdlane(cs, b);
-                    float part = 0.f;
-                    for (int iota = lane; iota < d; iota += 64)
-                        part += signed_by_parity(g_at<G_BF16>(P, W, tt, iota), W.mask[iota] & c);
-                    const float sum = wave_sum(part);
-                    if (lane == 0) W.coef[tt * k + s0 + b] = P.rsd * sum;
-                }
-            }
+        // hashed slots that route nowhere (every hashed slot when the plan has
+        // many children per parent): direct reductions over the coordinates
+        direct_scores<G_BF16, NG>(P, W);
         wave_sync();
         if (add_gc) {
             for (int i = lane; i < W.ntok * k; i += 64) W.coef[i] += add_gc[t0 * k + i];
