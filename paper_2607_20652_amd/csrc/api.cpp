@@ -179,10 +179,12 @@ inline uint32_t row_parity(uint32_t m, uint32_t p) { return (uint32_t)__builtin_
 inline uint16_t pm_one(uint32_t neg) { return neg ? 0xBF80 : 0x3F80; }  // bf16 -1 / +1
 
 // Sign-bitmap words of index (v << 4g): bit b of word w is the sign at coordinate 32w + b.
+// Groups nt_groups .. kNtGroupsPadded - 1 are zero words (index nibbles there are 0),
+// so kernels may fold a fixed number of groups.
 void build_nibble_tables(const dpb_plan* plan, std::vector<uint32_t>* out)
 {
     const DevPlan& P = plan->dev;
-    out->assign((size_t)P.nt_groups * 16 * P.nchunk, 0);
+    out->assign((size_t)std::max(P.nt_groups, dpb::kNtGroupsPadded) * 16 * P.nchunk, 0);
     for (int g = 0; g < P.nt_groups; ++g)
         for (uint32_t v = 0; v < 16; ++v)
             for (int w = 0; w < P.nchunk; ++w) {

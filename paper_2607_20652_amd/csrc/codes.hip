@@ -571,7 +571,8 @@ __device__ __forceinline__ uint32_t unit_pair(uint32_t R)
 template <bool G_BF16, int NG>
 __device__ void direct_scores(const DevPlan& P, const Wave& W)
 {
-    const int k = P.k_tot, n = W.ntok * k, lane = W.lane, nchunk = P.nchunk, d = P.d, ng = P.nt_groups;
+    static_assert(NG <= kNtGroupsPadded, "nibble groups beyond the padded tables");
+    const int k = P.k_tot, n = W.ntok * k, lane = W.lane, nchunk = P.nchunk, d = P.d;
     int32_t* list = (int32_t*)W.score;   // 256 entries
     const uint64_t below = (1ull << lane) - 1;
     for (int w0 = 0; w0 < n; w0 += 256) {
@@ -594,17 +595,20 @@ __device__ void direct_scores(const DevPlan& P, const Wave& W)
             const uint32_t c = (uint32_t)W.idx[item];
             float acc0 = 0.f, acc1 = 0.f;
             // the nibble-table words of the next chunk are requested before
-            // this chunk is summed (groups past ng read a valid word and drop it)
-            uint32_t tw[NG];
+            // this chunk is summed (the device tables hold at least NG groups,
+            // zero words past nt_groups)
+            uint32_t toff[NG], tw[NG];
+#pragma unroll
+            for (int g = 0; g < NG; ++g) toff[g] = 4u * ((uint32_t)(g * nchunk * 16) + ((c >> (4 * g)) & 15u));
+            const unsigned char* ntb = (const unsigned char*)P.nt;   // byte offsets: 32-bit address arithmetic
             auto fetch_words = [&](int w) {
 #pragma unroll
-                for (int g = 0; g < NG; ++g)
-                    tw[g] = P.nt[(min(g, ng - 1) * nchunk + w) * 16 + ((c >> (4 * g)) & 15u)];
+                for (int g = 0; g < NG; ++g) tw[g] = *(const uint32_t*)(ntb + (toff[g] + (uint32_t)(w * 64)));
             };
             auto fold_words = [&]() {
                 uint32_t v = 0;
 #pragma unroll
-                for (int g = 0; g < NG; ++g) v ^= g < ng ? tw[g] : 0u;
+                for (int g = 0; g < NG; ++g) v ^= tw[g];
                 return v;
             };
             fetch_words(min(part, nchunk - 1));

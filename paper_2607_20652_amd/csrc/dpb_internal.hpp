@@ -45,7 +45,7 @@ struct DevPlan {
     int cws;                    // row stride of column bitmaps in LDS (odd, >= nchunk)
     int prow;                   // row stride (dwords) of bf16 activation pairs in LDS: dp/2 + 16
     int cpt_shift[kMaxLevels];  // log2 cpt[l]
-    const uint32_t* nt;         // [nt_groups][nchunk][16] sign-bitmap word w of (v << 4g)
+    const uint32_t* nt;         // [max(nt_groups, kNtGroupsPadded)][nchunk][16] sign-bitmap word w of (v << 4g)
     int fr_cap;                 // slots per table-decode chunk (multiple of 32, <= kFrMax)
     int pb_bytes;               // bytes per coordinate of the leaf parents' sign bits (1 or 2)
     // Scoring A fragments in the interleaved-halves coordinate order: lane L,
@@ -83,6 +83,7 @@ struct CodeLayout {
     unsigned idx, coef, route, par, alpha, claim, fri, frc, frv, frt, pb, y, pairs, cw, score, bytes;
 };
 
+constexpr int kNtGroupsPadded = 8;   // nibble-table groups present on the device (zero words past nt_groups)
 constexpr int kFrMax = 256;          // largest table-decode chunk
 constexpr int kClaimed = 1 << 29;    // route flag: the slot is decoded through its column
 
