@@ -500,7 +500,11 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
 //    below the previous key) takes over.
 constexpr int kWideCols = 128;     // (token, parent) columns of a GEMM workgroup
 constexpr int kWideList = 1024;    // collected keys per token
+constexpr int kSeg = 16;           // keys per lane segment (64 kSeg = kWideList)
+constexpr int kSegStride = kSeg + 1;
+static_assert(64 * kSeg == kWideList && kSeg < 32, "segments fill the list; counts fit five bits");
 constexpr int kWideThreads = 256;
+static_assert(kWideThreads % kWideCols == 0, "column bitmaps: whole columns per thread group");
 
 template <bool X_BF16, bool STD>
 __global__ __launch_bounds__(kWideThreads) void wide_level0_kernel(DevPlan P, const void* __restrict__ xin, int64_t T,
@@ -587,14 +591,18 @@ __global__ __launch_bounds__(kWideThreads) void wide_gemm_kernel(DevPlan P, int 
                 xf[tt * dp + iota] = (tt < nt_tok && iota < d) ? xs[(t0 + tb + tt) * d + iota] : 0.f;
         }
     }
-    // parents' sign bitmaps: one nibble-table word per 4-bit group of the index
-    for (int e = threadIdx.x; e < kWideCols * nchunk; e += kWideThreads) {
-        const int col = e / nchunk, w = e - col * nchunk, tt = col / KC, q = col - tt * KC;
+    // parents' sign bitmaps: one nibble-table word per 4-bit group of the index;
+    // lanes take consecutive columns of one word, so a table read touches one
+    // 64-byte row of the table
+    {
+        const int col = threadIdx.x & (kWideCols - 1), tt = col / KC, q = col - tt * KC;
         const int32_t p = (tt < nt_tok && q < KP) ? idx[(t0 + tb + tt) * P.k_tot + P.slot_base[l - 1] + q] : -1;
-        uint32_t word = 0;
-        if (p >= 0)
-            for (int g = 0; g < P.nt_groups; ++g) word ^= P.nt[(g * nchunk + w) * 16 + ((p >> (4 * g)) & 15)];
-        cw[col * P.cws + w] = word;
+        for (int w = threadIdx.x / kWideCols; w < nchunk; w += kWideThreads / kWideCols) {
+            uint32_t word = 0;
+            if (p >= 0)
+                for (int g = 0; g < P.nt_groups; ++g) word ^= P.nt[(g * nchunk + w) * 16 + ((p >> (4 * g)) & 15)];
+            cw[col * P.cws + w] = word;
+        }
     }
     __syncthreads();
 
@@ -773,68 +781,75 @@ __global__ __launch_bounds__(kWideThreads) void wide_select_kernel(DevPlan P, in
                                                                    int32_t* __restrict__ out_idx,
                                                                    float* __restrict__ out_coef)
 {
-    __shared__ uint64_t s_list[4][kWideList];
+    __shared__ uint64_t s_list[4][64 * kSegStride];
     __shared__ int32_t s_par[4][128];
     __shared__ uint32_t s_gen[256];
-    __shared__ int s_cnt[4];
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, x32 = (lane ^ 32) << 2;
     const int KP = P.active[l - 1], D = P.delta[l], K = P.active[l], n = KP * D, sb = P.slot_base[l];
     const int dsh = 31 - __builtin_clz((unsigned)D);
     for (int j = threadIdx.x; j < D; j += kWideThreads) s_gen[j] = P.gens[P.gens_off[l] + j];
     __syncthreads();
-    const int64_t tl = (int64_t)blockIdx.x * 4 + wave;   // chunk-relative token
+    // chunk-relative token (wave-uniform: scalar, so score addresses are 32-bit offsets)
+    const int64_t tl = __builtin_amdgcn_readfirstlane((int)blockIdx.x * 4 + wave);
     if (tl >= ntok) return;
     const int64_t t = t0 + tl;
     for (int q = lane; q < KP; q += 64) s_par[wave][q] = out_idx[t * P.k_tot + P.slot_base[l - 1] + q];
-    if (lane == 0) s_cnt[wave] = 0;
     wave_sync();
+    // live parent slots as a bit set (padding parents have no children)
+    uint64_t live[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int q = 64 * h + lane;
+        live[h] = __ballot(q < KP && s_par[wave][q] >= 0);
+    }
     const float* src = scores + tl * (int64_t)n;
 
-    // keys of this lane's candidates f = 64 e + lane, eight per round
-    constexpr int B = 8;
-    auto keys8 = [&](int e0, uint64_t (&k)[B]) {
-        float v[B];
-#pragma unroll
-        for (int b = 0; b < B; ++b) {
-            const int f = (e0 + b) * 64 + lane;
-            v[b] = f < n ? src[f] : 0.f;
-        }
-#pragma unroll
-        for (int b = 0; b < B; ++b) {
-            const int f = (e0 + b) * 64 + lane;
-            k[b] = 0ull;
-            if (f < n) {
-                const int32_t p = s_par[wave][f >> dsh];
-                if (p >= 0) {
-                    const uint32_t c = (uint32_t)p ^ s_gen[f & (D - 1)];
-                    float z = v[b];
-                    if constexpr (STD) {
-                        const float2 st = stats[c];
-                        z = (z - st.x) * st.y;
-                    }
-                    k[b] = make_key(z, c);
-                }
-            }
-        }
+    // candidate f is child s_gen[f mod D] of parent slot f / D
+    auto child_index = [&](int f) -> uint32_t { return (uint32_t)s_par[wave][f >> dsh] ^ s_gen[f & (D - 1)]; };
+    auto is_live = [&](int f) -> bool {
+        const int q = f >> dsh;
+        const uint64_t lw = q < 64 ? live[0] : live[1];
+        return f < n && ((lw >> (q & 63)) & 1ull);
     };
+    // standardized score of a live candidate
+    auto z_of = [&](int f, float v) -> float {
+        if constexpr (STD) {
+            const float2 st = stats[child_index(f)];
+            v = (v - st.x) * st.y;
+        }
+        return v;
+    };
+    // magnitude key |z| bits + 1, 0 for padding: distinct values mean distinct children
+    auto mkey = [](bool ok, float z) -> uint32_t { return ok ? (__float_as_uint(z) & 0x7FFFFFFFu) + 1u : 0u; };
+    // this lane's candidates are streamed from the workspace eight at a time
+    // (unconditional, clamped loads: one wait per round)
+    constexpr int B = 8;
     const int rounds = (n + 64 * B - 1) / (64 * B);
+    auto load_round = [&](int rd, float (&v)[B]) {
+#pragma unroll
+        for (int b = 0; b < B; ++b)
+            v[b] = *(const float*)((const char*)src + 4u * (uint32_t)min((rd * B + b) * 64 + lane, n - 1));
+    };
 
-    // threshold: the K-th largest distinct key among the lanes' top two keys
-    constexpr int M = 2;
-    uint64_t top[M] = {0ull, 0ull};
+    // threshold tau: the K-th largest distinct magnitude key among the lanes'
+    // top two.  At least K distinct children have mkey >= tau, so the top K
+    // distinct (|z|, index) keys are all among the candidates with mkey >= tau.
+    uint32_t top0 = 0u, top1 = 0u;
     for (int rd = 0; rd < rounds; ++rd) {
-        uint64_t k[B];
-        keys8(rd * B, k);
+        float v[B];
+        load_round(rd, v);
 #pragma unroll
         for (int b = 0; b < B; ++b) {
-            if (k[b] > top[0]) {
-                top[1] = top[0];
-                top[0] = k[b];
-            } else if (k[b] > top[1] && k[b] != top[0]) {
-                top[1] = k[b];
-            }
+            const int f = (rd * B + b) * 64 + lane;
+            const bool ok = is_live(f);
+            const uint32_t m = mkey(ok, ok ? z_of(f, v[b]) : 0.f);
+            const bool gt0 = m > top0, gt1 = m > top1 && m != top0;
+            top1 = gt0 ? top0 : (gt1 ? m : top1);
+            top0 = gt0 ? m : top0;
         }
     }
+    constexpr int M = 2;
+    uint64_t top[M] = {top0, top1};
     sort_desc<M, 6, false>(top, lane, x32);
     uint64_t prev = shfl_u64(top[M - 1], (lane + 63) & 63);
     if (lane == 0) prev = 0ull;
@@ -848,31 +863,56 @@ __global__ __launch_bounds__(kWideThreads) void wide_select_kernel(DevPlan P, in
     }
     int total = 0;
     int rank = wave_prefix5(cnt, lane, total);
-    uint64_t tau_l = 0ull;
+    uint32_t tau_l = 0u;
 #pragma unroll
     for (int r = 0; r < M; ++r) {
-        if (((kept >> r) & 1) && rank == K - 1) tau_l = top[r];
+        if (((kept >> r) & 1) && rank == K - 1) tau_l = (uint32_t)top[r];
         rank += (kept >> r) & 1;
     }
-    // one lane holds tau when at least K distinct keys were seen; else take every key
-    uint64_t tau = 1ull;
-    const uint64_t hb = __ballot(tau_l != 0ull);
-    if (hb) tau = shfl_u64(tau_l, __builtin_ctzll(hb));
+    // one lane holds tau when at least K distinct magnitudes were seen; else take every live candidate
+    uint32_t tau = 1u;
+    const uint64_t hb = __ballot(tau_l != 0u);
+    if (hb) tau = (uint32_t)__shfl((int)tau_l, __builtin_ctzll(hb), 64);
 
-    // collect the keys >= tau
+    // collect (f, z) of the candidates with mkey >= tau: each lane appends to
+    // its own segment of kSeg entries (every candidate is stored, at the
+    // lane's next free entry, so the pass has no branches and no cross-lane
+    // steps; entry kSeg takes what does not fit).  The segments are then
+    // packed into one list of full keys.  A lane with more than kSeg hits
+    // sends the token to the exact extraction below.
     uint64_t* lst = s_list[wave];
+    int mine_n = 0;
     for (int rd = 0; rd < rounds; ++rd) {
-        uint64_t k[B];
-        keys8(rd * B, k);
+        float v[B];
+        load_round(rd, v);
 #pragma unroll
-        for (int b = 0; b < B; ++b)
-            if (k[b] >= tau && k[b] != 0ull) {
-                const int pos = atomicAdd(&s_cnt[wave], 1);
-                if (pos < kWideList) lst[pos] = k[b];
-            }
+        for (int b = 0; b < B; ++b) {
+            const int f = (rd * B + b) * 64 + lane;
+            const bool ok = is_live(f);
+            const float z = ok ? z_of(f, v[b]) : 0.f;
+            lst[lane * kSegStride + min(mine_n, kSeg)] = ((uint64_t)(uint32_t)f << 32) | __float_as_uint(z);
+            mine_n += (int)(mkey(ok, z) >= tau);
+        }
     }
     wave_sync();
-    const int nl = s_cnt[wave];
+    int nl = kWideList + 1;
+    if (!__ballot(mine_n > kSeg)) {
+        uint64_t mine[kSeg];
+#pragma unroll
+        for (int j = 0; j < kSeg; ++j) {
+            mine[j] = 0ull;
+            if (j < mine_n) {
+                const uint64_t en = lst[lane * kSegStride + j];
+                mine[j] = make_key(__uint_as_float((uint32_t)en), child_index((int)(en >> 32)));
+            }
+        }
+        const int pre = wave_prefix5(mine_n, lane, nl);
+        wave_sync();
+#pragma unroll
+        for (int j = 0; j < kSeg; ++j)
+            if (j < mine_n) lst[pre + j] = mine[j];
+    }
+    wave_sync();
     int emitted;
     if (nl <= 64) emitted = wide_emit<1>(P, lst, nl, K, lane, x32, t, sb, out_idx, out_coef);
     else if (nl <= 128) emitted = wide_emit<2>(P, lst, nl, K, lane, x32, t, sb, out_idx, out_coef);
@@ -886,11 +926,15 @@ __global__ __launch_bounds__(kWideThreads) void wide_select_kernel(DevPlan P, in
         for (int r = 0; r < K; ++r) {
             uint64_t best = 0ull;
             for (int rd = 0; rd < rounds; ++rd) {
-                uint64_t k[B];
-                keys8(rd * B, k);
+                float v[B];
+                load_round(rd, v);
 #pragma unroll
-                for (int b = 0; b < B; ++b)
-                    if (k[b] < last && k[b] > best) best = k[b];
+                for (int b = 0; b < B; ++b) {
+                    const int f = (rd * B + b) * 64 + lane;
+                    const bool ok = is_live(f);
+                    const uint64_t k = ok ? make_key(z_of(f, v[b]), child_index(f)) : 0ull;
+                    best = (k < last && k > best) ? k : best;
+                }
             }
 #pragma unroll
             for (int off = 32; off > 0; off >>= 1) {

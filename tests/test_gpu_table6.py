@@ -116,3 +116,45 @@ def test_decode_and_bwd_match_oracle(name, T, out):
     rgc, rgx = oracle.decode_bwd(w.d, m, oi, g.double().numpy())
     compare_dense(gc.cpu().numpy(), rgc, TOL_F32)
     compare_dense(gx.float().cpu().numpy(), rgx, tol)
+
+
+@pytest.mark.parametrize("name,T", [("pt_small_2l", 60), ("pt_small_3l", 40)])
+def test_encode_std_matches_oracle(name, T):
+    """The wide encoder on standardized scores (random EMA statistics)."""
+    say(f"[t6 encode std] {name} T={T}")
+    plan = plan_for(name)
+    w, nb, dl, K, m, gens = setup(name)
+    N = 1 << nb[-1]
+    rng = np.random.default_rng(77 + w.index)
+    mu = (0.3 * rng.standard_normal(N)).astype(np.float32)
+    var = rng.uniform(0.3, 3.0, N).astype(np.float32)
+    r = (1.0 / np.sqrt(var.astype(np.float64) + 1e-6)).astype(np.float32)
+    stats = torch.from_numpy(np.stack([mu, r], axis=1)).contiguous().to(DEV)
+    x = inputs.activations(name, T)
+    idx, coef = dpb.encode_std(plan, x.to(DEV), stats)
+    torch.cuda.synchronize()
+    oi, oc, om, oo = oracle.encode_std(w.d, m, nb, K, dl, gens, x.double().numpy(), mu, r)
+    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32)
+    say(f"  {st}")
+    assert st["exempt_tokens"] <= max(2, 0.02 * T)
+
+
+def test_encode_zero_and_constant_rows():
+    """Degenerate rows: all-zero activations (every score 0, ties broken by
+    index) and a constant row, through the wide encoder's threshold and
+    fallback paths."""
+    name = "pt_small_2l"
+    say(f"[t6 encode degenerate] {name}")
+    plan = plan_for(name)
+    w, nb, dl, K, m, gens = setup(name)
+    x = inputs.activations(name, 8).clone()
+    x[0] = 0
+    x[3] = 0.5
+    x[5, : w.d // 2] = 0
+    idx, coef = dpb.encode(plan, x.to(DEV))
+    torch.cuda.synchronize()
+    oi, oc, om, oo = oracle.encode(w.d, m, nb, K, dl, gens, x.double().numpy())
+    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32)
+    say(f"  {st}")
+    assert np.array_equal(idx.cpu().numpy()[0], oi[0])
+    assert st["exempt_tokens"] <= 2
