@@ -86,7 +86,7 @@ dpb_status fill_plan(dpb_plan* plan, const Hierarchy& h, const uint32_t* gens, u
             const bool live = l >= 1 && l < L;
             P.gpad[l] = live ? (h.branching[l] + 31) / 32 * 32 : 0;
             P.gbits_off[l] = gb;
-            gb += (int64_t)P.gpad[l] * P.nchunk;
+            gb += (int64_t)P.gpad[l] * (P.nchunk | 1);   // rows at stride cws (set below)
         }
     }
     P.bwd_direct = 0;
@@ -274,7 +274,7 @@ void build_gen_bits(const dpb_plan* plan, std::vector<uint32_t>* out)
 {
     const DevPlan& P = plan->dev;
     int64_t total = 0;
-    for (int l = 1; l < P.levels; ++l) total += (int64_t)P.gpad[l] * P.nchunk;
+    for (int l = 1; l < P.levels; ++l) total += (int64_t)P.gpad[l] * P.cws;
     out->assign((size_t)std::max<int64_t>(total, 1), 0);
     for (int l = 1; l < P.levels; ++l) {
         const uint32_t* g = plan->gens_h.data() + P.gens_off[l];
@@ -285,7 +285,7 @@ void build_gen_bits(const dpb_plan* plan, std::vector<uint32_t>* out)
                     const int iota = 32 * c + b;
                     if (iota < P.d) word |= row_parity(plan->masks_h[iota], g[j]) << b;
                 }
-                (*out)[P.gbits_off[l] + (int64_t)j * P.nchunk + c] = word;
+                (*out)[P.gbits_off[l] + (int64_t)j * P.cws + c] = word;
             }
     }
 }

@@ -66,9 +66,10 @@ struct DevPlan {
     int gtab_shift[kMaxLevels];
     int gtab_total;             // entries over all levels (0: routing disabled)
     int gens_total;             // sum_l Delta_l
-    // Generator sign bitmaps: word (j, c) of level l at gbits_off[l] + j * nchunk + c
+    // Generator sign bitmaps: word (j, c) of level l at gbits_off[l] + j * cws + c
     // has bit b = sign of phi~_{g_j} at coordinate 32c + b (1: negative), for
-    // j < gpad[l] = Delta_l rounded up to 32 (rows past Delta_l are zero).
+    // j < gpad[l] = Delta_l rounded up to 32 (rows past Delta_l are zero; the
+    // row stride cws = nchunk | 1 is the LDS layout, so a level is one copy).
     const uint32_t* gbits;
     int64_t gbits_off[kMaxLevels];
     int gpad[kMaxLevels];

@@ -567,7 +567,8 @@ __global__ __launch_bounds__(kWideThreads) void wide_gemm_kernel(DevPlan P, int 
 {
     extern __shared__ __align__(16) unsigned char smem[];
     const int KP = P.active[l - 1], KC = P.cpt[l], D = P.delta[l], nchunk = P.nchunk, d = P.d, dp = P.dp;
-    const int TT = kWideCols / KC;
+    const int csh = P.cpt_shift[l];   // KC = 2^csh
+    const int TT = kWideCols >> csh;
     const int64_t tb = (int64_t)blockIdx.x * TT;
     const int nt_tok = (int)min((int64_t)TT, ntok - tb);
     uint32_t* s_gb = (uint32_t*)smem;   // row stride cws (odd): the 16 rows of a fragment on 16 banks
@@ -577,10 +578,10 @@ __global__ __launch_bounds__(kWideThreads) void wide_gemm_kernel(DevPlan P, int 
     uint32_t* cw = (uint32_t*)(p1 + align16u(TT * (X_BF16 ? P.prow : dp) * 4));
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
 
-    const uint32_t* gsrc = P.gbits + P.gbits_off[l];
-    for (int i = threadIdx.x; i < P.gpad[l] * nchunk; i += kWideThreads) {
-        const int row = i / nchunk;
-        s_gb[row * P.cws + (i - row * nchunk)] = gsrc[i];
+    {   // generator bitmaps: already in the LDS layout (row stride cws), 16-byte copies
+        const u32x4* gsrc = (const u32x4*)(P.gbits + P.gbits_off[l]);
+        u32x4* gdst = (u32x4*)s_gb;
+        for (int i = threadIdx.x; i < P.gpad[l] * P.cws / 4; i += kWideThreads) gdst[i] = gsrc[i];
     }
     for (int tt = wave; tt < TT; tt += 4) {
         if constexpr (X_BF16) {
@@ -595,7 +596,7 @@ __global__ __launch_bounds__(kWideThreads) void wide_gemm_kernel(DevPlan P, int 
     // lanes take consecutive columns of one word, so a table read touches one
     // 64-byte row of the table
     {
-        const int col = threadIdx.x & (kWideCols - 1), tt = col / KC, q = col - tt * KC;
+        const int col = threadIdx.x & (kWideCols - 1), tt = col >> csh, q = col & (KC - 1);
         const int32_t p = (tt < nt_tok && q < KP) ? idx[(t0 + tb + tt) * P.k_tot + P.slot_base[l - 1] + q] : -1;
         for (int w = threadIdx.x / kWideCols; w < nchunk; w += kWideThreads / kWideCols) {
             uint32_t word = 0;
@@ -617,7 +618,7 @@ __global__ __launch_bounds__(kWideThreads) void wide_gemm_kernel(DevPlan P, int 
 #pragma unroll
     for (int n = 0; n < 4; ++n) {
         bcol[n] = wc * 64 + n * 16 + c16;
-        btok[n] = bcol[n] / KC;
+        btok[n] = bcol[n] >> csh;
     }
     // the LDS words of chunk c + 1 are requested before chunk c is computed
     // (two register sets, used in turn)
@@ -707,17 +708,17 @@ __global__ __launch_bounds__(kWideThreads) void wide_gemm_kernel(DevPlan P, int 
         if (c + 1 < nchunk) compute(c + 1, w1);
     }
     // scores (times 1/sqrt d) of the live (token, parent) columns and generator rows
+    const bool all_rows = 32 * MT == D;   // else rows from D on are padding
 #pragma unroll
     for (int n = 0; n < 4; ++n) {
-        const int col = wc * 64 + n * 16 + c16, tt = col / KC, q = col - tt * KC;
+        const int col = wc * 64 + n * 16 + c16, tt = col >> csh, q = col & (KC - 1);
         if (tt >= nt_tok || q >= KP) continue;
-        float* dst = scores + ((tb + tt) * KP + q) * D;
+        float* dst = scores + ((tb + tt) * KP + q) * D + wr * 16 * MT + 4 * kq;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-            const int j0 = wr * 16 * MT + 16 * mt + 4 * kq;
-            if (j0 < D) {
+            if (all_rows || wr * 16 * MT + 16 * mt + 4 * kq < D) {
                 const f32x4 v = acc[mt][n];
-                *(float4*)(dst + j0) = make_float4(v[0] * P.rsd, v[1] * P.rsd, v[2] * P.rsd, v[3] * P.rsd);
+                *(float4*)(dst + 16 * mt) = make_float4(v[0] * P.rsd, v[1] * P.rsd, v[2] * P.rsd, v[3] * P.rsd);
             }
         }
     }
