@@ -548,22 +548,51 @@ __global__ __launch_bounds__(kWideThreads) void wide_level0_kernel(DevPlan P, co
     }
 }
 
+// Exclusive prefix over the wave of per-lane counts below 2^5.
+__device__ __forceinline__ int wave_prefix5(int cnt, int lane, int& total)
+{
+    const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+    int before = 0;
+    total = 0;
+#pragma unroll
+    for (int b = 0; b < 5; ++b) {
+        const uint64_t m = __ballot((cnt >> b) & 1);
+        before += (int)__popcll(m & below) << b;
+        total += (int)__popcll(m) << b;
+    }
+    return before;
+}
+
 // LDS of a GEMM workgroup: generator bitmaps, the tokens' rows, column bitmaps.
 __host__ __device__ inline unsigned wide_gemm_lds(const DevPlan& P, int l, bool x_bf16)
 {
     const int TT = kWideCols / P.cpt[l];
     return align16u(P.gpad[l] * P.cws * 4) + align16u(TT * (x_bf16 ? P.prow : P.dp) * 4) +
-           align16u(kWideCols * P.cws * 4);
+           align16u(kWideCols * P.cws * 4) + align16u(kWideCols * 4);
+}
+
+// Whether level l's GEMM selects in its epilogue: 16 to 64 parent columns per
+// token (whole tokens per 64-column wave tile) and a token's score region can
+// hold the kWideList (candidate, z) entries.
+__host__ __device__ inline bool wide_fused(const DevPlan& P, int l)
+{
+    return P.cpt[l] >= 16 && P.cpt[l] <= 64 && P.active[l - 1] * P.delta[l] >= 2 * kWideList;
 }
 
 // Scores of tokens [t0 + TT blockIdx.x, ...) of a chunk of ntok tokens at level
 // l into scores[(t - t0) K_{l-1} + q][j] (t0-relative tokens).  MT = 16-row
 // tiles per wave: waves (wr, wc) cover rows 16 MT wr .. and columns 64 wc ..
-template <bool X_BF16, int MT>
-__global__ __launch_bounds__(kWideThreads) void wide_gemm_kernel(DevPlan P, int l, const void* __restrict__ xin,
+// FUSE: instead of all scores, each token's region receives the (candidate,
+// z) entries at or above a threshold tau computed here from the lanes' top
+// two distinct magnitude keys (the selection's first pass), and counts[t - t0]
+// their number; a token with more than kWideList entries gets its full scores
+// and its count says so.
+template <bool X_BF16, int MT, bool FUSE>
+__global__ __launch_bounds__(kWideThreads) __attribute__((amdgpu_waves_per_eu(2))) void wide_gemm_kernel(DevPlan P, int l, const void* __restrict__ xin,
                                                                  int64_t t0, int64_t ntok,
                                                                  const int32_t* __restrict__ idx,
-                                                                 float* __restrict__ scores)
+                                                                 float* __restrict__ scores,
+                                                                 int* __restrict__ counts)
 {
     extern __shared__ __align__(16) unsigned char smem[];
     const int KP = P.active[l - 1], KC = P.cpt[l], D = P.delta[l], nchunk = P.nchunk, d = P.d, dp = P.dp;
@@ -576,6 +605,7 @@ __global__ __launch_bounds__(kWideThreads) void wide_gemm_kernel(DevPlan P, int 
     uint32_t* pairs = (uint32_t*)p1;
     float* xf = (float*)p1;
     uint32_t* cw = (uint32_t*)(p1 + align16u(TT * (X_BF16 ? P.prow : dp) * 4));
+    int32_t* s_pidx = (int32_t*)((unsigned char*)cw + align16u(kWideCols * P.cws * 4));   // parent of each column
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
 
     {   // generator bitmaps: already in the LDS layout (row stride cws), 16-byte copies
@@ -598,6 +628,7 @@ __global__ __launch_bounds__(kWideThreads) void wide_gemm_kernel(DevPlan P, int 
     {
         const int col = threadIdx.x & (kWideCols - 1), tt = col >> csh, q = col & (KC - 1);
         const int32_t p = (tt < nt_tok && q < KP) ? idx[(t0 + tb + tt) * P.k_tot + P.slot_base[l - 1] + q] : -1;
+        if (threadIdx.x < kWideCols) s_pidx[col] = p;
         for (int w = threadIdx.x / kWideCols; w < nchunk; w += kWideThreads / kWideCols) {
             uint32_t word = 0;
             if (p >= 0)
@@ -709,10 +740,9 @@ __global__ __launch_bounds__(kWideThreads) void wide_gemm_kernel(DevPlan P, int 
     }
     // scores (times 1/sqrt d) of the live (token, parent) columns and generator rows
     const bool all_rows = 32 * MT == D;   // else rows from D on are padding
-#pragma unroll
-    for (int n = 0; n < 4; ++n) {
+    auto store_scores = [&](int n) {
         const int col = wc * 64 + n * 16 + c16, tt = col >> csh, q = col & (KC - 1);
-        if (tt >= nt_tok || q >= KP) continue;
+        if (tt >= nt_tok || q >= KP) return;
         float* dst = scores + ((tb + tt) * KP + q) * D + wr * 16 * MT + 4 * kq;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
@@ -721,22 +751,101 @@ __global__ __launch_bounds__(kWideThreads) void wide_gemm_kernel(DevPlan P, int 
                 *(float4*)(dst + 16 * mt) = make_float4(v[0] * P.rsd, v[1] * P.rsd, v[2] * P.rsd, v[3] * P.rsd);
             }
         }
-    }
-}
-
-// Exclusive prefix over the wave of per-lane counts below 2^5.
-__device__ __forceinline__ int wave_prefix5(int cnt, int lane, int& total)
-{
-    const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
-    int before = 0;
-    total = 0;
+    };
+    if constexpr (!FUSE) {
 #pragma unroll
-    for (int b = 0; b < 5; ++b) {
-        const uint64_t m = __ballot((cnt >> b) & 1);
-        before += (int)__popcll(m & below) << b;
-        total += (int)__popcll(m) << b;
+        for (int n = 0; n < 4; ++n) store_scores(n);
+    } else {
+        const int K = P.active[l], x32 = (lane ^ 32) << 2;
+        const int tpw = 64 >> csh;   // tokens in a wave's 64 columns: 4, 2 or 1
+        int32_t pid[4];
+#pragma unroll
+        for (int n = 0; n < 4; ++n) pid[n] = s_pidx[bcol[n]];
+        __syncthreads();   // the staging LDS is free from here on
+        uint32_t* s_top = (uint32_t*)smem;             // [TT][2 row halves][64 lanes][2]
+        uint32_t* s_tau = s_top + TT * 256;           // [TT]
+        int* s_cnt = (int*)(s_tau + TT);              // [TT]
+        // magnitude key of value i of tile (mt, n): |z| bits + 1, 0 for padding
+        auto mk = [&](int mt, int n, int i) -> uint32_t {
+            const bool ok = pid[n] >= 0 && (all_rows || wr * 16 * MT + 16 * mt + 4 * kq + i < D);
+            return ok ? (__float_as_uint(acc[mt][n][i] * P.rsd) & 0x7FFFFFFFu) + 1u : 0u;
+        };
+        // each lane's two largest distinct keys per token of this wave
+        for (int u = 0; u < tpw; ++u) {
+            uint32_t top0 = 0u, top1 = 0u;
+#pragma unroll
+            for (int n = 0; n < 4; ++n) {
+                if (((n * 16) >> csh) != u) continue;
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const uint32_t m = mk(mt, n, i);
+                        const bool gt0 = m > top0, gt1 = m > top1 && m != top0;
+                        top1 = gt0 ? top0 : (gt1 ? m : top1);
+                        top0 = gt0 ? m : top0;
+                    }
+            }
+            const int tt = ((wc * 64) >> csh) + u;
+            s_top[((tt * 2 + wr) * 64 + lane) * 2] = top0;
+            s_top[((tt * 2 + wr) * 64 + lane) * 2 + 1] = top1;
+        }
+        if (threadIdx.x < TT) s_cnt[threadIdx.x] = 0;
+        __syncthreads();
+        // tau of each token: the K-th largest distinct key among its 256 lane tops
+        for (int tt = wave; tt < TT; tt += 4) {
+            uint64_t v[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[r] = s_top[tt * 256 + lane * 4 + r];
+            sort_desc<4, 6, false>(v, lane, x32);
+            uint64_t prev = shfl_u64(v[3], (lane + 63) & 63);
+            if (lane == 0) prev = 0ull;
+            int kept = 0, cnt = 0;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const bool kk = v[r] != 0ull && v[r] != prev;
+                kept |= (int)kk << r;
+                cnt += (int)kk;
+                prev = v[r];
+            }
+            int total = 0;
+            int rank = wave_prefix5(cnt, lane, total);
+            uint32_t tau_l = 0u;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                if (((kept >> r) & 1) && rank == K - 1) tau_l = (uint32_t)v[r];
+                rank += (kept >> r) & 1;
+            }
+            const uint64_t hb = __ballot(tau_l != 0u);
+            const uint32_t tau = hb ? (uint32_t)__shfl((int)tau_l, __builtin_ctzll(hb), 64) : 1u;
+            if (lane == 0) s_tau[tt] = tau;
+        }
+        __syncthreads();
+        // list the candidates at or above tau in the token's region
+#pragma unroll
+        for (int n = 0; n < 4; ++n) {
+            const int tt = bcol[n] >> csh, q = bcol[n] & (KC - 1);
+            const uint32_t tau = s_tau[tt];
+            uint64_t* lst = (uint64_t*)(scores + (tb + tt) * KP * D);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (mk(mt, n, i) >= tau) {
+                        const int pos = atomicAdd(&s_cnt[tt], 1);
+                        if (pos < kWideList) {
+                            const uint32_t f = (uint32_t)(q * D + wr * 16 * MT + 16 * mt + 4 * kq + i);
+                            lst[pos] = ((uint64_t)f << 32) | __float_as_uint(acc[mt][n][i] * P.rsd);
+                        }
+                    }
+        }
+        __syncthreads();
+        // a token with too many entries gets its full scores instead
+#pragma unroll
+        for (int n = 0; n < 4; ++n)
+            if (s_cnt[bcol[n] >> csh] > kWideList) store_scores(n);
+        if (threadIdx.x < nt_tok) counts[tb + threadIdx.x] = s_cnt[threadIdx.x];
     }
-    return before;
 }
 
 // Sorts the n <= 64 R keys of the list (0-padded) and emits the first K
@@ -775,9 +884,14 @@ __device__ __forceinline__ int wide_emit(const DevPlan& P, const uint64_t* lst, 
     return total;
 }
 
+// counts (plain scores only): the GEMM listed counts[t - t0] <= kWideList
+// (candidate, z) entries at or above the threshold in the token's region; more
+// means the region holds the full scores.  Without counts the region always
+// holds the full scores.
 template <bool STD>
 __global__ __launch_bounds__(kWideThreads) void wide_select_kernel(DevPlan P, int l, int64_t t0, int64_t ntok,
                                                                    const float* __restrict__ scores,
+                                                                   const int* __restrict__ counts,
                                                                    const float2* __restrict__ stats,
                                                                    int32_t* __restrict__ out_idx,
                                                                    float* __restrict__ out_coef)
@@ -832,88 +946,100 @@ __global__ __launch_bounds__(kWideThreads) void wide_select_kernel(DevPlan P, in
             v[b] = *(const float*)((const char*)src + 4u * (uint32_t)min((rd * B + b) * 64 + lane, n - 1));
     };
 
-    // threshold tau: the K-th largest distinct magnitude key among the lanes'
-    // top two.  At least K distinct children have mkey >= tau, so the top K
-    // distinct (|z|, index) keys are all among the candidates with mkey >= tau.
-    uint32_t top0 = 0u, top1 = 0u;
-    for (int rd = 0; rd < rounds; ++rd) {
-        float v[B];
-        load_round(rd, v);
-#pragma unroll
-        for (int b = 0; b < B; ++b) {
-            const int f = (rd * B + b) * 64 + lane;
-            const bool ok = is_live(f);
-            const uint32_t m = mkey(ok, ok ? z_of(f, v[b]) : 0.f);
-            const bool gt0 = m > top0, gt1 = m > top1 && m != top0;
-            top1 = gt0 ? top0 : (gt1 ? m : top1);
-            top0 = gt0 ? m : top0;
-        }
-    }
-    constexpr int M = 2;
-    uint64_t top[M] = {top0, top1};
-    sort_desc<M, 6, false>(top, lane, x32);
-    uint64_t prev = shfl_u64(top[M - 1], (lane + 63) & 63);
-    if (lane == 0) prev = 0ull;
-    int kept = 0, cnt = 0;
-#pragma unroll
-    for (int r = 0; r < M; ++r) {
-        const bool kk = top[r] != 0ull && top[r] != prev;
-        kept |= (int)kk << r;
-        cnt += (int)kk;
-        prev = top[r];
-    }
-    int total = 0;
-    int rank = wave_prefix5(cnt, lane, total);
-    uint32_t tau_l = 0u;
-#pragma unroll
-    for (int r = 0; r < M; ++r) {
-        if (((kept >> r) & 1) && rank == K - 1) tau_l = (uint32_t)top[r];
-        rank += (kept >> r) & 1;
-    }
-    // one lane holds tau when at least K distinct magnitudes were seen; else take every live candidate
-    uint32_t tau = 1u;
-    const uint64_t hb = __ballot(tau_l != 0u);
-    if (hb) tau = (uint32_t)__shfl((int)tau_l, __builtin_ctzll(hb), 64);
-
-    // collect (f, z) of the candidates with mkey >= tau: each lane appends to
-    // its own segment of kSeg entries (every candidate is stored, at the
-    // lane's next free entry, so the pass has no branches and no cross-lane
-    // steps; entry kSeg takes what does not fit).  The segments are then
-    // packed into one list of full keys.  A lane with more than kSeg hits
-    // sends the token to the exact extraction below.
     uint64_t* lst = s_list[wave];
-    int mine_n = 0;
-    for (int rd = 0; rd < rounds; ++rd) {
-        float v[B];
-        load_round(rd, v);
-#pragma unroll
-        for (int b = 0; b < B; ++b) {
-            const int f = (rd * B + b) * 64 + lane;
-            const bool ok = is_live(f);
-            const float z = ok ? z_of(f, v[b]) : 0.f;
-            lst[lane * kSegStride + min(mine_n, kSeg)] = ((uint64_t)(uint32_t)f << 32) | __float_as_uint(z);
-            mine_n += (int)(mkey(ok, z) >= tau);
-        }
-    }
-    wave_sync();
     int nl = kWideList + 1;
-    if (!__ballot(mine_n > kSeg)) {
-        uint64_t mine[kSeg];
+    const int listed = counts ? counts[tl] : kWideList + 1;
+    if (listed <= kWideList) {
+        // the GEMM's list: full keys of its entries
+        const uint64_t* ent = (const uint64_t*)src;
+        for (int e = lane; e < listed; e += 64) {
+            const uint64_t en = ent[e];
+            lst[e] = make_key(__uint_as_float((uint32_t)en), child_index((int)(en >> 32)));
+        }
+        wave_sync();
+        nl = listed;
+    } else {
+        // threshold tau: the K-th largest distinct magnitude key among the lanes'
+        // top two.  At least K distinct children have mkey >= tau, so the top K
+        // distinct (|z|, index) keys are all among the candidates with mkey >= tau.
+        uint32_t top0 = 0u, top1 = 0u;
+        for (int rd = 0; rd < rounds; ++rd) {
+            float v[B];
+            load_round(rd, v);
 #pragma unroll
-        for (int j = 0; j < kSeg; ++j) {
-            mine[j] = 0ull;
-            if (j < mine_n) {
-                const uint64_t en = lst[lane * kSegStride + j];
-                mine[j] = make_key(__uint_as_float((uint32_t)en), child_index((int)(en >> 32)));
+            for (int b = 0; b < B; ++b) {
+                const int f = (rd * B + b) * 64 + lane;
+                const bool ok = is_live(f);
+                const uint32_t m = mkey(ok, ok ? z_of(f, v[b]) : 0.f);
+                const bool gt0 = m > top0, gt1 = m > top1 && m != top0;
+                top1 = gt0 ? top0 : (gt1 ? m : top1);
+                top0 = gt0 ? m : top0;
             }
         }
-        const int pre = wave_prefix5(mine_n, lane, nl);
-        wave_sync();
+        constexpr int M = 2;
+        uint64_t top[M] = {top0, top1};
+        sort_desc<M, 6, false>(top, lane, x32);
+        uint64_t prev = shfl_u64(top[M - 1], (lane + 63) & 63);
+        if (lane == 0) prev = 0ull;
+        int kept = 0, cnt = 0;
 #pragma unroll
-        for (int j = 0; j < kSeg; ++j)
-            if (j < mine_n) lst[pre + j] = mine[j];
+        for (int r = 0; r < M; ++r) {
+            const bool kk = top[r] != 0ull && top[r] != prev;
+            kept |= (int)kk << r;
+            cnt += (int)kk;
+            prev = top[r];
+        }
+        int total = 0;
+        int rank = wave_prefix5(cnt, lane, total);
+        uint32_t tau_l = 0u;
+#pragma unroll
+        for (int r = 0; r < M; ++r) {
+            if (((kept >> r) & 1) && rank == K - 1) tau_l = (uint32_t)top[r];
+            rank += (kept >> r) & 1;
+        }
+        // one lane holds tau when at least K distinct magnitudes were seen; else take every live candidate
+        uint32_t tau = 1u;
+        const uint64_t hb = __ballot(tau_l != 0u);
+        if (hb) tau = (uint32_t)__shfl((int)tau_l, __builtin_ctzll(hb), 64);
+
+        // collect (f, z) of the candidates with mkey >= tau: each lane appends to
+        // its own segment of kSeg entries (every candidate is stored, at the
+        // lane's next free entry, so the pass has no branches and no cross-lane
+        // steps; entry kSeg takes what does not fit).  The segments are then
+        // packed into one list of full keys.  A lane with more than kSeg hits
+        // sends the token to the exact extraction below.
+        int mine_n = 0;
+        for (int rd = 0; rd < rounds; ++rd) {
+            float v[B];
+            load_round(rd, v);
+#pragma unroll
+            for (int b = 0; b < B; ++b) {
+                const int f = (rd * B + b) * 64 + lane;
+                const bool ok = is_live(f);
+                const float z = ok ? z_of(f, v[b]) : 0.f;
+                lst[lane * kSegStride + min(mine_n, kSeg)] = ((uint64_t)(uint32_t)f << 32) | __float_as_uint(z);
+                mine_n += (int)(mkey(ok, z) >= tau);
+            }
+        }
+        wave_sync();
+        if (!__ballot(mine_n > kSeg)) {
+            uint64_t mine[kSeg];
+#pragma unroll
+            for (int j = 0; j < kSeg; ++j) {
+                mine[j] = 0ull;
+                if (j < mine_n) {
+                    const uint64_t en = lst[lane * kSegStride + j];
+                    mine[j] = make_key(__uint_as_float((uint32_t)en), child_index((int)(en >> 32)));
+                }
+            }
+            const int pre = wave_prefix5(mine_n, lane, nl);
+            wave_sync();
+#pragma unroll
+            for (int j = 0; j < kSeg; ++j)
+                if (j < mine_n) lst[pre + j] = mine[j];
+        }
+        wave_sync();
     }
-    wave_sync();
     int emitted;
     if (nl <= 64) emitted = wide_emit<1>(P, lst, nl, K, lane, x32, t, sb, out_idx, out_coef);
     else if (nl <= 128) emitted = wide_emit<2>(P, lst, nl, K, lane, x32, t, sb, out_idx, out_coef);
@@ -1055,15 +1181,23 @@ bool encode_wide_supported(const DevPlan& P, bool x_bf16)
     return true;
 }
 
+// Workspace: per chunk token, the scores (or the GEMM's list) of its
+// candidates, then one count per chunk token.
+static size_t wide_scores_bytes(const DevPlan& P, int64_t ch)
+{
+    return ((size_t)ch * wide_max_cands(P) * 4 + 255) & ~(size_t)255;
+}
+
 size_t encode_wide_workspace_bytes(const DevPlan& P, int64_t T)
 {
     const int64_t ch = std::min<int64_t>(T, kWideChunkTokens);
-    return ch > 0 ? ((size_t)ch * wide_max_cands(P) * 4 + 255) & ~(size_t)255 : 0;
+    return ch > 0 ? wide_scores_bytes(P, ch) + (((size_t)ch * 4 + 255) & ~(size_t)255) : 0;
 }
 
-template <bool XB>
+// counts != nullptr: the fused epilogue (lists instead of scores).
+template <bool XB, bool FUSE>
 static void launch_wide_gemm(const DevPlan& P, int l, const void* x, int64_t c0, int64_t nc, const int32_t* idx,
-                             float* scores, hipStream_t stream)
+                             float* scores, int* counts, hipStream_t stream)
 {
     const int TT = kWideCols / P.cpt[l];
     const dim3 grid((unsigned)((nc + TT - 1) / TT));
@@ -1071,9 +1205,9 @@ static void launch_wide_gemm(const DevPlan& P, int l, const void* x, int64_t c0,
     const int MT = std::max(32, P.delta[l]) / 32;
 #define DPB_WG(M)                                                                                             \
     do {                                                                                                      \
-        allow_lds(wide_gemm_kernel<XB, M>, lds);                                                              \
-        hipLaunchKernelGGL((wide_gemm_kernel<XB, M>), grid, dim3(kWideThreads), lds, stream, P, l, x, c0, nc, idx, \
-                           scores);                                                                           \
+        allow_lds(wide_gemm_kernel<XB, M, FUSE>, lds);                                                        \
+        hipLaunchKernelGGL((wide_gemm_kernel<XB, M, FUSE>), grid, dim3(kWideThreads), lds, stream, P, l, x, c0, nc, \
+                           idx, scores, counts);                                                              \
     } while (0)
     if (MT == 1) DPB_WG(1);
     else if (MT == 2) DPB_WG(2);
@@ -1084,11 +1218,11 @@ static void launch_wide_gemm(const DevPlan& P, int l, const void* x, int64_t c0,
 
 template <bool STD>
 static void launch_wide_select(const DevPlan& P, int l, int64_t c0, int64_t nc, const float* scores,
-                               const float2* st, int32_t* idx, float* coef, hipStream_t stream)
+                               const int* counts, const float2* st, int32_t* idx, float* coef, hipStream_t stream)
 {
     const dim3 grid((unsigned)((nc + 3) / 4));
-    hipLaunchKernelGGL((wide_select_kernel<STD>), grid, dim3(kWideThreads), 0, stream, P, l, c0, nc, scores, st, idx,
-                       coef);
+    hipLaunchKernelGGL((wide_select_kernel<STD>), grid, dim3(kWideThreads), 0, stream, P, l, c0, nc, scores, counts,
+                       st, idx, coef);
 }
 
 hipError_t launch_encode_wide(const DevPlan& P, const void* x, bool x_bf16, int64_t T, const float* stats,
@@ -1115,13 +1249,18 @@ hipError_t launch_encode_wide(const DevPlan& P, const void* x, bool x_bf16, int6
 #undef DPB_W0
     }
     float* scores = (float*)ws;
+    int* counts = (int*)((char*)ws + wide_scores_bytes(P, std::min<int64_t>(T, kWideChunkTokens)));
     for (int64_t c0 = 0; c0 < T; c0 += kWideChunkTokens) {
         const int64_t nc = std::min<int64_t>(kWideChunkTokens, T - c0);
         for (int l = 1; l < P.levels; ++l) {
-            if (x_bf16) launch_wide_gemm<true>(P, l, x, c0, nc, idx, scores, stream);
-            else launch_wide_gemm<false>(P, l, x, c0, nc, idx, scores, stream);
-            if (st) launch_wide_select<true>(P, l, c0, nc, scores, st, idx, coef, stream);
-            else launch_wide_select<false>(P, l, c0, nc, scores, st, idx, coef, stream);
+            // standardized scores keep the two-pass selection (z needs each candidate's statistics)
+            const bool fuse = !st && wide_fused(P, l);
+            if (x_bf16 && fuse) launch_wide_gemm<true, true>(P, l, x, c0, nc, idx, scores, counts, stream);
+            else if (x_bf16) launch_wide_gemm<true, false>(P, l, x, c0, nc, idx, scores, nullptr, stream);
+            else if (fuse) launch_wide_gemm<false, true>(P, l, x, c0, nc, idx, scores, counts, stream);
+            else launch_wide_gemm<false, false>(P, l, x, c0, nc, idx, scores, nullptr, stream);
+            if (st) launch_wide_select<true>(P, l, c0, nc, scores, nullptr, st, idx, coef, stream);
+            else launch_wide_select<false>(P, l, c0, nc, scores, fuse ? counts : nullptr, st, idx, coef, stream);
         }
     }
     return hipGetLastError();
