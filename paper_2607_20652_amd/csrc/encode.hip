@@ -629,11 +629,19 @@ __global__ __launch_bounds__(kWideThreads) __attribute__((amdgpu_waves_per_eu(2)
         const int col = threadIdx.x & (kWideCols - 1), tt = col >> csh, q = col & (KC - 1);
         const int32_t p = (tt < nt_tok && q < KP) ? idx[(t0 + tb + tt) * P.k_tot + P.slot_base[l - 1] + q] : -1;
         if (threadIdx.x < kWideCols) s_pidx[col] = p;
+        // all kNtGroupsPadded groups are read (zero words past nt_groups): the
+        // loads of a word are independent and wait once
+        const uint32_t pu = p >= 0 ? (uint32_t)p : 0u;
+        uint32_t toff[kNtGroupsPadded];
+#pragma unroll
+        for (int g = 0; g < kNtGroupsPadded; ++g) toff[g] = 4u * ((uint32_t)(g * nchunk * 16) + ((pu >> (4 * g)) & 15u));
+        const unsigned char* ntb = (const unsigned char*)P.nt;
+#pragma unroll 2
         for (int w = threadIdx.x / kWideCols; w < nchunk; w += kWideThreads / kWideCols) {
             uint32_t word = 0;
-            if (p >= 0)
-                for (int g = 0; g < P.nt_groups; ++g) word ^= P.nt[(g * nchunk + w) * 16 + ((p >> (4 * g)) & 15)];
-            cw[col * P.cws + w] = word;
+#pragma unroll
+            for (int g = 0; g < kNtGroupsPadded; ++g) word ^= *(const uint32_t*)(ntb + toff[g] + (uint32_t)w * 64u);
+            cw[col * P.cws + w] = p >= 0 ? word : 0u;
         }
     }
     __syncthreads();
