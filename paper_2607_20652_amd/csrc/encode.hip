@@ -505,6 +505,7 @@ constexpr int kSegStride = kSeg + 1;
 static_assert(64 * kSeg == kWideList && kSeg < 32, "segments fill the list; counts fit five bits");
 constexpr int kWideThreads = 256;
 static_assert(kWideThreads % kWideCols == 0, "column bitmaps: whole columns per thread group");
+// (the fused epilogue keeps a lane's hits of one column tile, 4 MT <= 32 values, in one word)
 
 template <bool X_BF16, bool STD>
 __global__ __launch_bounds__(kWideThreads) void wide_level0_kernel(DevPlan P, const void* __restrict__ xin, int64_t T,
@@ -548,20 +549,22 @@ __global__ __launch_bounds__(kWideThreads) void wide_level0_kernel(DevPlan P, co
     }
 }
 
-// Exclusive prefix over the wave of per-lane counts below 2^5.
-__device__ __forceinline__ int wave_prefix5(int cnt, int lane, int& total)
+// Exclusive prefix over the wave of per-lane counts below 2^BITS.
+template <int BITS>
+__device__ __forceinline__ int wave_prefix(int cnt, int lane, int& total)
 {
     const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
     int before = 0;
     total = 0;
 #pragma unroll
-    for (int b = 0; b < 5; ++b) {
+    for (int b = 0; b < BITS; ++b) {
         const uint64_t m = __ballot((cnt >> b) & 1);
         before += (int)__popcll(m & below) << b;
         total += (int)__popcll(m) << b;
     }
     return before;
 }
+__device__ __forceinline__ int wave_prefix5(int cnt, int lane, int& total) { return wave_prefix<5>(cnt, lane, total); }
 
 // LDS of a GEMM workgroup: generator bitmaps, the tokens' rows, column bitmaps.
 __host__ __device__ inline unsigned wide_gemm_lds(const DevPlan& P, int l, bool x_bf16)
@@ -775,8 +778,9 @@ __global__ __launch_bounds__(kWideThreads) __attribute__((amdgpu_waves_per_eu(2)
         int* s_cnt = (int*)(s_tau + TT);              // [TT]
         // magnitude key of value i of tile (mt, n): |z| bits + 1, 0 for padding
         auto mk = [&](int mt, int n, int i) -> uint32_t {
-            const bool ok = pid[n] >= 0 && (all_rows || wr * 16 * MT + 16 * mt + 4 * kq + i < D);
-            return ok ? (__float_as_uint(acc[mt][n][i] * P.rsd) & 0x7FFFFFFFu) + 1u : 0u;
+            const bool ok = (pid[n] >= 0) & (all_rows | (wr * 16 * MT + 16 * mt + 4 * kq + i < D));
+            const uint32_t m = (__float_as_uint(acc[mt][n][i] * P.rsd) & 0x7FFFFFFFu) + 1u;
+            return ok ? m : 0u;
         };
         // each lane's two largest distinct keys per token of this wave
         for (int u = 0; u < tpw; ++u) {
@@ -802,16 +806,16 @@ __global__ __launch_bounds__(kWideThreads) __attribute__((amdgpu_waves_per_eu(2)
         __syncthreads();
         // tau of each token: the K-th largest distinct key among its 256 lane tops
         for (int tt = wave; tt < TT; tt += 4) {
-            uint64_t v[4];
+            uint32_t v[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r) v[r] = s_top[tt * 256 + lane * 4 + r];
             sort_desc<4, 6, false>(v, lane, x32);
-            uint64_t prev = shfl_u64(v[3], (lane + 63) & 63);
-            if (lane == 0) prev = 0ull;
+            uint32_t prev = (uint32_t)__shfl((int)v[3], (lane + 63) & 63, 64);
+            if (lane == 0) prev = 0u;
             int kept = 0, cnt = 0;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const bool kk = v[r] != 0ull && v[r] != prev;
+                const bool kk = v[r] != 0u && v[r] != prev;
                 kept |= (int)kk << r;
                 cnt += (int)kk;
                 prev = v[r];
@@ -821,7 +825,7 @@ __global__ __launch_bounds__(kWideThreads) __attribute__((amdgpu_waves_per_eu(2)
             uint32_t tau_l = 0u;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                if (((kept >> r) & 1) && rank == K - 1) tau_l = (uint32_t)v[r];
+                if (((kept >> r) & 1) && rank == K - 1) tau_l = v[r];
                 rank += (kept >> r) & 1;
             }
             const uint64_t hb = __ballot(tau_l != 0u);
@@ -829,23 +833,37 @@ __global__ __launch_bounds__(kWideThreads) __attribute__((amdgpu_waves_per_eu(2)
             if (lane == 0) s_tau[tt] = tau;
         }
         __syncthreads();
-        // list the candidates at or above tau in the token's region
+        // list the candidates at or above tau in the token's region: each
+        // lane counts its hits of a column tile, a wave prefix gives its
+        // offsets, one LDS atomic per wave and tile reserves the space, and
+        // every value is stored (misses and overflow to the discard entry
+        // kWideList), so the loop has no branches
 #pragma unroll
         for (int n = 0; n < 4; ++n) {
             const int tt = bcol[n] >> csh, q = bcol[n] & (KC - 1);
             const uint32_t tau = s_tau[tt];
             uint64_t* lst = (uint64_t*)(scores + (tb + tt) * KP * D);
+            uint32_t hm = 0u;   // bit 4 mt + i: value (mt, i) is listed
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    if (mk(mt, n, i) >= tau) {
-                        const int pos = atomicAdd(&s_cnt[tt], 1);
-                        if (pos < kWideList) {
-                            const uint32_t f = (uint32_t)(q * D + wr * 16 * MT + 16 * mt + 4 * kq + i);
-                            lst[pos] = ((uint64_t)f << 32) | __float_as_uint(acc[mt][n][i] * P.rsd);
-                        }
-                    }
+                for (int i = 0; i < 4; ++i) hm |= (uint32_t)(mk(mt, n, i) >= tau) << (4 * mt + i);
+            int total = 0;
+            int pos = wave_prefix<6>(__popc(hm), lane, total);   // at most 4 MT = 32 hits
+            int base = 0;
+            if (lane == 0 && total > 0) base = atomicAdd(&s_cnt[tt], total);
+            pos += __shfl(base, 0, 64);
+            if (total == 0) continue;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const bool hit = (hm >> (4 * mt + i)) & 1u;
+                    const uint32_t f = (uint32_t)(q * D + wr * 16 * MT + 16 * mt + 4 * kq + i);
+                    lst[(hit && pos < kWideList) ? pos : kWideList] =
+                        ((uint64_t)f << 32) | __float_as_uint(acc[mt][n][i] * P.rsd);
+                    pos += (int)hit;
+                }
         }
         __syncthreads();
         // a token with too many entries gets its full scores instead
@@ -985,14 +1003,14 @@ __global__ __launch_bounds__(kWideThreads) void wide_select_kernel(DevPlan P, in
             }
         }
         constexpr int M = 2;
-        uint64_t top[M] = {top0, top1};
+        uint32_t top[M] = {top0, top1};
         sort_desc<M, 6, false>(top, lane, x32);
-        uint64_t prev = shfl_u64(top[M - 1], (lane + 63) & 63);
-        if (lane == 0) prev = 0ull;
+        uint32_t prev = (uint32_t)__shfl((int)top[M - 1], (lane + 63) & 63, 64);
+        if (lane == 0) prev = 0u;
         int kept = 0, cnt = 0;
 #pragma unroll
         for (int r = 0; r < M; ++r) {
-            const bool kk = top[r] != 0ull && top[r] != prev;
+            const bool kk = top[r] != 0u && top[r] != prev;
             kept |= (int)kk << r;
             cnt += (int)kk;
             prev = top[r];
@@ -1002,7 +1020,7 @@ __global__ __launch_bounds__(kWideThreads) void wide_select_kernel(DevPlan P, in
         uint32_t tau_l = 0u;
 #pragma unroll
         for (int r = 0; r < M; ++r) {
-            if (((kept >> r) & 1) && rank == K - 1) tau_l = (uint32_t)top[r];
+            if (((kept >> r) & 1) && rank == K - 1) tau_l = top[r];
             rank += (kept >> r) & 1;
         }
         // one lane holds tau when at least K distinct magnitudes were seen; else take every live candidate
