@@ -158,3 +158,52 @@ def test_encode_zero_and_constant_rows():
     say(f"  {st}")
     assert np.array_equal(idx.cpu().numpy()[0], oi[0])
     assert st["exempt_tokens"] <= 2
+
+
+@pytest.mark.parametrize("name,T", [("pt_small_2l", 50), ("pt_small_3l", 33)])
+def test_encode_f32_input_matches_oracle(name, T):
+    """fp32 activations: the wide GEMM splits each value into three bf16 terms."""
+    say(f"[t6 encode f32] {name} T={T}")
+    plan = plan_for(name)
+    w, nb, dl, K, m, gens = setup(name)
+    x = inputs.normal((T, w.d), 500 + w.index)
+    idx, coef = dpb.encode(plan, x.to(DEV))
+    torch.cuda.synchronize()
+    oi, oc, om, oo = oracle.encode(w.d, m, nb, K, dl, gens, x.double().numpy())
+    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32)
+    say(f"  {st}")
+    assert st["exempt_tokens"] <= max(2, 0.02 * T)
+
+
+@pytest.mark.parametrize("name,T", [("pt_small_2l", 45), ("pt_small_3l", 29)])
+def test_decode_bwd_f32_grad_matches_oracle(name, T):
+    """fp32 upstream gradient through the direct reductions of wide plans."""
+    say(f"[t6 bwd f32 g] {name} T={T}")
+    plan = plan_for(name)
+    w, nb, dl, K, m, gens = setup(name)
+    x = inputs.activations(name, T)
+    oi, _, _, _ = oracle.encode(w.d, m, nb, K, dl, gens, x.double().numpy())
+    g = inputs.normal((T, w.d), 600 + w.index)
+    gc, gx = dpb.decode_bwd(plan, torch.from_numpy(oi).to(DEV), g.to(DEV), torch.float32)
+    torch.cuda.synchronize()
+    rgc, rgx = oracle.decode_bwd(w.d, m, oi, g.double().numpy())
+    compare_dense(gc.cpu().numpy(), rgc, TOL_F32)
+    compare_dense(gx.cpu().numpy(), rgx, TOL_F32)
+
+
+def test_encode_chunk_boundary_and_full_chunks():
+    """More than one 4096-token chunk of the wide encoder with a ragged last
+    chunk: sampled rows on both sides of each chunk boundary."""
+    name = "pt_small_2l"
+    T = 2 * 4096 + 77
+    say(f"[t6 encode chunks] {name} T={T}")
+    plan = plan_for(name)
+    w, nb, dl, K, m, gens = setup(name)
+    x = inputs.activations(name, T)
+    idx, coef = dpb.encode(plan, x.to(DEV))
+    torch.cuda.synchronize()
+    rows = np.array([0, 1, 4094, 4095, 4096, 4097, 8190, 8191, 8192, 8193, T - 2, T - 1])
+    oi, oc, om, oo = oracle.encode(w.d, m, nb, K, dl, gens, x[rows].double().numpy())
+    st = compare_encode(K, idx.cpu().numpy()[rows], coef.cpu().numpy()[rows], oi, oc, om, oo, TOL_F32)
+    say(f"  {st}")
+    assert st["exempt_tokens"] <= 2
