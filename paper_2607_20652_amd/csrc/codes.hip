@@ -11,11 +11,14 @@
 //    cores (16x16x16 bf16, coefficients split exactly into bf16 terms), and
 //    each column is modulated once by the parent's signs.  Other slots are
 //    added directly: +-coef per coordinate, the sign being parity(M & c).
-//  * backward: grad_coef of the children of a parent p is
+//  * backward, last level: grad_coef of the children of a parent p is
 //    Gamma_l (phi~_p (.) g) -- the encoder's child-scoring contraction with g
 //    in place of x (§2.2 child-scoring equation) -- on the matrix cores; the
 //    parent's sign pattern comes from nibble tables (parity is linear in the
-//    index bits), and grad_x is the decode of grad_coef.
+//    index bits).  The other levels select few of their parents' children
+//    (K_l of K_{l-1} Delta_l), so their slots are reduced directly, one lane
+//    per slot with two-element dot products.  grad_x is the decode of
+//    grad_coef.
 //
 // Workgroups hold kCodeWaves independent waves; each wave takes groups of
 // `wave_tokens` tokens in a grid-stride loop and synchronises only with itself.
@@ -675,9 +678,10 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
         }
         wave_sync();
 
-        // route every slot of levels >= 1 to a parent slot of the previous level
-        // (plans with many children per parent take every slot directly below)
-        if (!P.bwd_direct) route_slots(P, W, 1);
+        // route the last level's slots to a parent slot of the previous level
+        // (its scoring and the decode's leaf columns use the routes; plans with
+        // many children per parent take every slot directly below)
+        if (!P.bwd_direct) route_slots(P, W, P.levels - 1);
         // coefficients for basis slots and padding
         for (int tt = 0; tt < TPW; ++tt)
             for (int s = lane; s < k; s += 64) {
@@ -689,11 +693,11 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
         wave_sync();
 
         // grad_coef of routed slots: child scores of each parent column against g
-        if (!P.bwd_direct)
-            for (int l = 1; l < P.levels; ++l) score_level<G_BF16>(P, W, l);
+        if (!P.bwd_direct && P.levels > 1) score_level<G_BF16>(P, W, P.levels - 1);
 
-        // hashed slots that route nowhere (every hashed slot when the plan has
-        // many children per parent): direct reductions over the coordinates
+        // hashed slots that are not routed (levels below the last, slots that
+        // route nowhere, every hashed slot when the plan has many children per
+        // parent): direct reductions over the coordinates
         direct_scores<G_BF16, NG>(P, W);
         wave_sync();
         if (add_gc) {
