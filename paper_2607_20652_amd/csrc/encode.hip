@@ -576,10 +576,10 @@ __host__ __device__ inline unsigned wide_gemm_lds(const DevPlan& P, int l, bool 
 
 // Whether level l's GEMM selects in its epilogue: 16 to 64 parent columns per
 // token (whole tokens per 64-column wave tile) and a token's score region can
-// hold the kWideList (candidate, z) entries.
+// hold the kWideList (candidate, z) entries plus the discard entry after them.
 __host__ __device__ inline bool wide_fused(const DevPlan& P, int l)
 {
-    return P.cpt[l] >= 16 && P.cpt[l] <= 64 && P.active[l - 1] * P.delta[l] >= 2 * kWideList;
+    return P.cpt[l] >= 16 && P.cpt[l] <= 64 && P.active[l - 1] * P.delta[l] >= 2 * (kWideList + 1);
 }
 
 // Scores of tokens [t0 + TT blockIdx.x, ...) of a chunk of ntok tokens at level

@@ -207,3 +207,38 @@ def test_encode_chunk_boundary_and_full_chunks():
     st = compare_encode(K, idx.cpu().numpy()[rows], coef.cpu().numpy()[rows], oi, oc, om, oo, TOL_F32)
     say(f"  {st}")
     assert st["exempt_tokens"] <= 2
+
+
+# Wide hierarchies beyond Table 6, for the encoder's other tile shapes: 128 and
+# 64 children per parent (4 and 2 row tiles per wave), 48 parents per token
+# (one token per 64-column wave tile), and a level of 16 children inside a
+# wide plan (padding generator rows, scores written in full).
+CUSTOM = {
+    "wide_mixed": dict(d=1024, level_bits=(10, 14, 17), branchings=(0, 128, 64), active=(16, 48, 40)),
+    "wide_small_delta": dict(d=1024, level_bits=(10, 15, 19), branchings=(0, 256, 16), active=(16, 32, 64)),
+}
+
+
+@pytest.mark.parametrize("hname,T", [("wide_mixed", 70), ("wide_small_delta", 50)])
+def test_custom_wide_hierarchies(hname, T):
+    h = CUSTOM[hname]
+    d, nb, dl, K = h["d"], list(h["level_bits"]), list(h["branchings"]), list(h["active"])
+    say(f"[wide custom] {hname} T={T}")
+    plan = dpb.Plan(d, seed=0, level_bits=nb, branchings=dl, active=K)
+    m, gens = oracle.masks(d, nb[-1]), oracle.generators(nb, dl, 0)
+    x = inputs.normal((T, d), 700 + len(hname), "bf16")
+    idx, coef = dpb.encode(plan, x.to(DEV))
+    torch.cuda.synchronize()
+    oi, oc, om, oo = oracle.encode(d, m, nb, K, dl, gens, x.double().numpy())
+    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32)
+    say(f"  {st}")
+    assert st["exempt_tokens"] <= max(2, 0.02 * T)
+    g = inputs.normal((T, d), 800 + len(hname), "bf16")
+    gc, gx = dpb.decode_bwd(plan, torch.from_numpy(oi).to(DEV), g.to(DEV), torch.float32)
+    y = dpb.decode(plan, torch.from_numpy(oi).to(DEV), torch.from_numpy(oc.astype(np.float32)).to(DEV),
+                   torch.float32)
+    torch.cuda.synchronize()
+    rgc, rgx = oracle.decode_bwd(d, m, oi, g.double().numpy())
+    compare_dense(gc.cpu().numpy(), rgc, TOL_F32)
+    compare_dense(gx.cpu().numpy(), rgx, TOL_F32)
+    compare_dense(y.cpu().numpy(), oracle.decode(d, m, oi, oc.astype(np.float32).astype(np.float64)), TOL_F32)
