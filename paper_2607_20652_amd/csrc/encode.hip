@@ -483,21 +483,24 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
 // ---------------------------------------------------------------------------
 // Wide encoder: levels that score many children per parent (the paper's own
 // hierarchies score 256, App. G Table 6).  Level 0 runs one wave per token.
-// Each level l >= 1 is then a GEMM and a selection:
-//  * wide_gemm_kernel: the scores of all K_{l-1} x Delta_l children of a
-//    chunk of tokens, S[(t, q)][j] = <gamma_j, phi~_{p_tq} (.) x_t> (§2.2
+// Each level l >= 1 is then a GEMM and a selection over chunks of tokens:
+//  * wide_gemm_kernel: the scores of all K_{l-1} x Delta_l children of the
+//    chunk's tokens, S[(t, q)][j] = <gamma_j, phi~_{p_tq} (.) x_t> (§2.2
 //    child-scoring equation), as 16x16x32 bf16 MFMAs over a workgroup tile of
 //    all generator rows x 128 (token, parent) columns.  A fragments (exact
 //    +-1) are built from per-generator sign bitmaps held in LDS, B fragments
 //    from the token rows and the parents' sign bitmaps (nibble tables), as in
-//    the narrow encoder.  Scores go to a workspace, token-major.
+//    the narrow encoder.  Its epilogue computes each token's threshold (the
+//    K_l-th largest distinct magnitude among the lanes' top two; distinct
+//    magnitudes are distinct children) and writes only the (candidate, z)
+//    entries at or above it to the workspace; tokens with too many entries,
+//    shapes it does not cover and standardized scores get the full scores.
 //  * wide_select_kernel: one wave per token; AbsTopK with deduplication (a
-//    child reached from several parents has bit-identical keys).  The K-th
-//    largest distinct key among each lane's top keys is a threshold with at
-//    least K distinct keys above it; the keys above it are collected in LDS,
-//    sorted by a bitonic network, and the first K distinct ones emitted.  If
-//    too many keys pass, an exact extraction (K rounds of a wave maximum
-//    below the previous key) takes over.
+//    child reached from several parents has bit-identical keys): the listed
+//    entries, or the candidates above the same threshold found from the full
+//    scores, are sorted as 64-bit keys by a bitonic network and the first K
+//    distinct ones emitted; too many hits fall back to an exact extraction
+//    (K rounds of a wave maximum below the previous key).
 constexpr int kWideCols = 128;     // (token, parent) columns of a GEMM workgroup
 constexpr int kWideList = 1024;    // collected keys per token
 constexpr int kSeg = 16;           // keys per lane segment (64 kSeg = kWideList)
