@@ -92,53 +92,79 @@ __global__ void std_init_kernel(float2* stats, float* var, int64_t N)
 }
 
 // Column sums of x and x^2 over the tokens [T g / G, T (g + 1) / G) of
-// workgroup g = blockIdx.x; each thread takes 4 consecutive columns of a
-// 1024-column strip (blockIdx.y), eight rows per round.
+// workgroup g = blockIdx.x.  Each of its kStdColSlices slices sums a
+// contiguous part of those rows, a thread four consecutive columns of a
+// 1024-column strip (blockIdx.y), eight rows per round; the slices' sums are
+// then added in slice order (a fixed order: the statistics do not depend on
+// scheduling).
+constexpr int kStdColSlices = 4;
+
 template <bool BF16>
-__global__ __launch_bounds__(kStdThreads) void std_col_kernel(const void* x, int d, int64_t T, StdWs W)
+__global__ __launch_bounds__(kStdThreads * kStdColSlices) void std_col_kernel(const void* x, int d, int64_t T,
+                                                                             StdWs W)
 {
-    const int c0 = blockIdx.y * 4 * kStdThreads + 4 * threadIdx.x;
-    if (c0 >= d) return;
-    const int64_t t0 = T * blockIdx.x / kStdGroups, t1 = T * (blockIdx.x + 1) / kStdGroups;
+    __shared__ double part[kStdColSlices - 1][kStdThreads][8];
+    const int slice = threadIdx.x / kStdThreads, tid = threadIdx.x % kStdThreads;
+    const int c0 = blockIdx.y * 4 * kStdThreads + 4 * tid;
+    const int64_t g0 = T * blockIdx.x / kStdGroups, g1 = T * (blockIdx.x + 1) / kStdGroups;
+    const int64_t t0 = g0 + (g1 - g0) * slice / kStdColSlices, t1 = g0 + (g1 - g0) * (slice + 1) / kStdColSlices;
     const bool vec = (d & 3) == 0;
     double s1[4] = {0.0, 0.0, 0.0, 0.0}, s2[4] = {0.0, 0.0, 0.0, 0.0};
-    for (int64_t t = t0; t < t1; t += 8) {
-        float v[8][4];
+    if (c0 < d) {
+        for (int64_t t = t0; t < t1; t += 8) {
+            float v[8][4];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int64_t i = (t + e) * d + c0;
-            if (t + e >= t1) {
+            for (int e = 0; e < 8; ++e) {
+                const int64_t i = (t + e) * d + c0;
+                if (t + e >= t1) {
 #pragma unroll
-                for (int q = 0; q < 4; ++q) v[e][q] = 0.f;
-            } else if (vec && BF16) {
-                const uint2 u = *(const uint2*)((const uint16_t*)x + i);
-                v[e][0] = bf16_bits_to_f32(u.x & 0xFFFFu);
-                v[e][1] = bf16_bits_to_f32(u.x >> 16);
-                v[e][2] = bf16_bits_to_f32(u.y & 0xFFFFu);
-                v[e][3] = bf16_bits_to_f32(u.y >> 16);
-            } else if (vec) {
-                const float4 f = *(const float4*)((const float*)x + i);
-                v[e][0] = f.x; v[e][1] = f.y; v[e][2] = f.z; v[e][3] = f.w;
-            } else {
+                    for (int q = 0; q < 4; ++q) v[e][q] = 0.f;
+                } else if (vec && BF16) {
+                    const uint2 u = *(const uint2*)((const uint16_t*)x + i);
+                    v[e][0] = bf16_bits_to_f32(u.x & 0xFFFFu);
+                    v[e][1] = bf16_bits_to_f32(u.x >> 16);
+                    v[e][2] = bf16_bits_to_f32(u.y & 0xFFFFu);
+                    v[e][3] = bf16_bits_to_f32(u.y >> 16);
+                } else if (vec) {
+                    const float4 f = *(const float4*)((const float*)x + i);
+                    v[e][0] = f.x; v[e][1] = f.y; v[e][2] = f.z; v[e][3] = f.w;
+                } else {
 #pragma unroll
-                for (int q = 0; q < 4; ++q) v[e][q] = c0 + q < d ? load_act<BF16>(x, i + q) : 0.f;
+                    for (int q = 0; q < 4; ++q) v[e][q] = c0 + q < d ? load_act<BF16>(x, i + q) : 0.f;
+                }
             }
-        }
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
+            for (int e = 0; e < 8; ++e)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    s1[q] += (double)v[e][q];
+                    s2[q] += (double)v[e][q] * (double)v[e][q];
+                }
+        }
+    }
+    if (slice > 0)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            part[slice - 1][tid][q] = s1[q];
+            part[slice - 1][tid][4 + q] = s2[q];
+        }
+    __syncthreads();
+    if (slice == 0 && c0 < d) {
+#pragma unroll
+        for (int sl = 0; sl < kStdColSlices - 1; ++sl)
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                s1[q] += (double)v[e][q];
-                s2[q] += (double)v[e][q] * (double)v[e][q];
+                s1[q] += part[sl][tid][q];
+                s2[q] += part[sl][tid][4 + q];
+            }
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            if (c0 + q < d) {
+                double* o = W.col + ((int64_t)blockIdx.x * d + c0 + q) * 2;
+                o[0] = s1[q];
+                o[1] = s2[q];
             }
     }
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-        if (c0 + q < d) {
-            double* o = W.col + ((int64_t)blockIdx.x * d + c0 + q) * 2;
-            o[0] = s1[q];
-            o[1] = s2[q];
-        }
 }
 
 __global__ void std_col_update_kernel(int d, int64_t T, StdWs W, float2* stats, float* var, float beta, float eps)
@@ -282,8 +308,9 @@ hipError_t launch_std_update(const DevPlan& P, const void* x, bool x_bf16, int64
     const StdWs W = std_ws(ws, P, nullptr);
     float2* st = (float2*)stats;
     const dim3 gc(kStdGroups, (P.d + 4 * kStdThreads - 1) / (4 * kStdThreads));
-    if (x_bf16) hipLaunchKernelGGL(std_col_kernel<true>, gc, dim3(kStdThreads), 0, stream, x, P.d, T, W);
-    else hipLaunchKernelGGL(std_col_kernel<false>, gc, dim3(kStdThreads), 0, stream, x, P.d, T, W);
+    const dim3 bc(kStdThreads * kStdColSlices);
+    if (x_bf16) hipLaunchKernelGGL(std_col_kernel<true>, gc, bc, 0, stream, x, P.d, T, W);
+    else hipLaunchKernelGGL(std_col_kernel<false>, gc, bc, 0, stream, x, P.d, T, W);
     hipLaunchKernelGGL(std_col_update_kernel, dim3((P.d + 255) / 256), dim3(256), 0, stream, P.d, T, W, st, var, beta,
                        eps);
     const int m = (int)std::min<int64_t>(T, kStdSample);
