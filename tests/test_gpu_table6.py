@@ -242,3 +242,33 @@ def test_custom_wide_hierarchies(hname, T):
     compare_dense(gc.cpu().numpy(), rgc, TOL_F32)
     compare_dense(gx.cpu().numpy(), rgx, TOL_F32)
     compare_dense(y.cpu().numpy(), oracle.decode(d, m, oi, oc.astype(np.float32).astype(np.float64)), TOL_F32)
+
+
+def test_encode_without_workspace_uses_general_kernel():
+    """With a workspace that is too small the library runs the general
+    encoder instead of the wide one: the same codes (to the parity rules)."""
+    name, T = "pt_small_3l", 24
+    say(f"[t6 encode small workspace] {name} T={T}")
+    plan = plan_for(name)
+    w, nb, dl, K, m, gens = setup(name)
+    x = inputs.activations(name, T)
+    tiny = torch.empty(4, dtype=torch.float32, device=DEV)
+    idx, coef = dpb.encode(plan, x.to(DEV), workspace=tiny)
+    torch.cuda.synchronize()
+    oi, oc, om, oo = oracle.encode(w.d, m, nb, K, dl, gens, x.double().numpy())
+    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32)
+    say(f"  {st}")
+    assert st["exempt_tokens"] <= 2
+
+
+def test_empty_batches():
+    name = "pt_small_2l"
+    say(f"[t6 empty] {name}")
+    plan = plan_for(name)
+    w = inputs.workload(name)
+    x = torch.empty((0, w.d), dtype=torch.bfloat16, device=DEV)
+    idx, coef = dpb.encode(plan, x)
+    y = dpb.decode(plan, idx, coef, torch.bfloat16)
+    gc, gx = dpb.decode_bwd(plan, idx, torch.empty((0, w.d), dtype=torch.bfloat16, device=DEV), torch.bfloat16)
+    torch.cuda.synchronize()
+    assert idx.shape == (0, plan.k_tot) and y.shape == (0, w.d) and gc.shape == (0, plan.k_tot)
