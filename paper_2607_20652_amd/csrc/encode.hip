@@ -472,9 +472,61 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
                     keys[4 * mb + i] = ok ? make_key(sc, c) : 0ull;
                 }
             }
-            sort_desc<R, NB, true>(keys, lanepos, x32);
-            emit_mfma<R, CPT>(P, keys, lane, lanepos, ct, prev_addr, before_mask, token_mask, t0, ntok, P.active[l],
-                              P.slot_base[l], par, EL.kmaxp, out_idx, out_coef);
+            // Levels that keep few of their candidates (K_l <= 2 CPT, the beam
+            // levels): the K_l-th largest distinct lane maximum tau bounds the
+            // answer (at least K_l distinct keys reach it), only the keys >= tau
+            // are listed, and that short list (one key per lane of the token) is
+            // sorted and emitted.  A token with more keys >= tau than lanes, or
+            // any other level, sorts all its keys.
+            const int Kl = P.active[l];
+            bool done = false;
+            if (Kl <= 2 * CPT && EL.listn >= 4 * CPT) {
+                uint64_t mx[1] = {keys[0]};
+#pragma unroll
+                for (int r = 1; r < R; ++r) mx[0] = keys[r] > mx[0] ? keys[r] : mx[0];
+                sort_desc<1, NB, true>(mx, lanepos, x32);
+                const uint32_t ph = (uint32_t)__builtin_amdgcn_ds_bpermute(prev_addr, (int)(uint32_t)(mx[0] >> 32));
+                const uint32_t pl = (uint32_t)__builtin_amdgcn_ds_bpermute(prev_addr, (int)(uint32_t)mx[0]);
+                const uint64_t prev = lanepos > 0 ? (((uint64_t)ph << 32) | pl) : 0ull;
+                const bool kept = mx[0] != 0ull && mx[0] != prev;
+                const int rank = (int)__popcll(__ballot(kept) & before_mask);
+                const uint64_t owner = __ballot(kept && rank == Kl - 1) & token_mask;
+                uint64_t tau = 1ull;   // fewer than K_l distinct maxima: every key
+                if (owner) {
+                    const int oa = (int)__builtin_ctzll(owner) << 2;
+                    tau = ((uint64_t)(uint32_t)__builtin_amdgcn_ds_bpermute(oa, (int)(uint32_t)(mx[0] >> 32)) << 32) |
+                          (uint32_t)__builtin_amdgcn_ds_bpermute(oa, (int)(uint32_t)mx[0]);
+                }
+                int c = 0;
+#pragma unroll
+                for (int r = 0; r < R; ++r) c += (int)(keys[r] >= tau);
+                int before = 0, total = 0;
+#pragma unroll
+                for (int b = 0; b < 3; ++b) {   // c <= R = 4
+                    const uint64_t m = __ballot((c >> b) & 1);
+                    before += (int)__popcll(m & before_mask) << b;
+                    total += (int)__popcll(m & token_mask) << b;
+                }
+                if (!__ballot(total > 4 * CPT)) {
+                    uint64_t* tl = list + ct * EL.listn;
+                    int pos = before;
+#pragma unroll
+                    for (int r = 0; r < R; ++r)
+                        if (keys[r] >= tau) tl[pos++] = keys[r];
+                    wave_sync();
+                    uint64_t one[1] = {lanepos < total ? tl[lanepos] : 0ull};
+                    wave_sync();
+                    sort_desc<1, NB, true>(one, lanepos, x32);
+                    emit_mfma<1, CPT>(P, one, lane, lanepos, ct, prev_addr, before_mask, token_mask, t0, ntok, Kl,
+                                      P.slot_base[l], par, EL.kmaxp, out_idx, out_coef);
+                    done = true;
+                }
+            }
+            if (!done) {
+                sort_desc<R, NB, true>(keys, lanepos, x32);
+                emit_mfma<R, CPT>(P, keys, lane, lanepos, ct, prev_addr, before_mask, token_mask, t0, ntok, Kl,
+                                  P.slot_base[l], par, EL.kmaxp, out_idx, out_coef);
+            }
             wave_sync();
         }
     }
