@@ -1231,7 +1231,7 @@ hipError_t launch_encode2(const DevPlan& P, const void* x, bool x_bf16, int64_t 
 }
 
 // Tokens per pass of the wide encoder (bounds its workspace).
-constexpr int64_t kWideChunkTokens = 4096;
+constexpr int64_t kWideChunkTokens = 16384;
 
 static int wide_max_cands(const DevPlan& P)
 {

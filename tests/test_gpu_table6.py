@@ -191,18 +191,22 @@ def test_decode_bwd_f32_grad_matches_oracle(name, T):
     compare_dense(gx.cpu().numpy(), rgx, TOL_F32)
 
 
+CHUNK = 16384   # tokens per pass of the wide encoder
+
+
 def test_encode_chunk_boundary_and_full_chunks():
-    """More than one 4096-token chunk of the wide encoder with a ragged last
-    chunk: sampled rows on both sides of each chunk boundary."""
+    """More than one chunk of the wide encoder with a ragged last chunk:
+    sampled rows on both sides of each chunk boundary."""
     name = "pt_small_2l"
-    T = 2 * 4096 + 77
+    T = 2 * CHUNK + 77
     say(f"[t6 encode chunks] {name} T={T}")
     plan = plan_for(name)
     w, nb, dl, K, m, gens = setup(name)
-    x = inputs.activations(name, T)
+    x = inputs.normal((T, w.d), 900, "bf16")
     idx, coef = dpb.encode(plan, x.to(DEV))
     torch.cuda.synchronize()
-    rows = np.array([0, 1, 4094, 4095, 4096, 4097, 8190, 8191, 8192, 8193, T - 2, T - 1])
+    rows = np.array([0, 1, CHUNK - 2, CHUNK - 1, CHUNK, CHUNK + 1, 2 * CHUNK - 2, 2 * CHUNK - 1, 2 * CHUNK,
+                     2 * CHUNK + 1, T - 2, T - 1])
     oi, oc, om, oo = oracle.encode(w.d, m, nb, K, dl, gens, x[rows].double().numpy())
     st = compare_encode(K, idx.cpu().numpy()[rows], coef.cpu().numpy()[rows], oi, oc, om, oo, TOL_F32)
     say(f"  {st}")
