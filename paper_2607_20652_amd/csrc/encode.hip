@@ -164,6 +164,7 @@ __device__ __forceinline__ void emit_mfma(const DevPlan& P, const uint64_t (&key
                                           int ntok, int K, int sb, int32_t* par, int kmaxp, int32_t* out_idx,
                                           float* out_coef)
 {
+    (void)lane;
     const int k_tot = P.k_tot;
     const uint32_t ph = (uint32_t)__builtin_amdgcn_ds_bpermute(prev_addr, (int)(uint32_t)(key[R - 1] >> 32));
     const uint32_t pl = (uint32_t)__builtin_amdgcn_ds_bpermute(prev_addr, (int)(uint32_t)key[R - 1]);
@@ -857,7 +858,7 @@ __global__ __launch_bounds__(kWideThreads) __attribute__((amdgpu_waves_per_eu(2)
             s_top[((tt * 2 + wr) * 64 + lane) * 2] = top0;
             s_top[((tt * 2 + wr) * 64 + lane) * 2 + 1] = top1;
         }
-        if (threadIdx.x < TT) s_cnt[threadIdx.x] = 0;
+        if ((int)threadIdx.x < TT) s_cnt[threadIdx.x] = 0;
         __syncthreads();
         // tau of each token: the K-th largest distinct key among its 256 lane tops
         for (int tt = wave; tt < TT; tt += 4) {
@@ -925,7 +926,7 @@ __global__ __launch_bounds__(kWideThreads) __attribute__((amdgpu_waves_per_eu(2)
 #pragma unroll
         for (int n = 0; n < 4; ++n)
             if (s_cnt[bcol[n] >> csh] > kWideList) store_scores(n);
-        if (threadIdx.x < nt_tok) counts[tb + threadIdx.x] = s_cnt[threadIdx.x];
+        if ((int)threadIdx.x < nt_tok) counts[tb + threadIdx.x] = s_cnt[threadIdx.x];
     }
 }
 

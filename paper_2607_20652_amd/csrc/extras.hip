@@ -635,6 +635,7 @@ __device__ __forceinline__ void var_bucket_loop(const VarRec* rec, int64_t p0, i
 __global__ __launch_bounds__(kVarBucketThreads) void var_bucket_kernel(int64_t nfeat, int S, int bsh, int n_min,
                                                                        VarWs W)
 {
+    (void)nfeat;   // buckets cover [S, nfeat) by construction of the grid
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ double rs[kVarBucketThreads / 64];
     __shared__ unsigned long long rc[kVarBucketThreads / 64];

@@ -67,6 +67,7 @@ template <bool ACT_BF16>
 __device__ __forceinline__ void score_chunk(const DevPlan& P, int kq, u32x4 a, uint32_t wd, const uint32_t* prow,
                                             const float* frow, int c, f32x4& acc)
 {
+    (void)P;
     const bf16x8 av = __builtin_bit_cast(bf16x8, a);
     if constexpr (ACT_BF16) {
         // dword i: coordinates 4kq + i (low half) and 4kq + i + 16 (high half)
