@@ -339,20 +339,34 @@ __device__ void decode_tokens(const DevPlan& P, const Wave& W, const float* cf)
         wave_sync();
     }
 
-    // basis slots: coefficient at their own coordinate, in slot order
+    // basis slots: coefficient at their own coordinate.  Distinct
+    // coordinates (the encoder's level 0) are added by all lanes at once; a
+    // block with a repeated coordinate adds its slots one by one, in slot order.
     for (int tt = 0; tt < W.ntok; ++tt)
         for (int s0 = 0; s0 < k; s0 += 64) {
             const int s = s0 + lane;
             const int32_t c = s < k ? W.idx[tt * k + s] : -1;
             const int a = s < k ? __float_as_int(cf[tt * k + s]) : 0;
-            uint64_t m = __ballot(c >= 0 && c < d);
-            while (m) {
-                const int b = __builtin_ctzll(m);
-                m &= m - 1;
-                const int cb = rdlane(c, b);
-                const float ab = __int_as_float(rdlane(a, b));
-                if (lane == 0) W.y[tt * dp + cb] += ab;
+            const bool basis = c >= 0 && c < d;
+            uint64_t m = __ballot(basis);
+            if (!m) continue;
+            bool dup = false;
+            for (uint64_t mm = m; mm; mm &= mm - 1) {
+                const int b = __builtin_ctzll(mm);
+                dup |= basis && b < lane && rdlane(c, b) == c;
             }
+            if (!__ballot(dup)) {
+                if (basis) W.y[tt * dp + c] += __int_as_float(a);
+            } else {
+                while (m) {
+                    const int b = __builtin_ctzll(m);
+                    m &= m - 1;
+                    const int cb = rdlane(c, b);
+                    const float ab = __int_as_float(rdlane(a, b));
+                    if (lane == 0) W.y[tt * dp + cb] += ab;
+                }
+            }
+            wave_sync();
         }
     wave_sync();
 }

@@ -203,6 +203,7 @@ def test_decode_arbitrary_codes(name):
     rng = np.random.default_rng(11)
     idx = rng.integers(0, 1 << w.n, size=(T, k)).astype(np.int32)
     idx[:, :3] = rng.integers(0, w.d, size=(T, 3))
+    idx[::4, 1] = idx[::4, 0]          # a basis coordinate held twice
     idx[:, 5] = idx[:, 6]
     idx[::3, -2:] = -1
     coef = rng.standard_normal((T, k)).astype(np.float32)
@@ -226,6 +227,7 @@ def _mixed_codes(name, T, seed=21):
     idx[::4, last + 1] = -1
     idx[::5, K[0]] = rng.integers(0, w.d, size=idx[::5].shape[0])
     idx[::7, 1] = rng.integers(w.d, 1 << w.n, size=idx[::7].shape[0])
+    idx[3::7, 2] = idx[3::7, 0]        # a basis coordinate held twice
     coef[:, last + 4] *= -3.0
     return w, m, idx, coef
 
