@@ -276,3 +276,27 @@ def test_empty_batches():
     gc, gx = dpb.decode_bwd(plan, idx, torch.empty((0, w.d), dtype=torch.bfloat16, device=DEV), torch.bfloat16)
     torch.cuda.synchronize()
     assert idx.shape == (0, plan.k_tot) and y.shape == (0, w.d) and gc.shape == (0, plan.k_tot)
+
+
+@pytest.mark.parametrize("name", ["pt_small_3l", "pt_large_2l"])
+def test_decode_and_bwd_full_size_sampled(name):
+    """The step at its full size (16,384 tokens, the benchmarked launch):
+    encode on the GPU, decode and backward of its codes, sampled rows against
+    the oracle's decode and backward of the same codes."""
+    w, nb, dl, K, m, gens = setup(name)
+    say(f"[t6 decode+bwd full] {name} T={w.tokens}")
+    plan = plan_for(name)
+    x = inputs.activations(name).to(DEV)
+    g = inputs.upstream_grad(name).to(DEV)
+    idx, coef = dpb.encode(plan, x)
+    y = dpb.decode(plan, idx, coef, torch.bfloat16)
+    gc, gx = dpb.decode_bwd(plan, idx, g, torch.bfloat16)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(5 + w.index)
+    rows = np.unique(np.concatenate([np.arange(8), rng.choice(w.tokens, 24, replace=False),
+                                     np.arange(w.tokens - 8, w.tokens)]))
+    ii, cc = idx.cpu().numpy()[rows], coef.cpu().numpy()[rows].astype(np.float64)
+    compare_dense(y.float().cpu().numpy()[rows], oracle.decode(w.d, m, ii, cc), TOL_BF16)
+    rgc, rgx = oracle.decode_bwd(w.d, m, ii, g.double().cpu().numpy()[rows])
+    compare_dense(gc.cpu().numpy()[rows], rgc, TOL_F32)
+    compare_dense(gx.float().cpu().numpy()[rows], rgx, TOL_BF16)
