@@ -116,17 +116,20 @@ dpb_status dpb_encode(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, in
 
 /* Bytes of device workspace dpb_encode_ws needs for T tokens: 0 when the
  * plan runs on the narrow encoder (at most 64 children per parent and the
- * other limits of dpb_encode's fast path), else the child scores of up to
- * 4096 tokens, 4 * min(T, 4096) * max_l K_{l-1} Delta_l bytes (128 MiB for
- * the paper's 3-level hierarchy). */
+ * other limits of dpb_encode's fast path), else, for up to C = min(T, 16384)
+ * tokens per pass, a region of 4 * max_l K_{l-1} Delta_l bytes per token (it
+ * holds the token's listed candidates, or all its child scores) and one
+ * 4-byte count per token, each part rounded up to 256 bytes (512 MiB for the
+ * paper's 3-level hierarchy at 16384 tokens). */
 size_t dpb_encode_workspace_bytes(const dpb_plan* plan, int64_t T);
 
 /* ENCODE with a workspace: the general entry of which dpb_encode and
  * dpb_encode_std are special cases.  For plans that score many children per
  * parent (up to 256, as the paper's own hierarchies do, App. G Table 6) it
  * runs each level as a matrix-core GEMM of all K_{l-1} x Delta_l child
- * scores into the workspace, followed by the AbsTopK selection; results are
- * the same as dpb_encode's.
+ * scores whose epilogue lists each token's candidates above a threshold in
+ * the workspace (or all its scores), followed by the AbsTopK selection;
+ * results are the same as dpb_encode's.
  *   stats     : device fp32 [N][2] standardization statistics, or NULL for
  *               raw scores (see dpb_encode_std)
  *   workspace : device, >= dpb_encode_workspace_bytes(plan, T), 16-B aligned,
