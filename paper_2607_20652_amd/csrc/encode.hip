@@ -544,7 +544,7 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
 //    +-1) are built from per-generator sign bitmaps held in LDS, B fragments
 //    from the token rows and the parents' sign bitmaps (nibble tables), as in
 //    the narrow encoder.  Its epilogue computes each token's threshold (the
-//    K_l-th largest distinct magnitude among the lanes' top two; distinct
+//    K_l-th largest distinct magnitude among the lanes' maxima; distinct
 //    magnitudes are distinct children) and writes only the (candidate, z)
 //    entries at or above it to the workspace; tokens with too many entries,
 //    shapes it does not cover and standardized scores get the full scores.
@@ -642,8 +642,8 @@ __host__ __device__ inline bool wide_fused(const DevPlan& P, int l)
 // l into scores[(t - t0) K_{l-1} + q][j] (t0-relative tokens).  MT = 16-row
 // tiles per wave: waves (wr, wc) cover rows 16 MT wr .. and columns 64 wc ..
 // FUSE: instead of all scores, each token's region receives the (candidate,
-// z) entries at or above a threshold tau computed here from the lanes' top
-// two distinct magnitude keys (the selection's first pass), and counts[t - t0]
+// z) entries at or above a threshold tau computed here from the lanes'
+// largest magnitude keys (the selection's first pass), and counts[t - t0]
 // their number; a token with more than kWideList entries gets its full scores
 // and its count says so.
 template <bool X_BF16, int MT, bool FUSE>
@@ -829,8 +829,8 @@ __global__ __launch_bounds__(kWideThreads) __attribute__((amdgpu_waves_per_eu(2)
 #pragma unroll
         for (int n = 0; n < 4; ++n) pid[n] = s_pidx[bcol[n]];
         __syncthreads();   // the staging LDS is free from here on
-        uint32_t* s_top = (uint32_t*)smem;             // [TT][2 row halves][64 lanes][2]
-        uint32_t* s_tau = s_top + TT * 256;           // [TT]
+        uint32_t* s_top = (uint32_t*)smem;             // [TT][2 row halves][64 lanes]
+        uint32_t* s_tau = s_top + TT * 128;           // [TT]
         int* s_cnt = (int*)(s_tau + TT);              // [TT]
         // magnitude key of value i of tile (mt, n): |z| bits + 1, 0 for padding
         auto mk = [&](int mt, int n, int i) -> uint32_t {
@@ -838,39 +838,33 @@ __global__ __launch_bounds__(kWideThreads) __attribute__((amdgpu_waves_per_eu(2)
             const uint32_t m = (__float_as_uint(acc[mt][n][i] * P.rsd) & 0x7FFFFFFFu) + 1u;
             return ok ? m : 0u;
         };
-        // each lane's two largest distinct keys per token of this wave
+        // each lane's largest key per token of this wave
         for (int u = 0; u < tpw; ++u) {
-            uint32_t top0 = 0u, top1 = 0u;
+            uint32_t top = 0u;
 #pragma unroll
             for (int n = 0; n < 4; ++n) {
                 if (((n * 16) >> csh) != u) continue;
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const uint32_t m = mk(mt, n, i);
-                        const bool gt0 = m > top0, gt1 = m > top1 && m != top0;
-                        top1 = gt0 ? top0 : (gt1 ? m : top1);
-                        top0 = gt0 ? m : top0;
-                    }
+                    for (int i = 0; i < 4; ++i) top = max(top, mk(mt, n, i));
             }
             const int tt = ((wc * 64) >> csh) + u;
-            s_top[((tt * 2 + wr) * 64 + lane) * 2] = top0;
-            s_top[((tt * 2 + wr) * 64 + lane) * 2 + 1] = top1;
+            s_top[(tt * 2 + wr) * 64 + lane] = top;
         }
         if ((int)threadIdx.x < TT) s_cnt[threadIdx.x] = 0;
         __syncthreads();
-        // tau of each token: the K-th largest distinct key among its 256 lane tops
+        // tau of each token: the K-th largest distinct key among its 128 lane maxima
         for (int tt = wave; tt < TT; tt += 4) {
-            uint32_t v[4];
+            uint32_t v[2];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) v[r] = s_top[tt * 256 + lane * 4 + r];
-            sort_desc<4, 6, false>(v, lane, x32);
-            uint32_t prev = (uint32_t)__shfl((int)v[3], (lane + 63) & 63, 64);
+            for (int r = 0; r < 2; ++r) v[r] = s_top[tt * 128 + lane * 2 + r];
+            sort_desc<2, 6, false>(v, lane, x32);
+            uint32_t prev = (uint32_t)__shfl((int)v[1], (lane + 63) & 63, 64);
             if (lane == 0) prev = 0u;
             int kept = 0, cnt = 0;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
+            for (int r = 0; r < 2; ++r) {
                 const bool kk = v[r] != 0u && v[r] != prev;
                 kept |= (int)kk << r;
                 cnt += (int)kk;
@@ -880,7 +874,7 @@ __global__ __launch_bounds__(kWideThreads) __attribute__((amdgpu_waves_per_eu(2)
             int rank = wave_prefix5(cnt, lane, total);
             uint32_t tau_l = 0u;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
+            for (int r = 0; r < 2; ++r) {
                 if (((kept >> r) & 1) && rank == K - 1) tau_l = v[r];
                 rank += (kept >> r) & 1;
             }
