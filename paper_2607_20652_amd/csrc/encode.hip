@@ -633,9 +633,16 @@ __host__ __device__ inline unsigned wide_gemm_lds(const DevPlan& P, int l, bool 
 // Whether level l's GEMM selects in its epilogue: 16 to 64 parent columns per
 // token (whole tokens per 64-column wave tile) and a token's score region can
 // hold the kWideList (candidate, z) entries plus the discard entry after them.
+// The fused epilogue reuses the staging LDS: the lane maxima, thresholds and
+// counts below kWideEpiZ, then each wave's z values of one column tile.
+constexpr unsigned kWideEpiZ = 8192;
+__host__ __device__ inline unsigned wide_epi_lds(int MT) { return kWideEpiZ + 4u * 64u * (4u * MT + 4u) * 4u; }
+
 __host__ __device__ inline bool wide_fused(const DevPlan& P, int l)
 {
-    return P.cpt[l] >= 16 && P.cpt[l] <= 64 && P.active[l - 1] * P.delta[l] >= 2 * (kWideList + 1);
+    const int MT = (P.delta[l] > 32 ? P.delta[l] : 32) / 32;
+    return P.cpt[l] >= 16 && P.cpt[l] <= 64 && P.active[l - 1] * P.delta[l] >= 2 * (kWideList + 1) &&
+           wide_gemm_lds(P, l, true) - align16u(kWideCols * 4) >= wide_epi_lds(MT);
 }
 
 // Scores of tokens [t0 + TT blockIdx.x, ...) of a chunk of ntok tokens at level
@@ -885,9 +892,10 @@ __global__ __launch_bounds__(kWideThreads) __attribute__((amdgpu_waves_per_eu(2)
         __syncthreads();
         // list the candidates at or above tau in the token's region: each
         // lane counts its hits of a column tile, a wave prefix gives its
-        // offsets, one LDS atomic per wave and tile reserves the space, and
-        // every value is stored (misses and overflow to the discard entry
-        // kWideList), so the loop has no branches
+        // offsets, one LDS atomic per wave and tile reserves the space; the
+        // tile's z values go through the wave's LDS rows so that each lane
+        // visits only its hits
+        float* zrow = (float*)(smem + kWideEpiZ) + (wave * 64 + lane) * (4 * MT + 4);
 #pragma unroll
         for (int n = 0; n < 4; ++n) {
             const int tt = bcol[n] >> csh, q = bcol[n] & (KC - 1);
@@ -905,15 +913,18 @@ __global__ __launch_bounds__(kWideThreads) __attribute__((amdgpu_waves_per_eu(2)
             pos += __shfl(base, 0, 64);
             if (total == 0) continue;
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const bool hit = (hm >> (4 * mt + i)) & 1u;
-                    const uint32_t f = (uint32_t)(q * D + wr * 16 * MT + 16 * mt + 4 * kq + i);
-                    lst[(hit && pos < kWideList) ? pos : kWideList] =
-                        ((uint64_t)f << 32) | __float_as_uint(acc[mt][n][i] * P.rsd);
-                    pos += (int)hit;
-                }
+            for (int mt = 0; mt < MT; ++mt) {
+                const f32x4 v = acc[mt][n];
+                *(float4*)(zrow + 4 * mt) = make_float4(v[0] * P.rsd, v[1] * P.rsd, v[2] * P.rsd, v[3] * P.rsd);
+            }
+            const uint32_t f0 = (uint32_t)(q * D + wr * 16 * MT + 4 * kq);
+            while (hm) {
+                const int b = __builtin_ctz(hm);
+                hm &= hm - 1;
+                const uint32_t f = f0 + 16u * (uint32_t)(b >> 2) + (uint32_t)(b & 3);
+                if (pos < kWideList) lst[pos] = ((uint64_t)f << 32) | __float_as_uint(zrow[b]);
+                ++pos;
+            }
         }
         __syncthreads();
         // a token with too many entries gets its full scores instead
