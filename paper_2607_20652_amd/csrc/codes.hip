@@ -500,14 +500,45 @@ __global__ __launch_bounds__(kThreads) void decode2_kernel(DevPlan P, const int3
 {
     extern __shared__ __align__(16) unsigned char smem[];
     load_shared(P, smem);
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, TPW = P.wave_tokens;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, TPW = P.wave_tokens, k = P.k_tot;
     Wave W = make_wave(P, smem, false, true, wave, lane);
     const int64_t ngroups = (T + TPW - 1) / TPW;
-    for (int64_t grp = (int64_t)blockIdx.x * kCodeWaves + wave; grp < ngroups;
-         grp += (int64_t)gridDim.x * kCodeWaves) {
+    const int64_t gstride = (int64_t)gridDim.x * kCodeWaves;
+    // the next group's code is requested while this group is decoded (two
+    // tokens of at most 128 slots: four words of each array per lane)
+    constexpr int kPrefetch = 4;
+    const bool pf = TPW == 2 && k <= 128;
+    int32_t nidx[kPrefetch];
+    float ncoef[kPrefetch];
+    auto fetch = [&](int64_t grp) {
+#pragma unroll
+        for (int e = 0; e < kPrefetch; ++e) {
+            const int tt = e >> 1, s = (e & 1) * 64 + lane;
+            const int64_t t = grp * TPW + tt;
+            const bool ok = s < k && t < T;
+            nidx[e] = ok ? idx[t * k + s] : -1;
+            ncoef[e] = ok ? coef[t * k + s] : 0.f;
+        }
+    };
+    int64_t grp = (int64_t)blockIdx.x * kCodeWaves + wave;
+    if (pf && grp < ngroups) fetch(grp);
+    for (; grp < ngroups; grp += gstride) {
         W.t0 = grp * TPW;
         W.ntok = (int)min((int64_t)TPW, T - W.t0);
-        load_codes(P, W, idx, coef);
+        if (pf) {
+#pragma unroll
+            for (int e = 0; e < kPrefetch; ++e) {
+                const int tt = e >> 1, s = (e & 1) * 64 + lane;
+                if (s < k) {
+                    W.idx[tt * k + s] = nidx[e];
+                    W.coef[tt * k + s] = ncoef[e];
+                    W.route[tt * k + s] = -1;
+                }
+            }
+            if (grp + gstride < ngroups) fetch(grp + gstride);
+        } else {
+            load_codes(P, W, idx, coef);
+        }
         wave_sync();
         if (P.leaf_columns) {
             route_slots(P, W, P.levels - 1);
