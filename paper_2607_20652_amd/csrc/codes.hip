@@ -705,14 +705,40 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
     const int d = P.d, dp = P.dp;
     Wave W = make_wave(P, smem, true, G_BF16, wave, lane);
     const int64_t ngroups = (T + TPW - 1) / TPW;
-    for (int64_t grp = (int64_t)blockIdx.x * kCodeWaves + wave; grp < ngroups;
-         grp += (int64_t)gridDim.x * kCodeWaves) {
+    const int64_t gstride = (int64_t)gridDim.x * kCodeWaves;
+    // the next group's code is requested while this group is processed
+    // (two tokens of at most 128 slots: four words per lane)
+    const bool pf = TPW == 2 && k <= 128;
+    int32_t nidx[4];
+    auto fetch = [&](int64_t gp) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int tt = e >> 1, s = (e & 1) * 64 + lane;
+            const int64_t t = gp * TPW + tt;
+            nidx[e] = (s < k && t < T) ? idx[t * k + s] : -1;
+        }
+    };
+    int64_t grp = (int64_t)blockIdx.x * kCodeWaves + wave;
+    if (pf && grp < ngroups) fetch(grp);
+    for (; grp < ngroups; grp += gstride) {
         const int64_t t0 = grp * TPW;
         W.t0 = t0;
         W.ntok = (int)min((int64_t)TPW, T - t0);
 
         // codes, routes reset, and g in LDS
-        load_codes(P, W, idx, nullptr);
+        if (pf) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int tt = e >> 1, s = (e & 1) * 64 + lane;
+                if (s < k) {
+                    W.idx[tt * k + s] = nidx[e];
+                    W.route[tt * k + s] = -1;
+                }
+            }
+            if (grp + gstride < ngroups) fetch(grp + gstride);
+        } else {
+            load_codes(P, W, idx, nullptr);
+        }
         if constexpr (G_BF16) {
             load_pairs(P, lane, W.ntok, TPW, (const uint16_t*)g, t0, W.pairs);
         } else {
