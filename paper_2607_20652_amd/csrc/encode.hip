@@ -413,12 +413,33 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
     const int prev_addr = (kq > 0 ? lane - 16 : lane + 47) << 2;
 
     const int64_t ngroups = (T + TPW - 1) / TPW;
-    for (int64_t grp = (int64_t)blockIdx.x * kEncWaves + wave; grp < ngroups;
-         grp += (int64_t)gridDim.x * kEncWaves) {
+    const int64_t gstride = (int64_t)gridDim.x * kEncWaves;
+    // bf16 rows of two tokens with d <= 1024 (d a multiple of 8): the next
+    // group's rows are requested while this group is encoded
+    const bool pf = X_BF16 && TPW == 2 && d <= 1024 && (d & 7) == 0;
+    u32x4 nx[4];
+    auto fetch = [&](int64_t gp) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int tt = e >> 1, o = (e & 1) * 512 + lane * 8;
+            const int64_t t = gp * TPW + tt;
+            nx[e] = (o < d && t < T) ? *(const u32x4*)((const uint16_t*)xin + t * d + o) : u32x4{0u, 0u, 0u, 0u};
+        }
+    };
+    int64_t grp = (int64_t)blockIdx.x * kEncWaves + wave;
+    if (pf && grp < ngroups) fetch(grp);
+    for (; grp < ngroups; grp += gstride) {
         const int64_t t0 = grp * TPW;
         const int ntok = (int)min((int64_t)TPW, T - t0);
 
-        if constexpr (X_BF16) {
+        if (pf) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int o = (e & 1) * 512 + lane * 8;
+                if (o < dp) store_pair_piece(lane, nx[e], o, pairs + (e >> 1) * P.prow);
+            }
+            if (grp + gstride < ngroups) fetch(grp + gstride);
+        } else if constexpr (X_BF16) {
             load_pairs(P, lane, ntok, TPW, (const uint16_t*)xin, t0, pairs);
         } else {
             const float* xs = (const float*)xin;

@@ -127,6 +127,28 @@ __device__ f32x4 mfma_scores(const DevPlan& P, int lane, int l, int mb, int trow
 // 4c + h reads coordinates 32c + 8h .. 32c + 8h + 7 (one 16-byte load when d
 // is a multiple of 8); lanes h and h + 2 of a quad swap two dwords so that
 // each lane writes four complete dwords with one 16-byte store.
+// One 8-coordinate piece (coordinates o .. o + 7) of a bf16 row, loaded by
+// lane (o / 8) mod 64, stored in the interleaved-halves layout of the row prow:
+// lane h < 2 of a quad keeps coordinates 8h + 0..3 and takes 16 + 8h + 0..3
+// from lane h + 2; lane h + 2 keeps 16 + 8h + 4..7 and takes 8h + 4..7 from
+// lane h.  Every lane of the wave must call it (lane exchanges).
+__device__ __forceinline__ void store_pair_piece(int lane, u32x4 q, int o, uint32_t* prow)
+{
+    const int h = lane & 3;
+    const bool lowq = h < 2;
+    const uint32_t s0 = lowq ? q.z : q.x, s1 = lowq ? q.w : q.y;
+    const uint32_t r0 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)s0, 0x4E, 0xF, 0xF, false);
+    const uint32_t r1 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)s1, 0x4E, 0xF, 0xF, false);
+    const uint32_t l0 = lowq ? q.x : r0, l1 = lowq ? q.y : r1;
+    const uint32_t h0 = lowq ? r0 : q.z, h1 = lowq ? r1 : q.w;
+    u32x4 w;
+    w.x = __builtin_amdgcn_perm(h0, l0, 0x05040100u);
+    w.y = __builtin_amdgcn_perm(h0, l0, 0x07060302u);
+    w.z = __builtin_amdgcn_perm(h1, l1, 0x05040100u);
+    w.w = __builtin_amdgcn_perm(h1, l1, 0x07060302u);
+    *(u32x4*)(prow + (o >> 5) * 16 + 8 * (h & 1) + 4 * (h >> 1)) = w;
+}
+
 __device__ inline void load_pairs(const DevPlan& P, int lane, int ntok, int tpw, const uint16_t* src, int64_t row0,
                                   uint32_t* pairs)
 {
