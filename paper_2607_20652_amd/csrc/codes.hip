@@ -120,6 +120,9 @@ __device__ __forceinline__ uint32_t transpose32(uint32_t x, int lane)
     return x;
 }
 
+template <int NG, int LG, bool PB16>
+__device__ __forceinline__ void fr_coords(const DevPlan& P, const Wave& W, int tt, int Wn, bool first, int pbpos, int pbn);
+
 // Table decode ("four Russians") of the n <= fr_cap slots listed in
 // W.fri / W.frc for token tt.  For a coordinate iota the signs of the listed
 // slots form bit words U(iota), bit j = parity(M_iota & fri[j]) (App. A.4,
@@ -171,6 +174,18 @@ __device__ void fr_chunk(const DevPlan& P, const Wave& W, int tt, int n, bool fi
     }
     wave_sync();
 
+    // a single word with at most 24 slots skips its last two groups
+    if (Wn == 1 && n <= 24) fr_coords<NG, 6, PB16>(P, W, tt, Wn, first, pbpos, pbn);
+    else fr_coords<NG, 8, PB16>(P, W, tt, Wn, first, pbpos, pbn);
+    wave_sync();
+}
+
+// Coordinate loop of the table decode over Wn words; LG (even, <= 8) groups
+// of each word are summed (the others hold no slot).
+template <int NG, int LG, bool PB16>
+__device__ __forceinline__ void fr_coords(const DevPlan& P, const Wave& W, int tt, int Wn, bool first, int pbpos, int pbn)
+{
+    const int lane = W.lane, dp = P.dp;
     const uint32_t vbase = lds_addr(W.frv), tbase = lds_addr(W.frt);
     float* yt = W.y + tt * dp;
     const int w0 = pbpos >> 5, sh = pbpos & 31;
@@ -189,12 +204,10 @@ __device__ void fr_chunk(const DevPlan& P, const Wave& W, int tt, int n, bool fi
             for (int g = 0; g < NG; ++g)
                 U ^= lds_ld(__builtin_amdgcn_perm(vb, (g & 1) ? s1 : s0, 0x07060500u | (uint32_t)(g >> 1)) +
                             (uint32_t)(g * 64));
+            const uint32_t e4 = (U << 2) & 0x3C3C3C3Cu, o4 = (U >> 2) & 0x3C3C3C3Cu;
 #pragma unroll
-            for (int i8 = 0; i8 < 8; ++i8) {
-                // frt is 64-byte aligned: the nibble goes in with one and-or
-                const uint32_t sh4 = i8 == 0 ? (U << 2) : (U >> (4 * i8 - 2));
-                acc += lds_ldf(((sh4 & 0x3Cu) | tb) + (uint32_t)(i8 * 64));
-            }
+            for (int i8 = 0; i8 < LG; ++i8)
+                acc += lds_ldf(__builtin_amdgcn_perm(tb, (i8 & 1) ? o4 : e4, 0x07060500u | (uint32_t)(i8 >> 1)) + (uint32_t)(i8 * 64));
             lo = w == w0 ? U : lo;
             hi = w == w0 + 1 ? U : hi;
         }
@@ -206,7 +219,6 @@ __device__ void fr_chunk(const DevPlan& P, const Wave& W, int tt, int n, bool fi
             else ((uint8_t*)W.pb)[tt * dp + iota] = (uint8_t)bits;
         }
     }
-    wave_sync();
 }
 
 // Decode of the wave's tokens from W.idx and coefficients `cf` into W.y.
@@ -270,20 +282,24 @@ __device__ void decode_tokens(const DevPlan& P, const Wave& W, const float* cf)
         wave_sync();
     }
 
-    // table decode of every slot not taken by a column, in chunks of fr_cap
-    const int pbpos = cols ? P.slot_base[L1 - 1] : 0, pbn = cols ? P.active[L1 - 1] : 0, cap = P.fr_cap;
+    // table decode of every non-basis slot not taken by a column, in chunks of
+    // fr_cap.  The leaf parents (slots sbP .. sbL - 1) are always listed, at
+    // consecutive positions from pbpos, for their sign bits.
+    const int sbP = cols ? P.slot_base[L1 - 1] : k, pbn = cols ? P.active[L1 - 1] : 0, cap = P.fr_cap;
     for (int tt = 0; tt < W.ntok; ++tt) {
         const int32_t* it = W.idx + tt * k;
         const int32_t* rt = W.route + tt * k;
         const float* ct = cf + tt * k;
+        int pbpos = 0;
         for (int cs = 0;; cs += cap) {
             int base = 0;
             for (int s0 = 0; s0 < k; s0 += 64) {
                 const int s = s0 + lane;
                 const int32_t c = s < k ? it[s] : -1;
                 const bool claimed = s < k && rt[s] >= 0 && (rt[s] & kClaimed);
-                const bool take = s < k && (s < sbL || (!claimed && c >= d));
+                const bool take = s < k && ((s >= sbP && s < sbL) || (c >= d && (s < sbL || !claimed)));
                 const uint64_t m = __ballot(take);
+                if (s0 <= sbP && sbP < s0 + 64) pbpos = base + (int)__popcll(m & ((1ull << (sbP - s0)) - 1ull));
                 const int pos = base + (int)__popcll(m & ((1ull << lane) - 1ull)) - cs;
                 if (take && pos >= 0 && pos < cap) {
                     W.fri[pos] = c > 0 ? c : 0;

@@ -216,7 +216,8 @@ def test_decode_arbitrary_codes(name):
 def _mixed_codes(name, T, seed=21):
     """Encoder codes with edits: a repeated last-level slot (two slots compete
     for one parent column), unroutable indices, a basis index in a hashed
-    level, a hashed index in level 0, and padding."""
+    level, a hashed index in level 0, and padding in the last level, among
+    its parents and below them."""
     w, m, oi, oc = _oracle_codes(name, T)
     nb, _, K = oracle.hierarchy(w.d, w.n, w.levels, w.branching, w.beam, w.k)
     rng = np.random.default_rng(seed)
@@ -228,6 +229,10 @@ def _mixed_codes(name, T, seed=21):
     idx[::5, K[0]] = rng.integers(0, w.d, size=idx[::5].shape[0])
     idx[::7, 1] = rng.integers(w.d, 1 << w.n, size=idx[::7].shape[0])
     idx[3::7, 2] = idx[3::7, 0]        # a basis coordinate held twice
+    lp = sum(K[:-2])                   # first slot of the last level's parents
+    idx[2::6, lp + 1] = -1             # padding among the last level's parents
+    if len(K) >= 4:
+        idx[5::8, K[0] + 1] = -1       # padding in a level below them
     coef[:, last + 4] *= -3.0
     return w, m, idx, coef
 
