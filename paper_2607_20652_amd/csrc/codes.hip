@@ -32,7 +32,8 @@ namespace dpb {
 namespace {
 
 constexpr int kThreads = 64 * kCodeWaves;
-constexpr int kBatch = 8;  // column-decode fragments fetched per batch
+constexpr int kBatch = 8;     // leaf columns decoded per batch
+constexpr int kBwdBatch = 4;  // the same in the backward, whose scoring leaves fewer registers
 
 struct Wave {
     int lane;
@@ -221,10 +222,109 @@ __device__ __forceinline__ void fr_coords(const DevPlan& P, const Wave& W, int t
     }
 }
 
+// Gamma^T alpha of the last level's columns on the matrix cores (16x16x16,
+// alpha split exactly into bf16 terms), each column multiplied by its
+// parent's signs (bits of W.pb) and added to y.  A lane holds four columns
+// of one token at one coordinate; the lanes of a token's CPT columns are
+// summed by a swizzle (and a permute), after which they hold bit-identical
+// sums (each addition is commutative).
+template <bool EXACT3>
+__device__ __forceinline__ float column_sum(bf16x4 ahi, bf16x4 amid, bf16x4 alo, u32x2 bfe, uint32_t pv)
+{
+    const bf16x4 b = __builtin_bit_cast(bf16x4, bfe);
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ahi, b, acc, 0, 0, 0);
+    if constexpr (EXACT3) acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(amid, b, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(alo, b, acc, 0, 0, 0);
+    return (__uint_as_float(__float_as_uint(acc[0]) ^ (pv << 31)) +
+            __uint_as_float(__float_as_uint(acc[1]) ^ ((pv >> 1) << 31))) +
+           (__uint_as_float(__float_as_uint(acc[2]) ^ ((pv >> 2) << 31)) +
+            __uint_as_float(__float_as_uint(acc[3]) ^ ((pv >> 3) << 31)));
+}
+
+// Leaf columns when every lane's column belongs to a live token (CPT
+// parents, 16 / CPT tokens, all present): each lane of a token's group
+// writes the same sum, so there are no masked stores or branches and the
+// compiler overlaps the NB columns of a batch.
+template <int CPT, bool EXACT3, bool PB16, int NB>
+__device__ __forceinline__ void leaf_columns(const DevPlan& P, const Wave& W, bf16x4 ahi, bf16x4 amid, bf16x4 alo)
+{
+    constexpr int CSH = CPT == 4 ? 2 : CPT == 8 ? 3 : 4;
+    const int L1 = P.levels - 1, dp = P.dp, lane = W.lane;
+    const int row = lane & 15, grp = lane >> 4;
+    const u32x2* bfr = (const u32x2*)P.gamma_t + P.gamma_t_off[L1] + lane;
+    const int tok = (4 * grp) >> CSH, q0 = (4 * grp) & (CPT - 1);
+    const int pbo = tok * dp + row;
+    float* yt = W.y + pbo;
+    const int x32 = ((lane ^ 32) << 2);
+    const int ncb = dp / 16;
+    auto pb_at = [&](int cb) -> uint32_t {
+        if constexpr (PB16) return (uint32_t)((const uint16_t*)W.pb)[pbo + 16 * cb] >> q0;
+        else return (uint32_t)((const uint8_t*)W.pb)[pbo + 16 * cb] >> q0;
+    };
+    auto token_sum = [&](float v) {
+        if constexpr (CPT >= 8) v += swz_xorf16(v);
+        if constexpr (CPT >= 16) v += __int_as_float(__builtin_amdgcn_ds_bpermute(x32, __float_as_int(v)));
+        return v;
+    };
+    int cb0 = 0;
+    for (; cb0 + NB <= ncb; cb0 += NB) {
+        u32x2 bf[NB];
+        uint32_t pbv[NB];
+#pragma unroll
+        for (int e = 0; e < NB; ++e) {
+            bf[e] = bfr[(int64_t)(cb0 + e) * 64];
+            pbv[e] = pb_at(cb0 + e);
+        }
+        float v[NB];
+#pragma unroll
+        for (int e = 0; e < NB; ++e) v[e] = token_sum(column_sum<EXACT3>(ahi, amid, alo, bf[e], pbv[e]));
+#pragma unroll
+        for (int e = 0; e < NB; ++e) yt[16 * (cb0 + e)] += P.rsd * v[e];
+    }
+    for (int cb = cb0; cb < ncb; ++cb)   // the last, partial batch
+        yt[16 * cb] += P.rsd * token_sum(column_sum<EXACT3>(ahi, amid, alo, bfr[(int64_t)cb * 64], pb_at(cb)));
+}
+
+// Leaf columns in general: CPT from the plan, one writer lane per token and
+// coordinate, none for absent tokens.
+template <bool EXACT3, bool PB16>
+__device__ __forceinline__ void leaf_columns_any(const DevPlan& P, const Wave& W, bf16x4 ahi, bf16x4 amid, bf16x4 alo)
+{
+    const int L1 = P.levels - 1, TPW = P.wave_tokens, dp = P.dp, lane = W.lane;
+    const int row = lane & 15, grp = lane >> 4;
+    const int CPT = P.cpt[L1];
+    const u32x2* bfr = (const u32x2*)P.gamma_t + P.gamma_t_off[L1] + lane;
+    const int tok = (4 * grp) >> P.cpt_shift[L1], q0 = (4 * grp) & (CPT - 1);
+    const bool writer = (grp & ((CPT >> 2) - 1)) == 0 && tok < W.ntok;
+    const int pbo = (tok < TPW ? tok : 0) * dp + row;
+    float* yt = W.y + pbo;
+    const int x32 = ((lane ^ 32) << 2);
+    const int ncb = dp / 16;
+    for (int cb0 = 0; cb0 < ncb; cb0 += kBatch) {
+        u32x2 bf[kBatch];
+        uint32_t pbv[kBatch];
+#pragma unroll
+        for (int e = 0; e < kBatch; ++e) {
+            const int cb = cb0 + e < ncb ? cb0 + e : ncb - 1;
+            bf[e] = bfr[(int64_t)cb * 64];
+            if constexpr (PB16) pbv[e] = (uint32_t)((const uint16_t*)W.pb)[pbo + 16 * cb] >> q0;
+            else pbv[e] = (uint32_t)((const uint8_t*)W.pb)[pbo + 16 * cb] >> q0;
+        }
+#pragma unroll
+        for (int e = 0; e < kBatch; ++e) {
+            float v = column_sum<EXACT3>(ahi, amid, alo, bf[e], pbv[e]);
+            if (CPT >= 8) v += swz_xorf16(v);
+            if (CPT >= 16) v += __int_as_float(__builtin_amdgcn_ds_bpermute(x32, __float_as_int(v)));
+            if (writer && cb0 + e < ncb) yt[16 * (cb0 + e)] += P.rsd * v;
+        }
+    }
+}
+
 // Decode of the wave's tokens from W.idx and coefficients `cf` into W.y.
 // W.route holds the routes of the last level's slots (when decoding through
 // leaf columns).  PB16: the leaf parents' sign bits take 16 bits (else 8).
-template <bool EXACT3, int NG, bool PB16>
+template <bool EXACT3, int NG, bool PB16, int LCB>
 __device__ void decode_tokens(const DevPlan& P, const Wave& W, const float* cf)
 {
     const int k = P.k_tot, d = P.d, dp = P.dp, TPW = P.wave_tokens, lane = W.lane;
@@ -316,42 +416,15 @@ __device__ void decode_tokens(const DevPlan& P, const Wave& W, const float* cf)
     }
 
     if (cols) {
-        // Gamma^T alpha on the matrix cores, then the parent's signs
+        // Gamma^T alpha on the matrix cores, then the parents' signs.  With
+        // every column a live token's (full waves of two tokens of eight
+        // parents) all lanes write.
         const int CPT = P.cpt[L1];
-        const u32x2* bfr = (const u32x2*)P.gamma_t + P.gamma_t_off[L1] + lane;
-        const int tok = (4 * grp) >> P.cpt_shift[L1], q0 = (4 * grp) & (CPT - 1);
-        const bool writer = (grp & ((CPT >> 2) - 1)) == 0 && tok < W.ntok;
-        const int pbo = (tok < TPW ? tok : 0) * dp + row;
-        float* yt = W.y + pbo;
-        const int x32 = ((lane ^ 32) << 2);
-        const int ncb = dp / 16;
-        for (int cb0 = 0; cb0 < ncb; cb0 += kBatch) {
-            u32x2 bf[kBatch];
-            uint32_t pbv[kBatch];
-#pragma unroll
-            for (int e = 0; e < kBatch; ++e) {
-                const int cb = cb0 + e < ncb ? cb0 + e : ncb - 1;
-                bf[e] = bfr[(int64_t)cb * 64];
-                if constexpr (PB16) pbv[e] = (uint32_t)((const uint16_t*)W.pb)[pbo + 16 * cb] >> q0;
-                else pbv[e] = (uint32_t)((const uint8_t*)W.pb)[pbo + 16 * cb] >> q0;
-            }
-#pragma unroll
-            for (int e = 0; e < kBatch; ++e) {
-                const bf16x4 b = __builtin_bit_cast(bf16x4, bf[e]);
-                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-                acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ahi, b, acc, 0, 0, 0);
-                if constexpr (EXACT3) acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(amid, b, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(alo, b, acc, 0, 0, 0);
-                const uint32_t pv = pbv[e];
-                float v = (__uint_as_float(__float_as_uint(acc[0]) ^ (pv << 31)) +
-                           __uint_as_float(__float_as_uint(acc[1]) ^ ((pv >> 1) << 31))) +
-                          (__uint_as_float(__float_as_uint(acc[2]) ^ ((pv >> 2) << 31)) +
-                           __uint_as_float(__float_as_uint(acc[3]) ^ ((pv >> 3) << 31)));
-                if (CPT >= 8) v += swz_xorf16(v);
-                if (CPT >= 16) v += __int_as_float(__builtin_amdgcn_ds_bpermute(x32, __float_as_int(v)));
-                if (writer && cb0 + e < ncb) yt[16 * (cb0 + e)] += P.rsd * v;
-            }
-        }
+        const bool all = TPW * CPT == 16 && W.ntok == TPW;
+        // (one compile-time layout only: more of them inlined here cost the
+        // kernels registers, and with them a wave per SIMD)
+        if (CPT == 8 && all) leaf_columns<8, EXACT3, PB16, LCB>(P, W, ahi, amid, alo);
+        else leaf_columns_any<EXACT3, PB16>(P, W, ahi, amid, alo);
         wave_sync();
     }
 
@@ -560,7 +633,7 @@ __global__ __launch_bounds__(kThreads) void decode2_kernel(DevPlan P, const int3
             route_slots(P, W, P.levels - 1);
             wave_sync();
         }
-        decode_tokens<!OUT_BF16, NG, PB16>(P, W, W.coef);
+        decode_tokens<!OUT_BF16, NG, PB16, kBatch>(P, W, W.coef);
         write_rows<OUT_BF16>(P, W, y);
         wave_sync();
     }
@@ -804,7 +877,7 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
         }
 
         // grad_x = decode(idx, grad_coef) (+ add_gx); the scoring buffers are dead now
-        decode_tokens<!GX_BF16, NG, PB16>(P, W, W.coef);
+        decode_tokens<!GX_BF16, NG, PB16, kBwdBatch>(P, W, W.coef);
         write_rows<GX_BF16>(P, W, grad_x, add_gx);
         wave_sync();
     }
