@@ -33,7 +33,8 @@ namespace {
 
 constexpr int kThreads = 64 * kCodeWaves;
 constexpr int kBatch = 8;     // leaf columns decoded per batch
-constexpr int kBwdBatch = 4;  // the same in the backward, whose scoring leaves fewer registers
+constexpr int kBwdBatch = 4;
+constexpr int kDecodeUnroll = 4;  // coordinates of the table decode overlapped (2 in the backward, for registers)  // the same in the backward, whose scoring leaves fewer registers
 
 struct Wave {
     int lane;
@@ -123,6 +124,8 @@ __device__ __forceinline__ uint32_t transpose32(uint32_t x, int lane)
 
 template <int NG, int LG, bool PB16>
 __device__ __forceinline__ void fr_coords(const DevPlan& P, const Wave& W, int tt, int Wn, bool first, int pbpos, int pbn);
+template <int NG, int LG, bool PB16, int FRU>
+__device__ __forceinline__ void fr_coords1(const DevPlan& P, const Wave& W, int tt, int pbpos, int pbn);
 
 // Table decode ("four Russians") of the n <= fr_cap slots listed in
 // W.fri / W.frc for token tt.  For a coordinate iota the signs of the listed
@@ -135,7 +138,7 @@ __device__ __forceinline__ void fr_coords(const DevPlan& P, const Wave& W, int t
 // `first` overwrites y, otherwise adds.  When pbn > 0, bits pbpos ..
 // pbpos + pbn - 1 of U (the leaf level's parents) are stored in W.pb.
 // NG = number of 4-bit groups of the widest index.
-template <int NG, bool PB16>
+template <int NG, bool PB16, int FRU>
 __device__ void fr_chunk(const DevPlan& P, const Wave& W, int tt, int n, bool first, int pbpos, int pbn)
 {
     const int lane = W.lane, dp = P.dp;
@@ -176,8 +179,14 @@ __device__ void fr_chunk(const DevPlan& P, const Wave& W, int tt, int n, bool fi
     wave_sync();
 
     // a single word with at most 24 slots skips its last two groups
-    if (Wn == 1 && n <= 24) fr_coords<NG, 6, PB16>(P, W, tt, Wn, first, pbpos, pbn);
-    else fr_coords<NG, 8, PB16>(P, W, tt, Wn, first, pbpos, pbn);
+    if (Wn == 1 && first && pbn > 0) {
+        if (n <= 24) fr_coords1<NG, 6, PB16, FRU>(P, W, tt, pbpos, pbn);
+        else fr_coords1<NG, 8, PB16, FRU>(P, W, tt, pbpos, pbn);
+    } else if (Wn == 1 && n <= 24) {
+        fr_coords<NG, 6, PB16>(P, W, tt, Wn, first, pbpos, pbn);
+    } else {
+        fr_coords<NG, 8, PB16>(P, W, tt, Wn, first, pbpos, pbn);
+    }
     wave_sync();
 }
 
@@ -219,6 +228,36 @@ __device__ __forceinline__ void fr_coords(const DevPlan& P, const Wave& W, int t
             if constexpr (PB16) ((uint16_t*)W.pb)[tt * dp + iota] = (uint16_t)bits;
             else ((uint8_t*)W.pb)[tt * dp + iota] = (uint8_t)bits;
         }
+    }
+}
+
+// The common case of the coordinate loop: one word, the first write of y,
+// the leaf parents' sign bits inside the word.  The body has no branches,
+// so the compiler overlaps the table reads of consecutive coordinates.
+template <int NG, int LG, bool PB16, int FRU>
+__device__ __forceinline__ void fr_coords1(const DevPlan& P, const Wave& W, int tt, int pbpos, int pbn)
+{
+    const int lane = W.lane, dp = P.dp;
+    const uint32_t vb = lds_addr(W.frv), tb = lds_addr(W.frt);
+    float* yt = W.y + tt * dp;
+    const uint32_t pmask = (1u << pbn) - 1u;   // pbpos + pbn <= 32
+#pragma unroll FRU
+    for (int iota = lane; iota < dp; iota += 64) {
+        const uint32_t M = W.mask[iota];
+        const uint32_t s0 = (M << 2) & 0x3C3C3C3Cu, s1 = (M >> 2) & 0x3C3C3C3Cu;
+        uint32_t U = 0;
+#pragma unroll
+        for (int g = 0; g < NG; ++g)
+            U ^= lds_ld(__builtin_amdgcn_perm(vb, (g & 1) ? s1 : s0, 0x07060500u | (uint32_t)(g >> 1)) + (uint32_t)(g * 64));
+        const uint32_t e4 = (U << 2) & 0x3C3C3C3Cu, o4 = (U >> 2) & 0x3C3C3C3Cu;
+        float acc = 0.f;
+#pragma unroll
+        for (int i8 = 0; i8 < LG; ++i8)
+            acc += lds_ldf(__builtin_amdgcn_perm(tb, (i8 & 1) ? o4 : e4, 0x07060500u | (uint32_t)(i8 >> 1)) + (uint32_t)(i8 * 64));
+        yt[iota] = acc;
+        const uint32_t bits = (U >> pbpos) & pmask;
+        if constexpr (PB16) ((uint16_t*)W.pb)[tt * dp + iota] = (uint16_t)bits;
+        else ((uint8_t*)W.pb)[tt * dp + iota] = (uint8_t)bits;
     }
 }
 
@@ -324,7 +363,7 @@ __device__ __forceinline__ void leaf_columns_any(const DevPlan& P, const Wave& W
 // Decode of the wave's tokens from W.idx and coefficients `cf` into W.y.
 // W.route holds the routes of the last level's slots (when decoding through
 // leaf columns).  PB16: the leaf parents' sign bits take 16 bits (else 8).
-template <bool EXACT3, int NG, bool PB16, int LCB>
+template <bool EXACT3, int NG, bool PB16, int LCB, int FRU>
 __device__ void decode_tokens(const DevPlan& P, const Wave& W, const float* cf)
 {
     const int k = P.k_tot, d = P.d, dp = P.dp, TPW = P.wave_tokens, lane = W.lane;
@@ -410,7 +449,7 @@ __device__ void decode_tokens(const DevPlan& P, const Wave& W, const float* cf)
             const int n = max(0, min(base - cs, cap));
             for (int j = n + lane; j < ((n + 31) & ~31); j += 64) W.frc[j] = 0.f;  // zero the rest of the last word
             wave_sync();
-            fr_chunk<NG, PB16>(P, W, tt, n, cs == 0, pbpos - cs, (pbpos >= cs && pbpos < cs + cap) ? pbn : 0);
+            fr_chunk<NG, PB16, FRU>(P, W, tt, n, cs == 0, pbpos - cs, (pbpos >= cs && pbpos < cs + cap) ? pbn : 0);
             if (base <= cs + cap) break;
         }
     }
@@ -633,7 +672,7 @@ __global__ __launch_bounds__(kThreads) void decode2_kernel(DevPlan P, const int3
             route_slots(P, W, P.levels - 1);
             wave_sync();
         }
-        decode_tokens<!OUT_BF16, NG, PB16, kBatch>(P, W, W.coef);
+        decode_tokens<!OUT_BF16, NG, PB16, kBatch, kDecodeUnroll>(P, W, W.coef);
         write_rows<OUT_BF16>(P, W, y);
         wave_sync();
     }
@@ -877,7 +916,7 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
         }
 
         // grad_x = decode(idx, grad_coef) (+ add_gx); the scoring buffers are dead now
-        decode_tokens<!GX_BF16, NG, PB16, kBwdBatch>(P, W, W.coef);
+        decode_tokens<!GX_BF16, NG, PB16, kBwdBatch, 2>(P, W, W.coef);
         write_rows<GX_BF16>(P, W, grad_x, add_gx);
         wave_sync();
     }
