@@ -479,9 +479,19 @@ __device__ void decode_tokens(const DevPlan& P, const Wave& W, const float* cf)
             uint64_t m = __ballot(basis);
             if (!m) continue;
             bool dup = false;
-            for (uint64_t mm = m; mm; mm &= mm - 1) {
-                const int b = __builtin_ctzll(mm);
-                dup |= basis && b < lane && rdlane(c, b) == c;
+            if (cols) {
+                // the leaf parents' sign bytes are dead now: each basis lane
+                // marks its coordinate; a lane that reads back another lane's
+                // mark shares the coordinate with it
+                uint8_t* mark = (uint8_t*)W.pb + tt * dp;
+                if (basis) mark[c] = (uint8_t)lane;
+                wave_sync();
+                dup = basis && mark[c] != (uint8_t)lane;
+            } else {
+                for (uint64_t mm = m; mm; mm &= mm - 1) {
+                    const int b = __builtin_ctzll(mm);
+                    dup |= basis && b < lane && rdlane(c, b) == c;
+                }
             }
             if (!__ballot(dup)) {
                 if (basis) W.y[tt * dp + c] += __int_as_float(a);
