@@ -44,13 +44,16 @@ __device__ void column_bitmaps(const DevPlan& P, int lane, int ntok, int csh, in
     // nibble table layout [g][w][16]: word w of group g for nibble value v at (g * nchunk + w) * 16 + v
     for (int wb = 0; wb < nchunk; wb += 4 * MW) {
         uint32_t acc[MW];
+        int woff[MW];   // words past nchunk read the last word (in bounds) and are not stored
 #pragma unroll
-        for (int m = 0; m < MW; ++m) acc[m] = 0;
+        for (int m = 0; m < MW; ++m) {
+            acc[m] = 0;
+            woff[m] = min(wb + w0 + 4 * m, nchunk - 1) * 16;
+        }
         for (int g = 0; g < P.nt_groups; ++g) {
-            const uint32_t* rg = nt + (g * nchunk + wb + w0) * 16 + ((pu >> (4 * g)) & 15u);
+            const uint32_t* rg = nt + g * nchunk * 16 + ((pu >> (4 * g)) & 15u);
 #pragma unroll
-            for (int m = 0; m < MW; ++m)
-                if (wb + w0 + 4 * m < nchunk) acc[m] ^= rg[m * 64];
+            for (int m = 0; m < MW; ++m) acc[m] ^= rg[woff[m]];
         }
 #pragma unroll
         for (int m = 0; m < MW; ++m) {

@@ -177,7 +177,7 @@ def _oracle_codes(name, T):
     return w, m, oi, oc.astype(np.float32)
 
 
-@pytest.mark.parametrize("name,T", [("tiny", 256), ("gpt2", 777), ("wide", 300), ("very_wide", 130)])
+@pytest.mark.parametrize("name,T", [("tiny", 256), ("gpt2", 777), ("wide", 300), ("wide", 301), ("very_wide", 130)])
 @pytest.mark.parametrize("out", ["f32", "bf16"])
 def test_decode_matches_oracle(name, T, out):
     say(f"[decode] {name} T={T} out={out}")
@@ -296,7 +296,7 @@ def test_decode_full_size_sampled(name):
 
 # ---------------------------------------------------------------- backward
 
-@pytest.mark.parametrize("name,T", [("tiny", 256), ("gpt2", 500), ("train", 300), ("very_wide", 120)])
+@pytest.mark.parametrize("name,T", [("tiny", 256), ("gpt2", 500), ("train", 300), ("train", 301), ("very_wide", 120)])
 def test_decode_bwd_matches_oracle(name, T):
     say(f"[bwd] {name} T={T}")
     plan = plan_for(name)
