@@ -105,19 +105,20 @@ __device__ void route_slots(const DevPlan& P, const Wave& W, int lmin)
 }
 
 // Bit transpose inside each 32-lane half: lane s of a half holds x_s on
-// entry; on exit lane b holds the word whose bit s is bit b of x_s.
+// entry; on exit lane b holds the word whose bit s is bit b of x_s.  The five
+// exchanges run on the vector ALU (a chain of LDS-path swizzles was slower).
 __device__ __forceinline__ uint32_t transpose32(uint32_t x, int lane)
 {
     uint32_t o;
-    o = swz_xor<16>(x);
+    o = lane_xor<16>(x);
     x = (lane & 16) ? ((x & 0xFFFF0000u) | ((o >> 16) & 0x0000FFFFu)) : ((x & 0x0000FFFFu) | ((o & 0x0000FFFFu) << 16));
-    o = swz_xor<8>(x);
+    o = lane_xor<8>(x);
     x = (lane & 8) ? ((x & 0xFF00FF00u) | ((o >> 8) & 0x00FF00FFu)) : ((x & 0x00FF00FFu) | ((o & 0x00FF00FFu) << 8));
-    o = swz_xor<4>(x);
+    o = lane_xor<4>(x);
     x = (lane & 4) ? ((x & 0xF0F0F0F0u) | ((o >> 4) & 0x0F0F0F0Fu)) : ((x & 0x0F0F0F0Fu) | ((o & 0x0F0F0F0Fu) << 4));
-    o = swz_xor<2>(x);
+    o = lane_xor<2>(x);
     x = (lane & 2) ? ((x & 0xCCCCCCCCu) | ((o >> 2) & 0x33333333u)) : ((x & 0x33333333u) | ((o & 0x33333333u) << 2));
-    o = swz_xor<1>(x);
+    o = lane_xor<1>(x);
     x = (lane & 1) ? ((x & 0xAAAAAAAAu) | ((o >> 1) & 0x55555555u)) : ((x & 0x55555555u) | ((o & 0x55555555u) << 1));
     return x;
 }

@@ -80,7 +80,8 @@ __host__ __device__ inline unsigned enc_shared_bytes(const DevPlan& P, bool std)
 }
 
 // Exchange with the lane whose index differs by m (a power of two): DPP for
-// 1 and 2, swizzles up to 16, a permute for 32.
+// 1 and 2, swizzles up to 16, a permute for 32 (the LDS-path exchanges cost
+// no vector-ALU slots, which the encoder is short of).
 __device__ __forceinline__ uint32_t xlane(uint32_t v, int m, int x32addr)
 {
     switch (m) {
