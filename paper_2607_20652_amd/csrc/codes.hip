@@ -802,6 +802,8 @@ __device__ void direct_scores(const DevPlan& P, const Wave& W)
             for (int w = part; w < nchunk; w += 1 << sh) {
                 const uint32_t word = fold_words();
                 fetch_words(min(w + (1 << sh), nchunk - 1));
+                // keeps the compiler from sinking those loads to their use
+                __asm__ volatile("" ::: "memory");
                 if constexpr (G_BF16) {
                     const u32x4* pr = (const u32x4*)(W.pairs + tt * P.prow + w * 16);
 #pragma unroll
