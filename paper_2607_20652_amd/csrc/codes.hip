@@ -32,7 +32,7 @@ namespace dpb {
 namespace {
 
 constexpr int kThreads = 64 * kCodeWaves;
-constexpr int kBatch = 8;     // leaf columns decoded per batch
+constexpr int kBatch = 16;    // leaf columns decoded per batch
 constexpr int kBwdBatch = 4;
 constexpr int kDecodeUnroll = 4;  // coordinates of the table decode overlapped (2 in the backward, for registers)  // the same in the backward, whose scoring leaves fewer registers
 
