@@ -484,7 +484,7 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
 #pragma unroll
             for (int mb = 0; mb < R / 4; ++mb) {
                 f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-                if (mb < P.mblocks[l]) acc = mfma_scores<X_BF16>(P, lane, l, mb, trow, A, cw);
+                if (mb < P.mblocks[l]) acc = mfma_scores<X_BF16, 6>(P, lane, l, mb, trow, A, cw);   // batches of 6 chunks: faster here than 4, 8 or 12
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int j = 16 * mb + 4 * kq + i;

@@ -17,7 +17,7 @@
 
 namespace dpb {
 
-constexpr int kScoreBatch = 8;  // A fragments fetched per batch
+constexpr int kScoreBatch = 8;  // A fragments fetched per batch (the encoder takes 6: see its call)
 
 // A wave's activations in LDS.
 struct ActTile {
@@ -100,7 +100,7 @@ __device__ __forceinline__ void score_chunk(const DevPlan& P, int kq, u32x4 a, u
     }
 }
 
-template <bool ACT_BF16>
+template <bool ACT_BF16, int SB = kScoreBatch>
 __device__ f32x4 mfma_scores(const DevPlan& P, int lane, int l, int mb, int trow, const ActTile& A, const uint32_t* cw)
 {
     const int nchunk = P.nchunk, dp = P.dp, col = lane & 15, kq = lane >> 4;
@@ -110,16 +110,16 @@ __device__ f32x4 mfma_scores(const DevPlan& P, int lane, int l, int mb, int trow
     const float* frow = A.f + trow * dp;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     int c0 = 0;
-    for (; c0 + kScoreBatch <= nchunk; c0 += kScoreBatch) {
-        u32x4 a[kScoreBatch];
-        uint32_t wd[kScoreBatch];
+    for (; c0 + SB <= nchunk; c0 += SB) {
+        u32x4 a[SB];
+        uint32_t wd[SB];
 #pragma unroll
-        for (int e = 0; e < kScoreBatch; ++e) {
+        for (int e = 0; e < SB; ++e) {
             a[e] = Ap[(int64_t)(c0 + e) * 64];
             wd[e] = cwp[c0 + e];
         }
 #pragma unroll
-        for (int e = 0; e < kScoreBatch; ++e) score_chunk<ACT_BF16>(P, kq, a[e], wd[e], prow, frow, c0 + e, acc);
+        for (int e = 0; e < SB; ++e) score_chunk<ACT_BF16>(P, kq, a[e], wd[e], prow, frow, c0 + e, acc);
     }
     for (; c0 < nchunk; ++c0) score_chunk<ACT_BF16>(P, kq, Ap[(int64_t)c0 * 64], cwp[c0], prow, frow, c0, acc);
     return acc;
