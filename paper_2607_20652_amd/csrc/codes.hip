@@ -953,13 +953,14 @@ int device_cus()
     return cus;
 }
 
-// Grid-stride launch: enough workgroups to fill the chip a few times over.
-dim3 code_grid(const DevPlan& P, int64_t T, size_t lds)
+// Grid-stride launch: `rounds` times the workgroups the chip holds at once
+// (measured best: one round for the decode, four for the backward).
+dim3 code_grid(const DevPlan& P, int64_t T, size_t lds, int rounds)
 {
     const int64_t groups = (T + P.wave_tokens - 1) / P.wave_tokens;
     const int64_t need = (groups + kCodeWaves - 1) / kCodeWaves;
     const int per_cu = lds ? (int)std::max<size_t>(1, (160 * 1024) / lds) : 4;
-    const int64_t cap = (int64_t)device_cus() * std::min(per_cu, 8) * 4;
+    const int64_t cap = (int64_t)device_cus() * std::min(per_cu, 8) * rounds;
     return dim3((unsigned)std::max<int64_t>(1, std::min(need, cap)));
 }
 
@@ -1004,7 +1005,7 @@ hipError_t launch_decode2(const DevPlan& P, const int32_t* idx, const float* coe
 {
     const size_t lds = code_lds_bytes(P, false, true);
     if (lds > (size_t)kLdsBudget) return hipErrorInvalidValue;
-    const dim3 grid = code_grid(P, T, lds);
+    const dim3 grid = code_grid(P, T, lds, 1);
     const bool pb16 = P.pb_bytes == 2;
     if (y_bf16 && pb16) launch_decode_ng<true, true>(P, grid, lds, stream, idx, coef, T, y);
     else if (y_bf16) launch_decode_ng<true, false>(P, grid, lds, stream, idx, coef, T, y);
@@ -1055,7 +1056,7 @@ hipError_t launch_decode_bwd2(const DevPlan& P, const int32_t* idx, const void* 
 {
     const size_t lds = code_lds_bytes(P, true, g_bf16);
     if (lds > (size_t)kLdsBudget) return hipErrorInvalidValue;
-    const dim3 grid = code_grid(P, T, lds);
+    const dim3 grid = code_grid(P, T, lds, 4);
     const BwdExtra ex{add_grad_coef, add_grad_x, (const float2*)stats};
     if (g_bf16 && gx_bf16) launch_bwd_ub<true, true>(P, grid, lds, stream, idx, g, T, grad_coef, grad_x, ex);
     else if (g_bf16) launch_bwd_ub<true, false>(P, grid, lds, stream, idx, g, T, grad_coef, grad_x, ex);
