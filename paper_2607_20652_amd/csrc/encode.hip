@@ -476,8 +476,11 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
             if constexpr (STD) {
 #pragma unroll
                 for (int e = 0; e < R; ++e) {
+                    // read unconditionally at an index that is always a
+                    // feature (a generator of the level when there is no parent)
                     const int j = 16 * (e >> 2) + 4 * kq + (e & 3);
-                    stv[e] = (valid && j < Dl) ? stats[(uint32_t)p ^ gens[j]] : make_float2(0.f, 1.f);
+                    const float2 v = stats[(valid ? (uint32_t)p : 0u) ^ gens[min(j, Dl - 1)]];
+                    stv[e] = (valid && j < Dl) ? v : make_float2(0.f, 1.f);
                 }
             }
             uint64_t keys[R];
