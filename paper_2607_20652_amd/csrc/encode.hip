@@ -470,24 +470,28 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
             const bool valid = p >= 0;
             const int trow = valid ? ct : 0;
             const uint32_t* gens = s_gens + P.gens_off[l];
-            // standardization statistics of this lane's children, requested
-            // before the scoring so that the gathers overlap it
+            // standardization statistics of this lane's children, gathered
+            // during the last batch of the first tile's scoring (read
+            // unconditionally at an index that is always a feature: a
+            // generator of the level when there is no parent)
             float2 stv[R];
-            if constexpr (STD) {
+            auto gather = [&]() {
+                if constexpr (STD) {
 #pragma unroll
-                for (int e = 0; e < R; ++e) {
-                    // read unconditionally at an index that is always a
-                    // feature (a generator of the level when there is no parent)
-                    const int j = 16 * (e >> 2) + 4 * kq + (e & 3);
-                    const float2 v = stats[(valid ? (uint32_t)p : 0u) ^ gens[min(j, Dl - 1)]];
-                    stv[e] = (valid && j < Dl) ? v : make_float2(0.f, 1.f);
+                    for (int e = 0; e < R; ++e) {
+                        const int j = 16 * (e >> 2) + 4 * kq + (e & 3);
+                        const float2 v = stats[(valid ? (uint32_t)p : 0u) ^ gens[min(j, Dl - 1)]];
+                        stv[e] = (valid && j < Dl) ? v : make_float2(0.f, 1.f);
+                    }
                 }
-            }
+            };
             uint64_t keys[R];
 #pragma unroll
             for (int mb = 0; mb < R / 4; ++mb) {
                 f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-                if (mb < P.mblocks[l]) acc = mfma_scores<X_BF16, 6>(P, lane, l, mb, trow, A, cw);   // batches of 6 chunks: faster here than 4, 8 or 12
+                // batches of 6 chunks: faster here than 4, 8 or 12
+                if (mb == 0) acc = mfma_scores<X_BF16, 6>(P, lane, l, mb, trow, A, cw, gather);
+                else if (mb < P.mblocks[l]) acc = mfma_scores<X_BF16, 6>(P, lane, l, mb, trow, A, cw);
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int j = 16 * mb + 4 * kq + i;

@@ -100,8 +100,16 @@ __device__ __forceinline__ void score_chunk(const DevPlan& P, int kq, u32x4 a, u
     }
 }
 
-template <bool ACT_BF16, int SB = kScoreBatch>
-__device__ f32x4 mfma_scores(const DevPlan& P, int lane, int l, int mb, int trow, const ActTile& A, const uint32_t* cw)
+struct NoLateLoads {
+    __device__ void operator()() const {}
+};
+
+// `late` is called once, right after the loads of the last batch are issued:
+// loads it issues then overlap that batch's work without holding up the
+// earlier batches (memory waits are in issue order).
+template <bool ACT_BF16, int SB = kScoreBatch, typename Late = NoLateLoads>
+__device__ f32x4 mfma_scores(const DevPlan& P, int lane, int l, int mb, int trow, const ActTile& A, const uint32_t* cw,
+                             Late late = Late())
 {
     const int nchunk = P.nchunk, dp = P.dp, col = lane & 15, kq = lane >> 4;
     const u32x4* Ap = (const u32x4*)P.gamma_pair + P.gamma_off[l] + (int64_t)mb * nchunk * 64 + lane;
@@ -118,9 +126,11 @@ __device__ f32x4 mfma_scores(const DevPlan& P, int lane, int l, int mb, int trow
             a[e] = Ap[(int64_t)(c0 + e) * 64];
             wd[e] = cwp[c0 + e];
         }
+        if (c0 + 2 * SB > nchunk) late();
 #pragma unroll
         for (int e = 0; e < SB; ++e) score_chunk<ACT_BF16>(P, kq, a[e], wd[e], prow, frow, c0 + e, acc);
     }
+    if (nchunk < SB) late();
     for (; c0 < nchunk; ++c0) score_chunk<ACT_BF16>(P, kq, Ap[(int64_t)c0 * 64], cwp[c0], prow, frow, c0, acc);
     return acc;
 }
