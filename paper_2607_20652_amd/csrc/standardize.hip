@@ -179,12 +179,15 @@ __global__ void std_col_update_kernel(int d, int64_t T, StdWs W, float2* stats, 
     ema(stats, var, c, (double)T, s1, s2, beta, eps);
 }
 
-// One workgroup per (sample token, level l >= 1): the token's candidates at
-// level l, each child once, scored <phi_c, x_t> from the definition.  The
-// candidate list and the row of x are staged in LDS; a candidate is a
-// duplicate when an earlier entry of the list holds the same child; each
-// wave scores one candidate at a time, lanes over the coordinates.
+// kStdSlices workgroups per (sample token, level l >= 1): the token's
+// candidates at level l, each child once, scored <phi_c, x_t> from the
+// definition.  The candidate list and the row of x are staged in LDS in each
+// workgroup; a candidate is a duplicate when an earlier entry of the list
+// holds the same child; each wave scores one candidate at a time, lanes over
+// the coordinates, and the slices of a list take turns (more waves in flight
+// for the few sampled tokens).
 constexpr int kStdMaxCand = 4096;
+constexpr int kStdSlices = 8;   // workgroups sharing one sampled token's candidates of a level
 
 template <bool BF16>
 __global__ __launch_bounds__(kStdThreads) void std_sample_kernel(DevPlan P, const void* x, int64_t T, int m,
@@ -192,7 +195,7 @@ __global__ __launch_bounds__(kStdThreads) void std_sample_kernel(DevPlan P, cons
 {
     __shared__ int32_t cand[kStdMaxCand];
     extern __shared__ __align__(16) float xrow[];
-    const int j = blockIdx.x, l = blockIdx.y + 1;
+    const int j = blockIdx.x, l = blockIdx.y + 1, z = blockIdx.z;
     const int64_t t = ((int64_t)j * T) / m;
     const int Kp = P.active[l - 1], Dl = P.delta[l], d = P.d, n = Kp * Dl;
     const int32_t* par = idx + t * P.k_tot + P.slot_base[l - 1];
@@ -207,30 +210,16 @@ __global__ __launch_bounds__(kStdThreads) void std_sample_kernel(DevPlan P, cons
     }
     for (int iota = threadIdx.x; iota < d; iota += kStdThreads) xrow[iota] = load_act<BF16>(x, t * d + iota);
     __syncthreads();
-    // a later copy of a child is marked (no later write to cand before the next barrier)
-    int32_t mine[kStdMaxCand / kStdThreads];
-#pragma unroll
-    for (int r = 0; r < kStdMaxCand / kStdThreads; ++r) {
-        const int e = threadIdx.x + r * kStdThreads;
-        int32_t c = e < n ? cand[e] : -1;
-        if (c >= 0)
-            for (int e2 = 0; e2 < e; ++e2)
-                if (cand[e2] == c) {
-                    c = -1;
-                    break;
-                }
-        mine[r] = c;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int r = 0; r < kStdMaxCand / kStdThreads; ++r) {
-        const int e = threadIdx.x + r * kStdThreads;
-        if (e < n) cand[e] = mine[r];
-    }
-    __syncthreads();
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    for (int e = wave; e < n; e += kStdThreads / 64) {
-        const int32_t c = cand[e];
+    // candidates e = z * waves + wave, step waves * slices: one wave each; a
+    // later copy of a child (found by a ballot over the earlier entries) is
+    // recorded as absent
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, nw = kStdThreads / 64;
+    for (int e = z * nw + wave; e < n; e += nw * kStdSlices) {
+        int32_t c = cand[e];
+        bool dup = false;
+        for (int e0 = 0; e0 < e && c >= 0; e0 += 64)
+            dup = dup || __ballot(e0 + lane < e && cand[min(e0 + lane, e)] == c) != 0ull;
+        if (dup) c = -1;
         float s = 0.f;
         if (c >= 0) {
             float part = 0.f;
@@ -315,7 +304,7 @@ hipError_t launch_std_update(const DevPlan& P, const void* x, bool x_bf16, int64
                        eps);
     const int m = (int)std::min<int64_t>(T, kStdSample);
     if (P.levels > 1 && m > 0) {
-        const dim3 g2(m, P.levels - 1);
+        const dim3 g2(m, P.levels - 1, kStdSlices);
         const size_t xl = (size_t)P.d * 4;
         allow_lds(std_sample_kernel<true>, xl);
         allow_lds(std_sample_kernel<false>, xl);
