@@ -253,6 +253,26 @@ def test_decode_and_bwd_mixed_codes(name):
     compare_dense(gx.cpu().numpy(), rgx, TOL_F32)
 
 
+@pytest.mark.parametrize("name", ["wide", "very_wide"])
+def test_decode_and_bwd_deterministic(name):
+    """Two launches on the same codes (with repeated coordinates and slots)
+    give the same bits: lanes that write the same LDS word write the same
+    value, and repeated coordinates are added in slot order."""
+    say(f"[decode+bwd deterministic] {name}")
+    plan = plan_for(name)
+    w, m, idx, coef = _mixed_codes(name, 301, seed=23)
+    di, dc = torch.from_numpy(idx).to(DEV), torch.from_numpy(coef).to(DEV)
+    g = inputs.upstream_grad(name, 301).to(DEV)
+    y1 = dpb.decode(plan, di, dc)
+    y2 = dpb.decode(plan, di, dc)
+    gc1, gx1 = dpb.decode_bwd(plan, di, g, torch.float32)
+    gc2, gx2 = dpb.decode_bwd(plan, di, g, torch.float32)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+    assert torch.equal(gc1, gc2) and torch.equal(gx1, gx2)
+    compare_dense(y1.cpu().numpy(), oracle.decode(w.d, m, idx, coef.astype(np.float64)), TOL_F32)
+
+
 def test_decode_dyadic_bit_exact_and_one_hot():
     say("[decode exact] tiny")
     plan = plan_for("tiny")
