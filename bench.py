@@ -162,7 +162,7 @@ def time_extras(plan, w, sets, act, steps: int) -> dict:
         torch.autograd.backward([yy, lv], [g, torch.ones((), device=dev)])
         xg.grad = None
 
-    stats, var = dpb.std_state(plan, dev)
+    stats, m2 = dpb.std_state(plan, dev)
     stats.copy_(torch.stack([0.1 * torch.randn(stats.shape[0], generator=gen),
                              torch.rand(stats.shape[0], generator=gen) + 0.5], dim=1))
     sidx = torch.empty_like(idx)
@@ -170,7 +170,7 @@ def time_extras(plan, w, sets, act, steps: int) -> dict:
     sws = dpb.std_workspace(plan, dev)
     cases = {
         "encode_std": (lambda: dpb.encode_std(plan, x, stats, sidx, scoef), d * xb + 8 * k),
-        "std_update": (lambda: dpb.std_update(plan, x, sidx, stats, var, 0.0, 1e-6, sws), d * xb),
+        "std_update": (lambda: dpb.std_update(plan, x, sidx, stats, m2, 0.0, 1e-6, sws), d * xb),
         "normalize": (lambda: dpb.normalize(plan, u, x, y=y), 3 * d * xb),
         "normalize_bwd": (lambda: dpb.normalize_bwd(plan, g, u, x, grad_ref=gref), 5 * d * xb),
         "variance_loss": (lambda: dpb.variance_loss(plan, idx, coef, n_min, workspace=ws), 12 * k),

@@ -96,10 +96,31 @@ void dpb_plan_destroy(dpb_plan* plan);
 /* k_tot = sum_l K_l, the slots per token of a code; 0 for a NULL plan. */
 int dpb_plan_code_width(const dpb_plan* plan);
 
+/* Host copies of the plan's constant tables, for checking them against an
+ * independent construction: masks_host [d] receives the packed rows M_iota
+ * (App. A.4, parity-mask-row equation; bit q = column q), gens_host
+ * [sum_{l>=1} Delta_l] the generators level by level (§2.2).  Host pointers
+ * owned by the caller; gens_host may be NULL for a one-level plan.  Touches
+ * no GPU.  DPB_EINVAL for a NULL plan or a missing output. */
+dpb_status dpb_plan_tables(const dpb_plan* plan, uint32_t* masks_host, uint32_t* gens_host);
+
 /* Copies the plan's hierarchy and host copies of its tables (any output may
  * be NULL): level_bits/branching/active [levels], masks [d], gens [sum Delta]. */
 dpb_status dpb_plan_describe(const dpb_plan* plan, int* d, int* levels, int* level_bits,
                              int* branching, int* active, uint32_t* masks, uint32_t* gens);
+
+/* Bytes of device workspace dpb_encode and dpb_encode_std need for T
+ * tokens (the same for either activation type, with or without statistics;
+ * 0 for a NULL plan or T <= 0).  0 when the plan runs on the narrow encoder
+ * (at most 64 children per parent, K_0 up to the lanes a token gets, and the
+ * other limits of that kernel) or on the general one; for plans that score
+ * many children per parent (up to 256, as the paper's own hierarchies do,
+ * App. G Table 6), for up to C = min(T, 16384) tokens per pass, a region of
+ * 4 * max_l K_{l-1} Delta_l bytes per token (it holds the token's listed
+ * candidates, or all its child scores) and one 4-byte count per token, each
+ * part rounded up to 256 bytes (512 MiB for the paper's 3-level hierarchy at
+ * 16384 tokens). */
+size_t dpb_encode_workspace_bytes(const dpb_plan* plan, int64_t T);
 
 /* ENCODE (§2.2): top-down beam search.  Level 0 scores every basis feature by
  * the coordinate itself (§2.1 Eq. 2) and keeps the K_0 of largest |x_iota|.
@@ -107,39 +128,21 @@ dpb_status dpb_plan_describe(const dpb_plan* plan, int* d, int* levels, int* lev
  * s_c = <phi_c, x> = <gamma_j, phi~_p (.) x> (§2.2 child-scoring equation),
  * counts a child reached from several parents once, and keeps the K_l of
  * largest |s_c| (AbsTopK; ties to the lower index); coef = signed s_c.
- *   x    : device [T, d], fp32 or bf16 (x_dtype)
- *   idx  : device [T, k_tot] int32 (written)
- *   coef : device [T, k_tot] fp32  (written)
- * Scores accumulate in fp32; 1/sqrt(d) is applied once, after accumulation. */
-dpb_status dpb_encode(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T,
-                      int32_t* idx, float* coef, void* stream);
-
-/* Bytes of device workspace dpb_encode_ws needs for T tokens: 0 when the
- * plan runs on the narrow encoder (at most 64 children per parent and the
- * other limits of dpb_encode's fast path), else, for up to C = min(T, 16384)
- * tokens per pass, a region of 4 * max_l K_{l-1} Delta_l bytes per token (it
- * holds the token's listed candidates, or all its child scores) and one
- * 4-byte count per token, each part rounded up to 256 bytes (512 MiB for the
- * paper's 3-level hierarchy at 16384 tokens). */
-size_t dpb_encode_workspace_bytes(const dpb_plan* plan, int64_t T);
-
-/* ENCODE with a workspace: the general entry of which dpb_encode and
- * dpb_encode_std are special cases.  For plans that score many children per
- * parent (up to 256, as the paper's own hierarchies do, App. G Table 6) it
- * runs each level as a matrix-core GEMM of all K_{l-1} x Delta_l child
- * scores whose epilogue lists each token's candidates above a threshold in
- * the workspace (or all its scores), followed by the AbsTopK selection;
- * results are the same as dpb_encode's.
- *   stats     : device fp32 [N][2] standardization statistics, or NULL for
- *               raw scores (see dpb_encode_std)
- *   workspace : device, >= dpb_encode_workspace_bytes(plan, T), 16-B aligned,
- *               caller-owned scratch (may be NULL when that is 0; with NULL,
- *               wide plans fall back to the general encoder, and with stats
- *               to DPB_EUNSUPPORTED)
- * Other arguments as dpb_encode. */
-dpb_status dpb_encode_ws(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T,
-                         const float* stats, int32_t* idx, float* coef, void* workspace,
-                         size_t ws_bytes, void* stream);
+ *   x         : device [T, d], fp32 or bf16 (x_dtype)
+ *   idx       : device [T, k_tot] int32 (written)
+ *   coef      : device [T, k_tot] fp32  (written)
+ *   workspace : device scratch of ws_bytes bytes, caller-owned, 16-B aligned,
+ *               overwritten (nothing needs clearing); may be NULL when
+ *               dpb_encode_workspace_bytes(plan, T) is 0.  A plan that needs
+ *               one and is given none, or too little, gets DPB_EINVAL before
+ *               anything is enqueued.
+ * Scores accumulate in fp32; 1/sqrt(d) is applied once, after accumulation.
+ * Plans with many children per parent run each level as a matrix-core GEMM
+ * of all K_{l-1} x Delta_l child scores whose epilogue lists each token's
+ * candidates above a threshold in the workspace, followed by the AbsTopK
+ * selection; the results are those of the definition either way. */
+dpb_status dpb_encode(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T, int32_t* idx,
+                      float* coef, void* workspace, size_t ws_bytes, void* stream);
 
 /* DECODE (§2.1): y = sum_slots coef * phi_idx, directions generated on chip.
  *   idx, coef : device [T, k_tot] (read; any valid code, not only encoder output)
@@ -185,23 +188,23 @@ dpb_status dpb_decode_bwd_ex(const dpb_plan* plan, const int32_t* idx, const voi
 
 /* SCORE STANDARDIZATION (§2.2 "Score Standardization").  The state is two
  * caller-owned device arrays over all N = 2^n_last features:
- *   stats : fp32 [N][2] = (mu, r): the EMA mean of the feature's raw score and
- *           r = 1 / sigma, sigma^2 = var + eps at the last update
- *   var   : fp32 [N], the EMA of the variance
- * Initial state (dpb_std_init): mu = 0, r = 1, var = 1 -- with it the
+ *   stats : fp32 [N][2] = (mu, r): the moving average of the feature's raw
+ *           score and r = 1 / sigma, sigma^2 = m2 - mu^2 + eps at the last update
+ *   m2    : fp32 [N], the moving average of the squared raw score
+ * Initial state (dpb_std_init): mu = 0, r = 1, m2 = 1 -- with it the
  * standardized encoder equals dpb_encode. */
 #define DPB_STD_SAMPLE 64   /* tokens per batch for the moments of levels >= 1 */
 
-dpb_status dpb_std_init(const dpb_plan* plan, float* stats, float* var, void* stream);
+dpb_status dpb_std_init(const dpb_plan* plan, float* stats, float* m2, void* stream);
 
 /* ENCODE on standardized scores: every candidate's raw score s_c becomes
  * z_c = (s_c - mu_c) r_c; AbsTopK runs on |z| (ties to the lower index) and
  * z is the coefficient written to the code.  Level-0 z is computed in fp32
- * as (x - mu) * r.  Arguments as dpb_encode, plus
- *   stats : device fp32 [N][2] (read).
- * DPB_EUNSUPPORTED for plans outside the fast encoder's limits. */
-dpb_status dpb_encode_std(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T,
-                          const float* stats, int32_t* idx, float* coef, void* stream);
+ * as (x - mu) * r.  Arguments as dpb_encode (the same workspace rule), plus
+ *   stats : device fp32 [N][2] (read; required).
+ * DPB_EUNSUPPORTED for plans only the general encoder covers. */
+dpb_status dpb_encode_std(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T, const float* stats,
+                          int32_t* idx, float* coef, void* workspace, size_t ws_bytes, void* stream);
 
 /* Bytes of device workspace dpb_std_update needs (0 for a NULL plan):
  * 32 bytes per feature, 4 KiB per coordinate, and 8 bytes per candidate of
@@ -214,17 +217,21 @@ size_t dpb_std_workspace_bytes(const dpb_plan* plan);
  * of level l >= 1, the tokens t_j = floor(j T / m), j < m = min(T, 64), at
  * which it is a child p XOR g_j of an active parent p (a level l-1 entry of
  * that token's code), counted once per token, s = <phi_c, x_t>.  A feature
- * with n samples, mean m1 and population variance v gets
- *   mu <- (1 - momentum) mu + momentum m1,  var <- (1 - momentum) var + momentum v,
- *   r = 1 / sqrt(var + eps);
- * other features keep their state.  Moments accumulate in fp64.
+ * with samples s_1..s_n gets moving averages of its first two raw moments,
+ *   mu <- (1 - momentum) mu + momentum mean(s),
+ *   m2 <- (1 - momentum) m2 + momentum mean(s^2),
+ *   r = 1 / sqrt(max(m2 - mu^2, 0) + eps)
+ * (so a feature sampled once per batch still measures its spread across
+ * batches); other features keep their state.  Sums of s and s^2 accumulate
+ * in fp64, the state update is fp32.  Supported while every level's
+ * K_{l-1} Delta_l is at most 8192 and d at most 16384 (else DPB_EUNSUPPORTED).
  *   momentum in [0, 1], eps >= 0
- *   stats, var : device (read and written)
+ *   stats, m2  : device (read and written)
  *   workspace  : device, >= dpb_std_workspace_bytes(plan), 16-B aligned;
  *                caller-owned scratch, overwritten, no clearing needed */
-dpb_status dpb_std_update(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T,
-                          const int32_t* idx, float momentum, float eps, float* stats, float* var,
-                          void* workspace, size_t ws_bytes, void* stream);
+dpb_status dpb_std_update(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T, const int32_t* idx,
+                          float momentum, float eps, float* stats, float* m2, void* workspace, size_t ws_bytes,
+                          void* stream);
 
 /* NORMALIZED RECONSTRUCTION (§2.2 "Normalized Reconstruction"): each row of
  * the decoder output u is rescaled to the norm of the bottleneck input,

@@ -56,6 +56,8 @@ def _load():
         "oracle_masks": (i32, [i32, i32, P]),
         "oracle_phi": (dbl, [i32, P, i64, i32]),
         "oracle_generators": (i32, [i32, P, P, u64, P]),
+        "oracle_splitmix64": (None, [u64, i32, P]),
+        "oracle_scores": (None, [i32, P, P, i64, P, P]),
         "oracle_hierarchy": (i32, [i32, i32, i32, i32, i32, i32, P, P, P]),
         "oracle_encode": (i32, [i32, P, i32, P, P, P, P, P, i64, P, P, P, P]),
         "oracle_decode": (None, [i32, P, i32, P, P, i64, P]),
@@ -65,6 +67,7 @@ def _load():
         "oracle_normalize_bwd": (None, [i32, i64, P, P, P, P, P]),
         "oracle_encode_std": (i32, [i32, P, i32, P, P, P, P, P, i64, P, P, P, P, P, P]),
         "oracle_std_update": (None, [i32, P, i32, P, P, P, P, P, i64, P, i32, dbl, P, P]),
+        "oracle_std_r": (None, [i64, P, P, dbl, P]),
         "oracle_edit_codes": (None, [i64, i32, P, P, P, P, i64, P, P, P, P, P]),
         "oracle_variance_loss": (dbl, [i64, i32, P, P, i32, P]),
         "oracle_num_threads": (i32, []),
@@ -165,6 +168,14 @@ def generators(nbits: Sequence[int], delta: Sequence[int], seed: int = 0) -> lis
     return res
 
 
+def splitmix64(state: int, n: int) -> list[int]:
+    """The first n outputs of the SplitMix64 generator (Steele, Lea and Flood
+    2014) from `state`, the stream the generator sampling draws from."""
+    out = np.zeros(max(n, 1), dtype=np.uint64)
+    _load().oracle_splitmix64(state & (2**64 - 1), n, _ptr(out))
+    return [int(v) for v in out[:n]]
+
+
 def hierarchy(d: int, n: int, levels: int, branching: int, beam: int, k: int):
     """Config terms -> (n_l, Delta_l, K_l) (reading of App. G Table 6; parity unpinned)."""
     nb = np.zeros(levels, dtype=np.int32)
@@ -205,6 +216,18 @@ def encode(d: int, m: np.ndarray, nbits, active, delta, gens: list[np.ndarray], 
     return idx, coef, margin, order
 
 
+def scores(d: int, m: np.ndarray, x_row: np.ndarray, ids) -> np.ndarray:
+    """<phi_c, x> in fp64 for each feature c of ids (basis features give the
+    coordinate itself), x_row one activation row [d]."""
+    x_row = np.ascontiguousarray(x_row, dtype=np.float64)
+    assert x_row.shape == (d,)
+    ids = np.ascontiguousarray(np.asarray(ids, dtype=np.int64).reshape(-1))
+    out = np.zeros(max(ids.size, 1), dtype=np.float64)
+    if ids.size:
+        _load().oracle_scores(d, _ptr(m), _ptr(x_row), ids.size, _ptr(ids), _ptr(out))
+    return out[: ids.size]
+
+
 def _hier_arrays(nbits, active, delta, gens):
     L = len(nbits)
     nb = np.asarray(nbits, dtype=np.int32)
@@ -241,22 +264,34 @@ def encode_std(d: int, m: np.ndarray, nbits, active, delta, gens: list[np.ndarra
 
 
 def std_update(d: int, m: np.ndarray, nbits, active, delta, gens: list[np.ndarray], x: np.ndarray,
-               idx: np.ndarray, mu: np.ndarray, var: np.ndarray, beta: float, sample: int = 64):
+               idx: np.ndarray, mu: np.ndarray, m2: np.ndarray, beta: float, sample: int = 64):
     """EMA update of the standardization statistics after a batch (§2.2
-    "Score Standardization"; sampling and update rule are readings).  x is
-    the batch, idx its code; mu, var fp64 [2^n_last].  Returns updated
-    copies (mu, var)."""
+    "Score Standardization"; the sample and the moving raw moments are
+    readings): mu and m2 are the moving first and second raw moments of each
+    feature's score while it is a candidate.  x is the batch, idx its code;
+    mu, m2 fp64 [2^n_last].  Returns updated copies (mu, m2)."""
     x = np.ascontiguousarray(x, dtype=np.float64)
     T = x.shape[0]
     L, nb, ac, dl, g = _hier_arrays(nbits, active, delta, gens)
     idx = np.ascontiguousarray(idx, dtype=np.int32)
     assert idx.shape == (T, int(ac.sum()))
     mu = np.array(mu, dtype=np.float64, order="C")
-    var = np.array(var, dtype=np.float64, order="C")
-    assert mu.shape == var.shape == (1 << int(nb[-1]),)
+    m2 = np.array(m2, dtype=np.float64, order="C")
+    assert mu.shape == m2.shape == (1 << int(nb[-1]),)
     _load().oracle_std_update(d, _ptr(m), L, _ptr(nb), _ptr(ac), _ptr(dl), _ptr(g), _ptr(x), T, _ptr(idx),
-                              int(sample), float(beta), _ptr(mu), _ptr(var))
-    return mu, var
+                              int(sample), float(beta), _ptr(mu), _ptr(m2))
+    return mu, m2
+
+
+def std_r(mu: np.ndarray, m2: np.ndarray, eps: float) -> np.ndarray:
+    """r = 1 / sqrt(max(m2 - mu^2, 0) + eps): the inverse standard deviation
+    the two moving moments imply, fp64."""
+    mu = np.ascontiguousarray(mu, dtype=np.float64)
+    m2 = np.ascontiguousarray(m2, dtype=np.float64)
+    assert mu.shape == m2.shape and mu.ndim == 1
+    r = np.zeros_like(mu)
+    _load().oracle_std_r(mu.shape[0], _ptr(mu), _ptr(m2), float(eps), _ptr(r))
+    return r
 
 
 def decode(d: int, m: np.ndarray, idx: np.ndarray, coef: np.ndarray) -> np.ndarray:

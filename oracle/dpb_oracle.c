@@ -29,9 +29,16 @@
  *   R9  every level is emitted, level-major, so k_tot = sum_l K_l.
  *   R10 without statistics, selection scores are the raw scores (EMA
  *       standardization at its initial state, mean 0 and std 1); with them,
- *       z = (s - mu) r, r = 1/sigma (§2.2 "Score Standardization"; the
- *       statistics are R16-R18 in the design notes).
+ *       z = (s - mu) r, r = 1/sigma (§2.2 "Score Standardization").
  *   R11 backward: grad_coef = Phi_S^T g, grad_x = Phi_S grad_coef.
+ *   R20 standardized scores: level-0 z = (x - mu) r is taken in fp32 (the
+ *       precision the kernel takes it in, so both sides rank the same level-0
+ *       keys), levels above in fp64; mu and r are fp32 per feature.
+ *   R21 statistics sample: level 0 every token of the batch; levels >= 1 the
+ *       m = min(64, T) tokens floor(j T / m), each child of an active parent
+ *       once per token.
+ *   R22 the moving averages are of the first two raw moments of a feature's
+ *       candidate scores; sigma^2 = m2 - mu^2.
  */
 #include <math.h>
 #include <stdint.h>
@@ -244,6 +251,13 @@ static uint64_t splitmix64_next(uint64_t* state)
     return z ^ (z >> 31);
 }
 
+/* The first n outputs of SplitMix64 from `state` (for checking the
+ * generator against its published reference outputs). */
+void oracle_splitmix64(uint64_t state, int n, uint64_t* out)
+{
+    for (int i = 0; i < n; ++i) out[i] = splitmix64_next(&state);
+}
+
 /* gens receives sum_{l>=1} delta[l] words, level by level. */
 int oracle_generators(int levels, const int* nbits, const int* delta, uint64_t seed, uint32_t* gens)
 {
@@ -318,6 +332,14 @@ static double dense_score(int d, const uint32_t* masks, int64_t c, const double*
     double s = 0.0;
     for (int iota = 0; iota < d; ++iota) s += oracle_phi(d, masks, c, iota) * x[iota];
     return s;
+}
+
+/* Scores <phi_c, x> of n features ids[0..n) against one activation row x
+ * (fp64, directions from the definition), for checking a selection made
+ * elsewhere against the exact scores. */
+void oracle_scores(int d, const uint32_t* masks, const double* x, int64_t n, const int64_t* ids, double* out)
+{
+    for (int64_t i = 0; i < n; ++i) out[i] = dense_score(d, masks, ids[i], x);
 }
 
 /* Records the selection margins used to decide which GPU/oracle
@@ -538,21 +560,23 @@ int oracle_walsh_spectrum(int d, const uint32_t* masks, int r, int64_t* S)
 }
 
 /* EMA update of the standardization statistics (§2.2 "Score
- * Standardization") after a batch encoded with them.  The statistics of a
- * feature are taken over the tokens where it was a candidate: a basis
- * feature (level 0) is a candidate at every token, so its sample is the
- * column x[:, iota] of the whole batch; a feature of level l >= 1 is a
- * candidate where it is a child p XOR g_j of an active parent p (a level
- * l-1 entry of the token's code), and its sample is taken on the `sample`
- * tokens t_j = floor(j T / m), j < m = min(sample, T) (the paper's 64-token
- * sub-samples), one raw score <phi_c, x_t> per token even when several
- * parents reach it.  For every feature with n >= 1 samples, mean m1 and
- * population variance v:
- *     mu <- (1 - beta) mu + beta m1,   var <- (1 - beta) var + beta v.
- * Features with no sample keep their state.  mu, var: fp64 [N]. */
+ * Standardization": an exponential moving average of each feature's mean and
+ * standard deviation, taken over the tokens where the feature was a
+ * candidate).  A basis feature (level 0) is a candidate at every token, so its
+ * sample is the column x[:, iota] of the whole batch; a feature of level
+ * l >= 1 is a candidate where it is a child p XOR g_j of an active parent p
+ * (a level l-1 entry of the token's code), and its sample is taken on the
+ * `sample` tokens t_j = floor(j T / m), j < m = min(sample, T) (the paper's
+ * sub-samples of 64 tokens), one raw score <phi_c, x_t> per token even when
+ * several parents reach it.  The moving averages are of the first two raw
+ * moments (reading R22): for every feature with n >= 1 samples,
+ *     mu <- (1 - beta) mu + beta * mean(s),   m2 <- (1 - beta) m2 + beta * mean(s^2),
+ * and sigma^2 = m2 - mu^2 (oracle_std_r), so a feature sampled once per batch
+ * still estimates its spread over the batches.  Features with no sample keep
+ * their state.  mu, m2: fp64 [N]. */
 void oracle_std_update(int d, const uint32_t* masks, int levels, const int* nbits, const int* active,
                        const int* delta, const uint32_t* gens, const double* x, int64_t T, const int32_t* idx,
-                       int sample, double beta, double* mu, double* var)
+                       int sample, double beta, double* mu, double* m2)
 {
     const int64_t N = (int64_t)1 << nbits[levels - 1];
     int k_tot = 0, max_ids = 1;
@@ -565,59 +589,59 @@ void oracle_std_update(int d, const uint32_t* masks, int levels, const int* nbit
     double* s2 = (double*)calloc((size_t)N, sizeof(double));
     int64_t* ids = (int64_t*)malloc(sizeof(int64_t) * (size_t)max_ids);
     const int64_t m = T < sample ? T : sample;
-    /* pass 1: counts and sums; pass 2: squared deviations about the mean */
-    for (int pass = 0; pass < 2; ++pass) {
-        for (int64_t t = 0; t < T; ++t)
-            for (int iota = 0; iota < d; ++iota) {
-                const double v = x[t * d + iota];
-                if (pass == 0) {
-                    cnt[iota] += 1.0;
-                    s1[iota] += v;
-                } else {
-                    const double dv = v - s1[iota] / cnt[iota];
-                    s2[iota] += dv * dv;
-                }
+    for (int64_t t = 0; t < T; ++t)
+        for (int iota = 0; iota < d; ++iota) {
+            const double v = x[t * d + iota];
+            cnt[iota] += 1.0;
+            s1[iota] += v;
+            s2[iota] += v * v;
+        }
+    for (int64_t j = 0; j < m; ++j) {
+        const int64_t t = (j * T) / m;
+        const int32_t* code = idx + t * k_tot;
+        const uint32_t* g = gens;
+        int slot = 0;
+        for (int l = 1; l < levels; ++l) {
+            const int pb = slot;          /* the parents: level l-1 entries */
+            slot += active[l - 1];
+            int n_ids = 0;
+            for (int q = pb; q < slot; ++q) {
+                if (code[q] < 0) continue;
+                for (int jj = 0; jj < delta[l]; ++jj) ids[n_ids++] = (int64_t)code[q] ^ (int64_t)g[jj];
             }
-        for (int64_t j = 0; j < m; ++j) {
-            const int64_t t = (j * T) / m;
-            const int32_t* code = idx + t * k_tot;
-            const uint32_t* g = gens;
-            int slot = 0;
-            for (int l = 1; l < levels; ++l) {
-                const int pb = slot;          /* the parents: level l-1 entries */
-                slot += active[l - 1];
-                int n_ids = 0;
-                for (int q = pb; q < slot; ++q) {
-                    if (code[q] < 0) continue;
-                    for (int jj = 0; jj < delta[l]; ++jj) ids[n_ids++] = (int64_t)code[q] ^ (int64_t)g[jj];
-                }
-                qsort(ids, (size_t)n_ids, sizeof(int64_t), idx_cmp);
-                for (int i = 0; i < n_ids; ++i) {
-                    if (i > 0 && ids[i] == ids[i - 1]) continue;
-                    const int64_t c = ids[i];
-                    const double v = dense_score(d, masks, c, x + t * d);
-                    if (pass == 0) {
-                        cnt[c] += 1.0;
-                        s1[c] += v;
-                    } else {
-                        const double dv = v - s1[c] / cnt[c];
-                        s2[c] += dv * dv;
-                    }
-                }
-                g += delta[l];
+            qsort(ids, (size_t)n_ids, sizeof(int64_t), idx_cmp);
+            for (int i = 0; i < n_ids; ++i) {
+                if (i > 0 && ids[i] == ids[i - 1]) continue;
+                const int64_t c = ids[i];
+                const double v = dense_score(d, masks, c, x + t * d);
+                cnt[c] += 1.0;
+                s1[c] += v;
+                s2[c] += v * v;
             }
+            g += delta[l];
         }
     }
     for (int64_t c = 0; c < N; ++c) {
         if (cnt[c] == 0.0) continue;
-        const double m1 = s1[c] / cnt[c], v = s2[c] / cnt[c];
-        mu[c] = (1.0 - beta) * mu[c] + beta * m1;
-        var[c] = (1.0 - beta) * var[c] + beta * v;
+        mu[c] = (1.0 - beta) * mu[c] + beta * (s1[c] / cnt[c]);
+        m2[c] = (1.0 - beta) * m2[c] + beta * (s2[c] / cnt[c]);
     }
     free(cnt);
     free(s1);
     free(s2);
     free(ids);
+}
+
+/* r = 1 / sigma = 1 / sqrt(max(m2 - mu^2, 0) + eps) of each of the n features
+ * (the variance implied by the two moving moments, clamped at 0 against
+ * rounding). */
+void oracle_std_r(int64_t n, const double* mu, const double* m2, double eps, double* r)
+{
+    for (int64_t c = 0; c < n; ++c) {
+        double v = m2[c] - mu[c] * mu[c];
+        if (v < 0.0) v = 0.0;
+        r[c] = 1.0 / sqrt(v + eps);
+    }
 }
 
 /* ------------------------------------------------------------------ */

@@ -31,17 +31,17 @@ from . import binding as B
 
 class Standardizer:
     """EMA score-standardization state of one bottleneck (§2.2 "Score
-    Standardization"): stats [N, 2] = (mu, r = 1/sigma) and var [N], updated
-    after every training backward with `momentum`."""
+    Standardization"): stats [N, 2] = (mu, r = 1/sigma) and m2 [N] (moving
+    second raw moment), updated after every training backward with `momentum`."""
 
     def __init__(self, plan: B.Plan, momentum: float = 0.01, eps: float = 1e-6, device=None):
         self.plan, self.momentum, self.eps = plan, momentum, eps
-        self.stats, self.var = B.std_state(plan, device)
+        self.stats, self.m2 = B.std_state(plan, device)
         self.workspace = B.std_workspace(plan, self.stats.device)
         self.training = True
 
     def update(self, x: torch.Tensor, idx: torch.Tensor):
-        B.std_update(self.plan, x, idx, self.stats, self.var, self.momentum, self.eps, self.workspace)
+        B.std_update(self.plan, x, idx, self.stats, self.m2, self.momentum, self.eps, self.workspace)
 
 
 class DPBLayer(torch.autograd.Function):
@@ -105,7 +105,7 @@ class DPBMLP(torch.nn.Module):
         self.std = Standardizer(plan, momentum, device=device) if standardize else None
         if self.std is not None:
             self.register_buffer("std_stats", self.std.stats)
-            self.register_buffer("std_var", self.std.var)
+            self.register_buffer("std_m2", self.std.m2)
         self.norm = torch.nn.RMSNorm(d, dtype=dtype, device=device)
         self.fc1 = torch.nn.Linear(d, d_ff, dtype=dtype, device=device)
         self.fc2 = torch.nn.Linear(d_ff, d, dtype=dtype, device=device)

@@ -47,13 +47,13 @@ def load():
         "dpb_plan_destroy": (None, [P]),
         "dpb_plan_code_width": (i32, [P]),
         "dpb_plan_describe": (i32, [P, P, P, P, P, P, P, P]),
-        "dpb_encode": (i32, [P, P, i32, i64, P, P, P]),
+        "dpb_plan_tables": (i32, [P, P, P]),
+        "dpb_encode": (i32, [P, P, i32, i64, P, P, P, ctypes.c_size_t, P]),
         "dpb_decode": (i32, [P, P, P, i64, P, i32, P]),
         "dpb_decode_bwd": (i32, [P, P, P, i32, i64, P, P, i32, P]),
         "dpb_decode_bwd_ex": (i32, [P, P, P, i32, i64, P, P, P, P, P, i32, P]),
-        "dpb_encode_std": (i32, [P, P, i32, i64, P, P, P, P]),
+        "dpb_encode_std": (i32, [P, P, i32, i64, P, P, P, P, ctypes.c_size_t, P]),
         "dpb_encode_workspace_bytes": (ctypes.c_size_t, [P, i64]),
-        "dpb_encode_ws": (i32, [P, P, i32, i64, P, P, P, P, ctypes.c_size_t, P]),
         "dpb_std_init": (i32, [P, P, P, P]),
         "dpb_std_workspace_bytes": (ctypes.c_size_t, [P]),
         "dpb_std_update": (i32, [P, P, i32, i64, P, ctypes.c_float, ctypes.c_float, P, P, P, ctypes.c_size_t, P]),
@@ -166,7 +166,7 @@ class Plan:
         masks = (ctypes.c_uint32 * self.d)()
         ng = max(1, sum(self.branching[1:]))
         gens = (ctypes.c_uint32 * ng)()
-        _check("dpb_plan_describe", lib.dpb_plan_describe(self._handle, None, None, None, None, None, masks, gens))
+        _check("dpb_plan_tables", lib.dpb_plan_tables(self._handle, masks, gens))
         return list(masks), list(gens[: sum(self.branching[1:])])
 
     def close(self):
@@ -201,9 +201,14 @@ def encode(plan: Plan, x: torch.Tensor, idx: torch.Tensor | None = None, coef: t
     if workspace is None:
         workspace = encode_workspace(plan, T, x.device)
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    _check("dpb_encode_ws", load().dpb_encode_ws(plan._handle, _dev(x, "x"), _dtype_code(x), T,
-                                                 _opt(stats, "stats"), _dev(idx, "idx"), _dev(coef, "coef"),
-                                                 _opt(workspace, "workspace"), nbytes, _stream(x)))
+    if stats is None:
+        _check("dpb_encode", load().dpb_encode(plan._handle, _dev(x, "x"), _dtype_code(x), T, _dev(idx, "idx"),
+                                               _dev(coef, "coef"), _opt(workspace, "workspace"), nbytes,
+                                               _stream(x)))
+    else:
+        _check("dpb_encode_std", load().dpb_encode_std(plan._handle, _dev(x, "x"), _dtype_code(x), T,
+                                                       _dev(stats, "stats"), _dev(idx, "idx"), _dev(coef, "coef"),
+                                                       _opt(workspace, "workspace"), nbytes, _stream(x)))
     return idx, coef
 
 
@@ -367,15 +372,15 @@ STD_SAMPLE = 64
 
 
 def std_state(plan: Plan, device=None):
-    """Fresh standardization state (stats [N, 2] = (mu, r), var [N]) at its
-    initial value (mu 0, r 1, var 1)."""
+    """Fresh standardization state (stats [N, 2] = (mu, r), m2 [N]) at its
+    initial value (mu 0, r 1, m2 1)."""
     device = device or plan.device
     N = 1 << plan.level_bits[-1]
     stats = torch.empty((N, 2), dtype=torch.float32, device=device)
-    var = torch.empty((N,), dtype=torch.float32, device=device)
-    _check("dpb_std_init", load().dpb_std_init(plan._handle, _dev(stats, "stats"), _dev(var, "var"),
+    m2 = torch.empty((N,), dtype=torch.float32, device=device)
+    _check("dpb_std_init", load().dpb_std_init(plan._handle, _dev(stats, "stats"), _dev(m2, "m2"),
                                                _stream(stats)))
-    return stats, var
+    return stats, m2
 
 
 def encode_std(plan: Plan, x: torch.Tensor, stats: torch.Tensor, idx: torch.Tensor | None = None,
@@ -390,15 +395,15 @@ def std_workspace(plan: Plan, device) -> torch.Tensor:
     return torch.empty(((n + 15) // 16) * 4, dtype=torch.float32, device=device)
 
 
-def std_update(plan: Plan, x: torch.Tensor, idx: torch.Tensor, stats: torch.Tensor, var: torch.Tensor,
+def std_update(plan: Plan, x: torch.Tensor, idx: torch.Tensor, stats: torch.Tensor, m2: torch.Tensor,
                momentum: float, eps: float = 1e-6, workspace: torch.Tensor | None = None):
-    """EMA update of (stats, var) in place from the batch x and its code idx."""
+    """EMA update of (stats, m2) in place from the batch x and its code idx."""
     T = x.shape[0]
     assert idx.shape == (T, plan.k_tot) and idx.dtype == torch.int32
     if workspace is None:
         workspace = std_workspace(plan, x.device)
     _check("dpb_std_update", load().dpb_std_update(
         plan._handle, _dev(x, "x"), _dtype_code(x), T, _dev(idx, "idx"), float(momentum), float(eps),
-        _dev(stats, "stats"), _dev(var, "var"), _dev(workspace, "workspace"),
+        _dev(stats, "stats"), _dev(m2, "m2"), _dev(workspace, "workspace"),
         workspace.numel() * workspace.element_size(), _stream(x)))
-    return stats, var
+    return stats, m2

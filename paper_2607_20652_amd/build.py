@@ -16,7 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libdpb.so")
 OBJ_DIR = os.path.join(os.path.dirname(HERE), "_build")
-SOURCES = ["api.cpp", "tables.cpp", "kernels.hip", "codes.hip", "encode.hip", "extras.hip", "standardize.hip"]
+SOURCES = ["api.cpp", "tables.cpp", "encode_general.hip", "codes.hip", "encode.hip", "extras.hip", "standardize.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

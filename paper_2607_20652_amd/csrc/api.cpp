@@ -355,6 +355,27 @@ dpb_status upload(dpb_plan* plan)
     return DPB_OK;
 }
 
+// The encoder that runs a plan: the narrow one (a level's candidates in one
+// wave's registers), the wide one (a GEMM per level and a workspace), or the
+// general one; None when no encoder covers the plan for this activation type
+// (or, with statistics, on standardized scores, which the general encoder
+// does not take).
+enum class Enc { Narrow, Wide, General, None };
+
+Enc pick_encoder(const DevPlan& P, bool x_bf16, bool std)
+{
+    if (dpb::encode2_supported(P) && (!std || dpb::encode2_std_supported(P))) return Enc::Narrow;
+    if (dpb::encode_wide_supported(P, x_bf16)) return Enc::Wide;
+    if (!std && dpb::general_encoder_fits(P)) return Enc::General;
+    return Enc::None;
+}
+
+// A plan is accepted when some encoder takes both activation types.
+bool any_encoder(const DevPlan& P)
+{
+    return pick_encoder(P, true, false) != Enc::None && pick_encoder(P, false, false) != Enc::None;
+}
+
 dpb_status create(dpb_plan** out, const Hierarchy& h, const uint32_t* gens, uint64_t seed)
 {
     if (!out) return DPB_EINVAL;
@@ -364,7 +385,7 @@ dpb_status create(dpb_plan** out, const Hierarchy& h, const uint32_t* gens, uint
     dpb_plan* plan = new (std::nothrow) dpb_plan();
     if (!plan) return DPB_ENOMEM;
     dpb_status s = fill_plan(plan, h, gens, seed);
-    if (s == DPB_OK && (!dpb::plan_fits(plan->dev) || !dpb::code_kernels_fit(plan->dev))) s = DPB_EUNSUPPORTED;
+    if (s == DPB_OK && (!any_encoder(plan->dev) || !dpb::code_kernels_fit(plan->dev))) s = DPB_EUNSUPPORTED;
     if (s == DPB_OK) s = upload(plan);
     if (s != DPB_OK) {
         dpb_plan_destroy(plan);
@@ -397,6 +418,32 @@ dpb_status launched(hipError_t e)
         return DPB_EHIP;
     }
     return DPB_OK;
+}
+
+// dpb_encode and dpb_encode_std: argument checks, then the plan's encoder.
+dpb_status encode_any(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T, const float* stats,
+                      int32_t* idx, float* coef, void* workspace, size_t ws_bytes, void* stream)
+{
+    dpb_status s = check_call(plan, T);
+    if (s) return s;
+    if (!dtype_ok(x_dtype)) return DPB_EINVAL;
+    const DevPlan& P = plan->dev;
+    const bool bf = x_dtype == DPB_BF16;
+    const Enc e = pick_encoder(P, bf, stats != nullptr);
+    if (e == Enc::None) return DPB_EUNSUPPORTED;
+    if (T == 0) return DPB_OK;
+    if (!x || !idx || !coef || !aligned16(x) || !aligned16(idx) || !aligned16(coef) || !aligned16(stats) ||
+        !aligned16(workspace))
+        return DPB_EINVAL;
+    hipStream_t st = (hipStream_t)stream;
+    switch (e) {
+    case Enc::Narrow: return launched(dpb::launch_encode2(P, x, bf, T, stats, idx, coef, st));
+    case Enc::Wide:
+        if (!workspace || ws_bytes < dpb::encode_wide_workspace_bytes(P, T)) return DPB_EINVAL;
+        return launched(dpb::launch_encode_wide(P, x, bf, T, stats, idx, coef, workspace, st));
+    case Enc::General: return launched(dpb::launch_encode(P, x, bf, T, idx, coef, st));
+    default: return DPB_EUNSUPPORTED;
+    }
 }
 
 }  // namespace
@@ -506,6 +553,14 @@ void dpb_plan_destroy(dpb_plan* plan)
 
 int dpb_plan_code_width(const dpb_plan* plan) { return plan ? plan->dev.k_tot : 0; }
 
+dpb_status dpb_plan_tables(const dpb_plan* plan, uint32_t* masks_host, uint32_t* gens_host)
+{
+    if (!plan || !masks_host || (!gens_host && !plan->gens_h.empty())) return DPB_EINVAL;
+    std::memcpy(masks_host, plan->masks_h.data(), plan->masks_h.size() * 4);
+    if (!plan->gens_h.empty()) std::memcpy(gens_host, plan->gens_h.data(), plan->gens_h.size() * 4);
+    return DPB_OK;
+}
+
 dpb_status dpb_plan_describe(const dpb_plan* plan, int* d, int* levels, int* level_bits, int* branching,
                              int* active, uint32_t* masks, uint32_t* gens)
 {
@@ -524,17 +579,9 @@ dpb_status dpb_plan_describe(const dpb_plan* plan, int* d, int* levels, int* lev
 }
 
 dpb_status dpb_encode(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T, int32_t* idx,
-                      float* coef, void* stream)
+                      float* coef, void* workspace, size_t ws_bytes, void* stream)
 {
-    dpb_status s = check_call(plan, T);
-    if (s) return s;
-    if (!dtype_ok(x_dtype)) return DPB_EINVAL;
-    if (T == 0) return DPB_OK;
-    if (!x || !idx || !coef || !aligned16(x) || !aligned16(idx) || !aligned16(coef)) return DPB_EINVAL;
-    if (dpb::encode2_supported(plan->dev))
-        return launched(dpb::launch_encode2(plan->dev, x, x_dtype == DPB_BF16, T, nullptr, idx, coef,
-                                            (hipStream_t)stream));
-    return launched(dpb::launch_encode(plan->dev, x, x_dtype == DPB_BF16, T, idx, coef, (hipStream_t)stream));
+    return encode_any(plan, x, x_dtype, T, nullptr, idx, coef, workspace, ws_bytes, stream);
 }
 
 dpb_status dpb_decode(const dpb_plan* plan, const int32_t* idx, const float* coef, int64_t T, void* y,
@@ -581,55 +628,28 @@ dpb_status dpb_decode_bwd_ex(const dpb_plan* plan, const int32_t* idx, const voi
 
 size_t dpb_encode_workspace_bytes(const dpb_plan* plan, int64_t T)
 {
-    // sized for either activation type (the workspace does not depend on it)
-    if (!plan || T <= 0 || dpb::encode2_supported(plan->dev) ||
-        !(dpb::encode_wide_supported(plan->dev, true) || dpb::encode_wide_supported(plan->dev, false)))
-        return 0;
-    return dpb::encode_wide_workspace_bytes(plan->dev, T);
-}
-
-dpb_status dpb_encode_ws(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T, const float* stats,
-                         int32_t* idx, float* coef, void* workspace, size_t ws_bytes, void* stream)
-{
-    dpb_status s = check_call(plan, T);
-    if (s) return s;
-    if (!dtype_ok(x_dtype)) return DPB_EINVAL;
-    if (T == 0) return DPB_OK;
-    if (!x || !idx || !coef || !aligned16(x) || !aligned16(idx) || !aligned16(coef) || !aligned16(stats) ||
-        !aligned16(workspace))
-        return DPB_EINVAL;
+    // the same for either activation type, with or without statistics
+    if (!plan || T <= 0) return 0;
     const DevPlan& P = plan->dev;
-    const bool bf = x_dtype == DPB_BF16;
-    hipStream_t st = (hipStream_t)stream;
-    if (dpb::encode2_supported(P)) {
-        if (stats && !dpb::encode2_std_supported(P)) return DPB_EUNSUPPORTED;
-        return launched(dpb::launch_encode2(P, x, bf, T, stats, idx, coef, st));
-    }
-    if (dpb::encode_wide_supported(P, bf) && workspace && ws_bytes >= dpb::encode_wide_workspace_bytes(P, T))
-        return launched(dpb::launch_encode_wide(P, x, bf, T, stats, idx, coef, workspace, st));
-    if (stats) return DPB_EUNSUPPORTED;
-    return launched(dpb::launch_encode(P, x, bf, T, idx, coef, st));
+    bool wide = false;
+    for (int b = 0; b < 2; ++b)
+        for (int st = 0; st < 2; ++st) wide = wide || pick_encoder(P, b != 0, st != 0) == Enc::Wide;
+    return wide ? dpb::encode_wide_workspace_bytes(P, T) : 0;
 }
 
 dpb_status dpb_encode_std(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T, const float* stats,
-                          int32_t* idx, float* coef, void* stream)
+                          int32_t* idx, float* coef, void* workspace, size_t ws_bytes, void* stream)
 {
-    dpb_status s = check_call(plan, T);
-    if (s) return s;
-    if (!dtype_ok(x_dtype)) return DPB_EINVAL;
-    if (!dpb::encode2_std_supported(plan->dev)) return DPB_EUNSUPPORTED;
-    if (T == 0) return DPB_OK;
-    if (!x || !idx || !coef || !stats || !aligned16(x) || !aligned16(idx) || !aligned16(coef) || !aligned16(stats))
-        return DPB_EINVAL;
-    return launched(dpb::launch_encode2(plan->dev, x, x_dtype == DPB_BF16, T, stats, idx, coef, (hipStream_t)stream));
+    if (plan && T > 0 && !stats) return DPB_EINVAL;
+    return encode_any(plan, x, x_dtype, T, stats, idx, coef, workspace, ws_bytes, stream);
 }
 
-dpb_status dpb_std_init(const dpb_plan* plan, float* stats, float* var, void* stream)
+dpb_status dpb_std_init(const dpb_plan* plan, float* stats, float* m2, void* stream)
 {
     dpb_status s = check_call(plan, 0);
     if (s) return s;
-    if (!stats || !var || !aligned16(stats) || !aligned16(var)) return DPB_EINVAL;
-    return launched(dpb::launch_std_init(plan->dev, stats, var, (hipStream_t)stream));
+    if (!stats || !m2 || !aligned16(stats) || !aligned16(m2)) return DPB_EINVAL;
+    return launched(dpb::launch_std_init(plan->dev, stats, m2, (hipStream_t)stream));
 }
 
 size_t dpb_std_workspace_bytes(const dpb_plan* plan)
@@ -638,7 +658,7 @@ size_t dpb_std_workspace_bytes(const dpb_plan* plan)
 }
 
 dpb_status dpb_std_update(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T, const int32_t* idx,
-                          float momentum, float eps, float* stats, float* var, void* workspace, size_t ws_bytes,
+                          float momentum, float eps, float* stats, float* m2, void* workspace, size_t ws_bytes,
                           void* stream)
 {
     dpb_status s = check_call(plan, T);
@@ -646,10 +666,10 @@ dpb_status dpb_std_update(const dpb_plan* plan, const void* x, dpb_dtype x_dtype
     if (!dtype_ok(x_dtype) || !(momentum >= 0.f && momentum <= 1.f) || !(eps >= 0.f)) return DPB_EINVAL;
     if (!dpb::std_supported(plan->dev)) return DPB_EUNSUPPORTED;
     if (T == 0) return DPB_OK;
-    if (!x || !idx || !stats || !var || !workspace || !aligned16(x) || !aligned16(idx) || !aligned16(stats) ||
-        !aligned16(var) || !aligned16(workspace) || ws_bytes < dpb::std_workspace_bytes(plan->dev))
+    if (!x || !idx || !stats || !m2 || !workspace || !aligned16(x) || !aligned16(idx) || !aligned16(stats) ||
+        !aligned16(m2) || !aligned16(workspace) || ws_bytes < dpb::std_workspace_bytes(plan->dev))
         return DPB_EINVAL;
-    return launched(dpb::launch_std_update(plan->dev, x, x_dtype == DPB_BF16, T, idx, momentum, eps, stats, var,
+    return launched(dpb::launch_std_update(plan->dev, x, x_dtype == DPB_BF16, T, idx, momentum, eps, stats, m2,
                                            workspace, (hipStream_t)stream));
 }
 

@@ -177,8 +177,8 @@ inline void allow_lds(F* kernel, size_t bytes)
         (void)hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
 }
 
-// True when every kernel's workgroup fits the LDS budget for this plan.
-bool plan_fits(const DevPlan& P);
+// True when the general encoder's workgroup (one fp32 token) fits the LDS budget.
+bool general_encoder_fits(const DevPlan& P);
 
 hipError_t launch_decode2(const DevPlan& P, const int32_t* idx, const float* coef, int64_t T, void* y,
                           bool y_bf16, hipStream_t stream);
@@ -202,9 +202,9 @@ hipError_t launch_encode2(const DevPlan& P, const void* x, bool x_bf16, int64_t 
 constexpr int kStdSample = 64;
 size_t std_workspace_bytes(const DevPlan& P);
 bool std_supported(const DevPlan& P);
-hipError_t launch_std_init(const DevPlan& P, float* stats, float* var, hipStream_t stream);
+hipError_t launch_std_init(const DevPlan& P, float* stats, float* m2, hipStream_t stream);
 hipError_t launch_std_update(const DevPlan& P, const void* x, bool x_bf16, int64_t T, const int32_t* idx,
-                             float beta, float eps, float* stats, float* var, void* ws, hipStream_t stream);
+                             float beta, float eps, float* stats, float* m2, void* ws, hipStream_t stream);
 
 // Row epilogues, code edits and the variance loss (extras.hip).
 hipError_t launch_normalize(int d, int64_t T, const void* u, bool u16, const void* ref, bool r16,
@@ -225,12 +225,9 @@ hipError_t launch_variance_loss(const int32_t* idx, const float* coef, int64_t T
 hipError_t launch_variance_grad(int64_t T, int k, int64_t nfeat, int S, void* ws, float* grad,
                                 const float* grad_scale, hipStream_t stream);
 
+// General encoder (encode_general.hip) for plans outside the narrow and wide encoders.
 hipError_t launch_encode(const DevPlan& P, const void* x, bool x_bf16, int64_t T, int32_t* idx,
                          float* coef, hipStream_t stream);
-hipError_t launch_decode(const DevPlan& P, const int32_t* idx, const float* coef, int64_t T, void* y,
-                         bool y_bf16, hipStream_t stream);
-hipError_t launch_decode_bwd(const DevPlan& P, const int32_t* idx, const void* g, bool g_bf16, int64_t T,
-                             float* grad_coef, void* grad_x, bool gx_bf16, hipStream_t stream);
 
 }  // namespace dpb
 

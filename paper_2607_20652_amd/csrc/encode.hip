@@ -530,9 +530,11 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
                 int c = 0;
 #pragma unroll
                 for (int r = 0; r < R; ++r) c += (int)(keys[r] >= tau);
+                // c <= R keys per lane (R = 4, 8 or 16): 3, 4 or 5 count bits
+                constexpr int CBITS = R <= 4 ? 3 : R <= 8 ? 4 : 5;
                 int before = 0, total = 0;
 #pragma unroll
-                for (int b = 0; b < 3; ++b) {   // c <= R = 4
+                for (int b = 0; b < CBITS; ++b) {
                     const uint64_t m = __ballot((c >> b) & 1);
                     before += (int)__popcll(m & before_mask) << b;
                     total += (int)__popcll(m & token_mask) << b;

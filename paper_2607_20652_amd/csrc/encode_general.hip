@@ -1,51 +1,25 @@
-// HIP kernels for gfx950 (CDNA4): DPB encode, decode and decode-backward.
-//
-// Sign generation: the sign of feature i at coordinate iota is the parity of
-// (M_iota AND i) (App. A.4, packed-parity equation) -- one AND and one
-// popcount per entry, computed in registers.
+// General encoder for gfx950: the top-down beam search of §2.2 for plans the
+// narrow encoder (encode.hip: every level's candidates in one wave's
+// registers) and the wide encoder (many children per parent, with a
+// workspace) do not cover -- e.g. full generator sets of thousands of
+// children per parent, or more level-0 features than a wave has lanes.
 //
 // Encode scores the children of the active parents with the matrix cores:
 // for level l and a tile of (token, parent) columns,
 //     S[j, (t,p)] = sum_iota gamma_j[iota] * (phi~_p (.) x_t)[iota]
 // (§2.2 child-scoring equation), with Gamma_l as the 16 x 32 bf16 A
-// fragments (exactly +-1) and the sign-flipped activations as B fragments.
-// Products of +-1 with bf16 are exact and accumulate in fp32; fp32 inputs
-// are split exactly into three bf16 terms.
-#include "dpb_internal.hpp"
+// fragments (exactly +-1) and the sign-flipped activations as B fragments,
+// the sign of feature p at coordinate iota being the parity of (M_iota AND p)
+// (App. A.4, packed-parity equation).  Products of +-1 with bf16 are exact
+// and accumulate in fp32; fp32 inputs are split exactly into three bf16
+// terms.  The keys of a token's candidates are sorted in LDS by a bitonic
+// network over the workgroup.
+#include "device_common.hpp"
 
 namespace dpb {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-
 constexpr int kWaves = kBlock / 64;
-
-__device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
-
-// float -> bf16 bits, round to nearest even.
-__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f)
-{
-    uint32_t u = __float_as_uint(f);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return u >> 16;
-}
-
-__device__ __forceinline__ uint32_t parity(uint32_t v) { return __popc(v) & 1u; }
-
-// AbsTopK sort key: |s| (as fp32 bits) first, then the smaller index, with
-// the sign of s in bit 0 so that the signed coefficient can be rebuilt.
-__device__ __forceinline__ uint64_t make_key(float s, uint32_t idx)
-{
-    const uint32_t u = __float_as_uint(s);
-    return ((uint64_t)(u & 0x7FFFFFFFu) << 32) | (uint64_t)(((0x7FFFFFFFu - idx) << 1) | (u >> 31));
-}
-__device__ __forceinline__ uint32_t key_index(uint64_t key) { return 0x7FFFFFFFu - ((uint32_t)key >> 1); }
-__device__ __forceinline__ float key_value(uint64_t key)
-{
-    return __uint_as_float((uint32_t)(key >> 32) | (((uint32_t)key & 1u) << 31));
-}
 
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v)
 {
@@ -62,131 +36,6 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v)
     return ((uint64_t)hi << 32) | lo;
 }
 
-__device__ __forceinline__ float wave_sum(float v)
-{
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-    return v;
-}
-
-template <bool BF16>
-__device__ __forceinline__ float load_act(const void* p, int64_t i)
-{
-    if constexpr (BF16) return bf16_bits_to_f32(((const uint16_t*)p)[i]);
-    else return ((const float*)p)[i];
-}
-
-template <bool BF16>
-__device__ __forceinline__ void store_act(void* p, int64_t i, float v)
-{
-    if constexpr (BF16) ((uint16_t*)p)[i] = (uint16_t)f32_to_bf16_rne(v);
-    else ((float*)p)[i] = v;
-}
-
-// ---------------------------------------------------------------------------
-// Decode: y = sum_s coef_s phi_{idx_s}.  A workgroup takes kCodeTokens tokens;
-// each thread owns coordinates iota and walks the token's slots (uniform
-// across the workgroup).  Basis slots add coef at their own coordinate;
-// hashed slots add +-coef everywhere and are scaled by 1/sqrt(d) once.
-// ---------------------------------------------------------------------------
-constexpr int kCodeTokens = 8;
-
-template <bool OUT_BF16>
-__global__ __launch_bounds__(kBlock) void decode_kernel(DevPlan P, const int32_t* __restrict__ idx,
-                                                        const float* __restrict__ coef, int64_t T,
-                                                        void* __restrict__ y)
-{
-    extern __shared__ __align__(16) unsigned char smem[];
-    const int k = P.k_tot;
-    int32_t* s_idx = (int32_t*)smem;
-    float* s_coef = (float*)(s_idx + kCodeTokens * k);
-    const int64_t t0 = (int64_t)blockIdx.x * kCodeTokens;
-    const int ntok = (int)min((int64_t)kCodeTokens, T - t0);
-    for (int i = threadIdx.x; i < ntok * k; i += kBlock) {
-        s_idx[i] = idx[t0 * k + i];
-        s_coef[i] = coef[t0 * k + i];
-    }
-    __syncthreads();
-    for (int tt = 0; tt < ntok; ++tt) {
-        const int32_t* ti = s_idx + tt * k;
-        const float* tc = s_coef + tt * k;
-        for (int iota = threadIdx.x; iota < P.d; iota += kBlock) {
-            const uint32_t m = P.masks[iota];
-            float acc_b = 0.f, acc_h = 0.f;
-            for (int s = 0; s < k; ++s) {
-                const int i = ti[s];
-                const float a = tc[s];
-                if (i < 0) continue;
-                if (i < P.d) {
-                    if (i == iota) acc_b += a;
-                } else {
-                    acc_h += __uint_as_float(__float_as_uint(a) ^ (parity(m & (uint32_t)i) << 31));
-                }
-            }
-            store_act<OUT_BF16>(y, (t0 + tt) * P.d + iota, acc_b + P.rsd * acc_h);
-        }
-    }
-}
-
-// ---------------------------------------------------------------------------
-// Decode backward: grad_coef[s] = <phi_{idx_s}, g>, then grad_x = decode of
-// grad_coef.  One wave reduces one token's slot over the coordinates.
-// ---------------------------------------------------------------------------
-template <bool G_BF16, bool GX_BF16>
-__global__ __launch_bounds__(kBlock) void decode_bwd_kernel(DevPlan P, const int32_t* __restrict__ idx,
-                                                            const void* __restrict__ g, int64_t T,
-                                                            float* __restrict__ grad_coef,
-                                                            void* __restrict__ grad_x, int tpb)
-{
-    extern __shared__ __align__(16) unsigned char smem[];
-    const int k = P.k_tot, d = P.d;
-    int32_t* s_idx = (int32_t*)smem;            // [tpb][k]
-    float* s_gc = (float*)(s_idx + tpb * k);    // [tpb][k]
-    float* s_g = s_gc + tpb * k;                // [tpb][d]
-    uint32_t* s_m = (uint32_t*)(s_g + tpb * d); // [d]
-    const int64_t t0 = (int64_t)blockIdx.x * tpb;
-    const int ntok = (int)min((int64_t)tpb, T - t0);
-    for (int i = threadIdx.x; i < ntok * k; i += kBlock) s_idx[i] = idx[t0 * k + i];
-    for (int i = threadIdx.x; i < ntok * d; i += kBlock) s_g[i] = load_act<G_BF16>(g, t0 * d + i);
-    for (int i = threadIdx.x; i < d; i += kBlock) s_m[i] = P.masks[i];
-    __syncthreads();
-
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    for (int tt = wave; tt < ntok; tt += kWaves) {
-        const float* gt = s_g + tt * d;
-        for (int s = 0; s < k; ++s) {
-            const int i = s_idx[tt * k + s];
-            float part = 0.f;
-            if (i >= d) {
-                for (int iota = lane; iota < d; iota += 64)
-                    part += __uint_as_float(__float_as_uint(gt[iota]) ^ (parity(s_m[iota] & (uint32_t)i) << 31));
-            }
-            const float sum = wave_sum(part);
-            if (lane == 0) s_gc[tt * k + s] = i < 0 ? 0.f : (i < d ? gt[i] : P.rsd * sum);
-        }
-    }
-    __syncthreads();
-    for (int i = threadIdx.x; i < ntok * k; i += kBlock) grad_coef[t0 * k + i] = s_gc[i];
-    for (int tt = 0; tt < ntok; ++tt) {
-        const int32_t* ti = s_idx + tt * k;
-        const float* tc = s_gc + tt * k;
-        for (int iota = threadIdx.x; iota < d; iota += kBlock) {
-            const uint32_t m = s_m[iota];
-            float acc_b = 0.f, acc_h = 0.f;
-            for (int s = 0; s < k; ++s) {
-                const int i = ti[s];
-                const float a = tc[s];
-                if (i < 0) continue;
-                if (i < d) {
-                    if (i == iota) acc_b += a;
-                } else {
-                    acc_h += __uint_as_float(__float_as_uint(a) ^ (parity(m & (uint32_t)i) << 31));
-                }
-            }
-            store_act<GX_BF16>(grad_x, (t0 + tt) * d + iota, acc_b + P.rsd * acc_h);
-        }
-    }
-}
 
 // ---------------------------------------------------------------------------
 // Encode.  A workgroup owns a tile of tokens held in LDS; levels run in turn.
@@ -393,15 +242,6 @@ __global__ __launch_bounds__(kBlock) void encode_kernel(DevPlan P, const void* _
     }
 }
 
-size_t bwd_lds_bytes(const DevPlan& P, int tpb) { return (size_t)tpb * (P.k_tot * 8 + P.d * 4) + (size_t)P.d * 4; }
-
-int bwd_tokens_per_block(const DevPlan& P)
-{
-    int tpb = kCodeTokens;
-    while (tpb > 1 && bwd_lds_bytes(P, tpb) > (size_t)kLdsBudget) --tpb;
-    return tpb;
-}
-
 int pick_tile_tokens(const DevPlan& P, int x_bytes)
 {
     int tt = 16;
@@ -411,11 +251,7 @@ int pick_tile_tokens(const DevPlan& P, int x_bytes)
 
 }  // namespace
 
-bool plan_fits(const DevPlan& P)
-{
-    return encode_layout(P, 4, 1).bytes <= (unsigned)kLdsBudget && bwd_lds_bytes(P, 1) <= (size_t)kLdsBudget &&
-           (size_t)kCodeTokens * P.k_tot * 8 <= (size_t)kLdsBudget;
-}
+bool general_encoder_fits(const DevPlan& P) { return encode_layout(P, 4, 1).bytes <= (unsigned)kLdsBudget; }
 
 hipError_t launch_encode(const DevPlan& P, const void* x, bool x_bf16, int64_t T, int32_t* idx, float* coef,
                          hipStream_t stream)
@@ -434,38 +270,6 @@ hipError_t launch_encode(const DevPlan& P, const void* x, bool x_bf16, int64_t T
     else
         hipLaunchKernelGGL(encode_kernel<false>, dim3((unsigned)blocks), dim3(kBlock), L.bytes, stream, P, x, T,
                            idx, coef, tt);
-    return hipGetLastError();
-}
-
-hipError_t launch_decode(const DevPlan& P, const int32_t* idx, const float* coef, int64_t T, void* y, bool y_bf16,
-                         hipStream_t stream)
-{
-    const size_t lds = (size_t)kCodeTokens * P.k_tot * 8;
-    const int64_t blocks = (T + kCodeTokens - 1) / kCodeTokens;
-    if (lds > (size_t)kLdsBudget || blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
-    if (y_bf16)
-        hipLaunchKernelGGL(decode_kernel<true>, dim3((unsigned)blocks), dim3(kBlock), lds, stream, P, idx, coef, T, y);
-    else
-        hipLaunchKernelGGL(decode_kernel<false>, dim3((unsigned)blocks), dim3(kBlock), lds, stream, P, idx, coef, T, y);
-    return hipGetLastError();
-}
-
-hipError_t launch_decode_bwd(const DevPlan& P, const int32_t* idx, const void* g, bool g_bf16, int64_t T,
-                             float* grad_coef, void* grad_x, bool gx_bf16, hipStream_t stream)
-{
-    const int tpb = bwd_tokens_per_block(P);
-    const size_t lds = bwd_lds_bytes(P, tpb);
-    const int64_t blocks = (T + tpb - 1) / tpb;
-    if (lds > (size_t)kLdsBudget || blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
-    const dim3 grid((unsigned)blocks), block(kBlock);
-    if (g_bf16 && gx_bf16)
-        hipLaunchKernelGGL((decode_bwd_kernel<true, true>), grid, block, lds, stream, P, idx, g, T, grad_coef, grad_x, tpb);
-    else if (g_bf16)
-        hipLaunchKernelGGL((decode_bwd_kernel<true, false>), grid, block, lds, stream, P, idx, g, T, grad_coef, grad_x, tpb);
-    else if (gx_bf16)
-        hipLaunchKernelGGL((decode_bwd_kernel<false, true>), grid, block, lds, stream, P, idx, g, T, grad_coef, grad_x, tpb);
-    else
-        hipLaunchKernelGGL((decode_bwd_kernel<false, false>), grid, block, lds, stream, P, idx, g, T, grad_coef, grad_x, tpb);
     return hipGetLastError();
 }
 

@@ -2,7 +2,7 @@
 // Standardization") for gfx950.
 //
 // State, owned by the caller: stats[N] = (mu, r = 1/sigma) as float2, read by
-// the encoder, and var[N] (the EMA of the variance).  After a batch encoded
+// the encoder, and m2[N] (the EMA of the second raw moment).  After a batch encoded
 // with the state, the moments of each feature over the tokens where it was a
 // candidate update it:
 //  * level 0: a basis feature is a candidate at every token, so its sample is
@@ -15,9 +15,11 @@
 //    combined with fp64 atomics in a per-feature accumulator that only the
 //    records themselves clear, and the record with the lowest position
 //    applies the update.
-// Update of a feature with n samples, mean m1, population variance v:
-//    mu <- (1 - beta) mu + beta m1,  var <- (1 - beta) var + beta v,
-//    r = 1 / sqrt(var + eps).
+// Update of a feature with n samples s_1..s_n (moving averages of the first
+// two raw moments, so that a feature sampled once per batch still measures
+// its spread across batches):
+//    mu <- (1 - beta) mu + beta mean(s),  m2 <- (1 - beta) m2 + beta mean(s^2),
+//    r = 1 / sqrt(max(m2 - mu^2, 0) + eps).
 #include <algorithm>
 
 #include "dpb_internal.hpp"
@@ -72,22 +74,20 @@ __host__ __device__ inline StdWs std_ws(void* ws, const DevPlan& P, size_t* tota
     return W;
 }
 
-__device__ __forceinline__ void ema(float2* stats, float* var, int64_t c, double n, double s1, double s2, float beta,
+__device__ __forceinline__ void ema(float2* stats, float* m2, int64_t c, double n, double s1, double s2, float beta,
                                     float eps)
 {
-    const double m1 = s1 / n;
-    const double v = fmax(s2 / n - m1 * m1, 0.0);
-    const float mu = (1.f - beta) * stats[c].x + beta * (float)m1;
-    const float vv = (1.f - beta) * var[c] + beta * (float)v;
-    var[c] = vv;
-    stats[c] = make_float2(mu, 1.f / sqrtf(vv + eps));
+    const float mu = (1.f - beta) * stats[c].x + beta * (float)(s1 / n);
+    const float q = (1.f - beta) * m2[c] + beta * (float)(s2 / n);
+    m2[c] = q;
+    stats[c] = make_float2(mu, 1.f / sqrtf(fmaxf(q - mu * mu, 0.f) + eps));
 }
 
-__global__ void std_init_kernel(float2* stats, float* var, int64_t N)
+__global__ void std_init_kernel(float2* stats, float* m2, int64_t N)
 {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N; i += (int64_t)gridDim.x * blockDim.x) {
         stats[i] = make_float2(0.f, 1.f);
-        var[i] = 1.f;
+        m2[i] = 1.f;
     }
 }
 
@@ -167,7 +167,7 @@ __global__ __launch_bounds__(kStdThreads * kStdColSlices) void std_col_kernel(co
     }
 }
 
-__global__ void std_col_update_kernel(int d, int64_t T, StdWs W, float2* stats, float* var, float beta, float eps)
+__global__ void std_col_update_kernel(int d, int64_t T, StdWs W, float2* stats, float* m2, float beta, float eps)
 {
     const int c = blockIdx.x * blockDim.x + threadIdx.x;
     if (c >= d || T <= 0) return;
@@ -176,7 +176,7 @@ __global__ void std_col_update_kernel(int d, int64_t T, StdWs W, float2* stats, 
         s1 += W.col[((int64_t)g * d + c) * 2];
         s2 += W.col[((int64_t)g * d + c) * 2 + 1];
     }
-    ema(stats, var, c, (double)T, s1, s2, beta, eps);
+    ema(stats, m2, c, (double)T, s1, s2, beta, eps);
 }
 
 // kStdSlices workgroups per (sample token, level l >= 1): the token's
@@ -186,7 +186,7 @@ __global__ void std_col_update_kernel(int d, int64_t T, StdWs W, float2* stats, 
 // holds the same child; each wave scores one candidate at a time, lanes over
 // the coordinates, and the slices of a list take turns (more waves in flight
 // for the few sampled tokens).
-constexpr int kStdMaxCand = 4096;
+constexpr int kStdMaxCand = 8192;   // K_{l-1} Delta_l of the paper's 3-level hierarchy (32 x 256)
 constexpr int kStdSlices = 8;   // workgroups sharing one sampled token's candidates of a level
 
 template <bool BF16>
@@ -252,13 +252,13 @@ __global__ void std_rec_accum_kernel(int64_t nrec, StdWs W)
     }
 }
 
-__global__ void std_rec_update_kernel(int64_t nrec, StdWs W, float2* stats, float* var, float beta, float eps)
+__global__ void std_rec_update_kernel(int64_t nrec, StdWs W, float2* stats, float* m2, float beta, float eps)
 {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nrec; i += (int64_t)gridDim.x * blockDim.x) {
         const StdRec r = W.rec[i];
         if (r.feat < 0) continue;
         const StdAcc a = W.acc[r.feat];
-        if (a.owner == (uint32_t)i) ema(stats, var, r.feat, (double)a.n, a.s1, a.s2, beta, eps);
+        if (a.owner == (uint32_t)i) ema(stats, m2, r.feat, (double)a.n, a.s1, a.s2, beta, eps);
     }
 }
 
@@ -284,15 +284,15 @@ size_t std_workspace_bytes(const DevPlan& P)
     return total;
 }
 
-hipError_t launch_std_init(const DevPlan& P, float* stats, float* var, hipStream_t stream)
+hipError_t launch_std_init(const DevPlan& P, float* stats, float* m2, hipStream_t stream)
 {
     const int64_t N = (int64_t)1 << P.level_bits[P.levels - 1];
-    hipLaunchKernelGGL(std_init_kernel, std_grid(N, 256), dim3(256), 0, stream, (float2*)stats, var, N);
+    hipLaunchKernelGGL(std_init_kernel, std_grid(N, 256), dim3(256), 0, stream, (float2*)stats, m2, N);
     return hipGetLastError();
 }
 
 hipError_t launch_std_update(const DevPlan& P, const void* x, bool x_bf16, int64_t T, const int32_t* idx,
-                             float beta, float eps, float* stats, float* var, void* ws, hipStream_t stream)
+                             float beta, float eps, float* stats, float* m2, void* ws, hipStream_t stream)
 {
     const StdWs W = std_ws(ws, P, nullptr);
     float2* st = (float2*)stats;
@@ -300,7 +300,7 @@ hipError_t launch_std_update(const DevPlan& P, const void* x, bool x_bf16, int64
     const dim3 bc(kStdThreads * kStdColSlices);
     if (x_bf16) hipLaunchKernelGGL(std_col_kernel<true>, gc, bc, 0, stream, x, P.d, T, W);
     else hipLaunchKernelGGL(std_col_kernel<false>, gc, bc, 0, stream, x, P.d, T, W);
-    hipLaunchKernelGGL(std_col_update_kernel, dim3((P.d + 255) / 256), dim3(256), 0, stream, P.d, T, W, st, var, beta,
+    hipLaunchKernelGGL(std_col_update_kernel, dim3((P.d + 255) / 256), dim3(256), 0, stream, P.d, T, W, st, m2, beta,
                        eps);
     const int m = (int)std::min<int64_t>(T, kStdSample);
     if (P.levels > 1 && m > 0) {
@@ -313,7 +313,7 @@ hipError_t launch_std_update(const DevPlan& P, const void* x, bool x_bf16, int64
         const int64_t nrec = (int64_t)m * std_cands(P);
         hipLaunchKernelGGL(std_rec_clear_kernel, std_grid(nrec, 256), dim3(256), 0, stream, nrec, W);
         hipLaunchKernelGGL(std_rec_accum_kernel, std_grid(nrec, 256), dim3(256), 0, stream, nrec, W);
-        hipLaunchKernelGGL(std_rec_update_kernel, std_grid(nrec, 256), dim3(256), 0, stream, nrec, W, st, var, beta,
+        hipLaunchKernelGGL(std_rec_update_kernel, std_grid(nrec, 256), dim3(256), 0, stream, nrec, W, st, m2, beta,
                            eps);
     }
     return hipGetLastError();

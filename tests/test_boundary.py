@@ -84,12 +84,12 @@ def test_plan_create_rejects_bad_arguments_before_touching_the_gpu(lib, args, st
 
 def test_compute_calls_reject_null_plan(lib):
     P = ctypes.c_void_p
-    assert lib.dpb_encode(None, P(16), 0, 4, P(16), P(16), None) == -1
+    assert lib.dpb_encode(None, P(16), 0, 4, P(16), P(16), None, 0, None) == -1
     assert lib.dpb_decode(None, P(16), P(16), 4, P(16), 0, None) == -1
     assert lib.dpb_decode_bwd(None, P(16), P(16), 0, 4, P(16), P(16), 0, None) == -1
     assert lib.dpb_decode_bwd_ex(None, P(16), P(16), 0, 4, None, None, None, P(16), P(16), 0, None) == -1
-    assert lib.dpb_encode_std(None, P(16), 0, 4, P(16), P(16), P(16), None) == -1
-    assert lib.dpb_encode_ws(None, P(16), 0, 4, None, P(16), P(16), None, 0, None) == -1
+    assert lib.dpb_encode_std(None, P(16), 0, 4, P(16), P(16), P(16), None, 0, None) == -1
+    assert lib.dpb_plan_tables(None, P(16), P(16)) == -1
     assert lib.dpb_encode_workspace_bytes(None, 4) == 0
     assert lib.dpb_std_init(None, P(16), P(16), None) == -1
     assert lib.dpb_std_update(None, P(16), 0, 4, P(16), 0.1, 1e-6, P(16), P(16), P(16), 1 << 20, None) == -1

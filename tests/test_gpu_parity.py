@@ -15,7 +15,7 @@ import torch
 import oracle
 from paper_2607_20652_amd import binding as dpb
 from paper_2607_20652_amd import inputs
-from parity_util import TOL_BF16, TOL_F32, compare_dense, compare_encode
+from parity_util import TOL_BF16, TOL_F32, compare_dense, compare_encode, EncodeCheck
 
 pytestmark = pytest.mark.gpu
 
@@ -78,7 +78,8 @@ def test_encode_matches_oracle(name, T):
     idx, coef = dpb.encode(plan, x.to(DEV))
     torch.cuda.synchronize()
     oi, oc, om, oo = oracle.encode(w.d, m, nb, K, dl, gens, x.double().numpy())
-    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32)
+    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32,
+                        ctx=EncodeCheck(w.d, m, gens, x.double().numpy()))
     say(f"  {st}")
     assert st["exempt_tokens"] <= max(2, 0.02 * T)
 
@@ -93,7 +94,8 @@ def test_encode_f32_input_matches_oracle(name, T):
     idx, coef = dpb.encode(plan, x.to(DEV))
     torch.cuda.synchronize()
     oi, oc, om, oo = oracle.encode(w.d, m, nb, K, dl, gens, x.double().numpy())
-    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32)
+    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32,
+                        ctx=EncodeCheck(w.d, m, gens, x.double().numpy()))
     say(f"  {st}")
     assert st["exempt_tokens"] <= max(2, 0.02 * T)
 
@@ -109,7 +111,8 @@ def test_encode_full_size_sampled(name, rows):
     torch.cuda.synchronize()
     r = sample_rows(w.tokens, rows, seed=w.index)
     oi, oc, om, oo = oracle.encode(w.d, m, nb, K, dl, gens, x[r].double().numpy())
-    st = compare_encode(K, idx.cpu().numpy()[r], coef.cpu().numpy()[r], oi, oc, om, oo, TOL_F32)
+    st = compare_encode(K, idx.cpu().numpy()[r], coef.cpu().numpy()[r], oi, oc, om, oo, TOL_F32,
+                        ctx=EncodeCheck(w.d, m, gens, x[r].double().numpy()))
     say(f"  {st}")
     assert st["exempt_tokens"] <= max(2, 0.02 * len(r))
     # every emitted index is unique within its token and lies in its level
@@ -138,8 +141,70 @@ def test_encode_exhaustive_generators_tiny():
     torch.cuda.synchronize()
     m = oracle.masks(d, nb[-1])
     oi, oc, om, oo = oracle.encode(d, m, nb, K, dl, [np.zeros(0, np.uint32)] + full, x.double().numpy())
-    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32)
+    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32,
+                        ctx=EncodeCheck(d, m, [np.zeros(0, np.uint32)] + full, x.double().numpy()))
     say(f"  {st}")
+
+
+# Narrow-encoder plans with 32 and 64 children per parent: 8 or 16 keys per
+# lane (two or four generator tiles) in the threshold selection of the beam
+# levels, whose per-lane counts then need 4 or 5 bits.  "k2" keeps 2 level-0
+# parents and 16 of their 64 children, so fewer lanes than K_1 hold keys: the
+# threshold is 1 and every live lane counts all 8 of its keys.
+NARROW_BRANCHY = {
+    "k2": dict(d=2048, level_bits=(11, 14, 17), branchings=(0, 32, 32), active=(2, 16, 24)),
+    "b32": dict(d=768, level_bits=(10, 13, 16, 19), branchings=(0, 32, 32, 32), active=(8, 8, 8, 32)),
+    "b64": dict(d=1024, level_bits=(10, 13, 16, 20), branchings=(0, 64, 64, 64), active=(4, 4, 8, 32)),
+}
+
+
+def _branchy(hname):
+    h = NARROW_BRANCHY[hname]
+    d, nb, dl, K = h["d"], list(h["level_bits"]), list(h["branchings"]), list(h["active"])
+    plan = dpb.Plan(d, seed=0, level_bits=nb, branchings=dl, active=K)
+    assert dpb.load().dpb_encode_workspace_bytes(plan._handle, 100) == 0   # the narrow encoder runs it
+    return plan, d, nb, dl, K, oracle.masks(d, nb[-1]), oracle.generators(nb, dl, 0)
+
+
+@pytest.mark.parametrize("hname,T", [("k2", 64), ("k2", 33), ("b32", 200), ("b32", 31), ("b64", 150)])
+def test_encode_narrow_many_children_per_parent(hname, T):
+    say(f"[encode branchy] {hname} T={T}")
+    plan, d, nb, dl, K, m, gens = _branchy(hname)
+    x = inputs.normal((T, d), 1100 + T + len(hname), "bf16")
+    idx, coef = dpb.encode(plan, x.to(DEV))
+    torch.cuda.synchronize()
+    oi, oc, om, oo = oracle.encode(d, m, nb, K, dl, gens, x.double().numpy())
+    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32,
+                        ctx=EncodeCheck(d, m, gens, x.double().numpy()))
+    say(f"  {st}")
+    assert st["exempt_tokens"] <= max(2, 0.02 * T)
+    assert (idx.cpu().numpy() >= 0).all()   # every level has enough candidates: no padding
+
+
+def test_encode_one_lane_holds_eight_keys_above_threshold():
+    """A token whose level-1 top 8 are exactly the 8 children one lane of the
+    matrix-core layout holds (generators 0-3 and 16-19 of one parent column),
+    so that lane counts 8 keys at or above the threshold."""
+    say("[encode branchy crafted] b32")
+    plan, d, nb, dl, K, m, gens = _branchy("b32")
+    x = inputs.normal((6, d), 1200, "bf16").double().numpy() * 0.05
+    p = 123
+    lane_rows = [0, 1, 2, 3, 16, 17, 18, 19]
+    kids = [p ^ int(gens[1][j]) for j in lane_rows]
+    for t in (0, 3):
+        x[t, p] = 8.0
+        for c in kids:
+            x[t] += 3.0 * oracle.phi(d, m, c)
+    xb = torch.from_numpy(x).to(torch.bfloat16)
+    idx, coef = dpb.encode(plan, xb.to(DEV))
+    torch.cuda.synchronize()
+    oi, oc, om, oo = oracle.encode(d, m, nb, K, dl, gens, xb.double().numpy())
+    for t in (0, 3):
+        assert oi[t, 0] == p and sorted(oi[t, K[0]:K[0] + K[1]].tolist()) == sorted(kids)
+    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32,
+                        ctx=EncodeCheck(d, m, gens, xb.double().numpy()))
+    say(f"  {st}")
+    assert sorted(idx.cpu().numpy()[0, K[0]:K[0] + K[1]].tolist()) == sorted(kids)
 
 
 def test_encode_dyadic_ties_tiny():

@@ -18,7 +18,7 @@ import oracle
 from paper_2607_20652_amd import autograd as dpb_autograd
 from paper_2607_20652_amd import binding as dpb
 from paper_2607_20652_amd import inputs
-from parity_util import TOL_BF16, TOL_F32, compare_dense, compare_encode
+from parity_util import TOL_BF16, TOL_F32, compare_dense, compare_encode, random_std_state, EncodeCheck
 
 pytestmark = pytest.mark.gpu
 
@@ -52,11 +52,7 @@ def setup(name):
 
 
 def random_state(N, seed, scale=1.0):
-    rng = np.random.default_rng(seed)
-    mu = (0.3 * scale * rng.standard_normal(N)).astype(np.float32)
-    var = rng.uniform(0.3, 3.0, N).astype(np.float32)
-    r = (1.0 / np.sqrt(var.astype(np.float64) + 1e-6)).astype(np.float32)
-    return mu, var, r
+    return random_std_state(N, seed, scale)
 
 
 def device_stats(mu, r):
@@ -86,7 +82,8 @@ def test_encode_std_matches_oracle(name, T, f32):
     idx, coef = dpb.encode_std(plan, x.to(DEV), device_stats(mu, r))
     torch.cuda.synchronize()
     oi, oc, om, oo = oracle.encode_std(w.d, m, nb, K, dl, gens, x.double().numpy(), mu, r)
-    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32)
+    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32,
+                        ctx=EncodeCheck(w.d, m, gens, x.double().numpy(), mu, r))
     say(f"  {st}")
     assert st["exempt_tokens"] <= max(2, 0.02 * T)
 
@@ -103,7 +100,8 @@ def test_encode_std_full_size_sampled():
     rows = np.unique(np.concatenate([np.arange(64), np.random.default_rng(2).choice(w.tokens, 128, replace=False),
                                      np.arange(w.tokens - 64, w.tokens)]))
     oi, oc, om, oo = oracle.encode_std(w.d, m, nb, K, dl, gens, x[rows].double().numpy(), mu, r)
-    st = compare_encode(K, idx.cpu().numpy()[rows], coef.cpu().numpy()[rows], oi, oc, om, oo, TOL_F32)
+    st = compare_encode(K, idx.cpu().numpy()[rows], coef.cpu().numpy()[rows], oi, oc, om, oo, TOL_F32,
+                        ctx=EncodeCheck(w.d, m, gens, x[rows].double().numpy(), mu, r))
     say(f"  {st}")
     assert st["exempt_tokens"] <= max(2, 0.02 * len(rows))
 
@@ -115,28 +113,37 @@ def test_std_update_matches_oracle(name, T, beta):
     plan = plan_for(name)
     w, nb, dl, K, m, gens = setup(name)
     N = 1 << w.n
-    mu, var, r = random_state(N, 31 + w.index)
+    mu, m2, r = random_state(N, 31 + w.index)
     stats = device_stats(mu, r)
-    vard = torch.from_numpy(var).to(DEV)
+    m2d = torch.from_numpy(m2).to(DEV)
     x = inputs.activations(name, T)
     idx, _ = dpb.encode_std(plan, x.to(DEV), stats)
     before = stats.clone()
-    dpb.std_update(plan, x.to(DEV), idx, stats, vard, beta, 1e-6)
+    dpb.std_update(plan, x.to(DEV), idx, stats, m2d, beta, 1e-6)
     torch.cuda.synchronize()
-    rmu, rvar = oracle.std_update(w.d, m, nb, K, dl, gens, x.double().numpy(), idx.cpu().numpy(),
-                                  mu.astype(np.float64), var.astype(np.float64), beta)
-    gs, gv = stats.cpu().numpy(), vard.cpu().numpy()
-    touched = (rmu != mu.astype(np.float64)) | (rvar != var.astype(np.float64))
+    rmu, rm2 = oracle.std_update(w.d, m, nb, K, dl, gens, x.double().numpy(), idx.cpu().numpy(),
+                                  mu.astype(np.float64), m2.astype(np.float64), beta)
+    gs, gv = stats.cpu().numpy(), m2d.cpu().numpy()
+    touched = (rmu != mu.astype(np.float64)) | (rm2 != m2.astype(np.float64))
     say(f"  touched {int(touched.sum())} of {N}")
     assert np.array_equal(gs[~touched], before.cpu().numpy()[~touched])
-    assert np.array_equal(gv[~touched], var[~touched])
-    # raw scores here are O(1) (unit-norm directions, unit-variance inputs): a
-    # score off by its fp32 accumulation error moves mean and variance by
-    # ~1e-6 absolutely, which is large relative to a near-zero variance of
-    # a few nearly equal samples, hence the absolute part of the bound
+    assert np.array_equal(gv[~touched], m2[~touched])
+    # raw scores here are O(1) (unit-norm directions, unit-variance inputs):
+    # fp32 accumulation and the fp32 state update move mean and second moment
+    # by ~1e-6 absolutely, hence the absolute part of the bound
     assert np.allclose(gs[touched, 0], rmu[touched], rtol=1e-5, atol=1e-5)
-    assert np.allclose(gv[touched], rvar[touched], rtol=1e-5, atol=1e-5)
-    assert np.allclose(gs[touched, 1], 1.0 / np.sqrt(gv[touched].astype(np.float64) + 1e-6), rtol=1e-6, atol=0)
+    assert np.allclose(gv[touched], rm2[touched], rtol=1e-5, atol=1e-5)
+    # r is the one the GPU's own fp32 (mu, m2) imply (fp32 subtraction m2 - mu^2)
+    rr = oracle.std_r(gs[touched, 0].astype(np.float64), gv[touched].astype(np.float64), 1e-6)
+    assert np.allclose(gs[touched, 1], rr, rtol=2e-6, atol=0)
+    # and the oracle's own state's r where the variance is not a small
+    # difference of the two moments (there fp32 rounding of m2 and mu^2
+    # dominates it: e.g. a single sample with beta = 1 has variance exactly 0)
+    well = touched & (rm2 - rmu ** 2 > 1e-2 * rm2)
+    ro = oracle.std_r(rmu[well], rm2[well], 1e-6)
+    assert np.allclose(gs[well, 1], ro, rtol=1e-4, atol=0)
+    if beta < 1.0:
+        assert well.sum() > 0.9 * touched.sum()
 
 
 @pytest.mark.parametrize("name,T", [("tiny", 77), ("train", 500)])
@@ -167,9 +174,9 @@ def test_standardized_layer_matches_oracle_and_updates(name, T):
     plan = plan_for(name)
     w, nb, dl, K, m, gens = setup(name)
     std = dpb_autograd.Standardizer(plan, momentum=0.1, eps=1e-6)
-    mu, var, r = random_state(1 << w.n, 51)
+    mu, m2, r = random_state(1 << w.n, 51)
     std.stats.copy_(device_stats(mu, r))
-    std.var.copy_(torch.from_numpy(var))
+    std.m2.copy_(torch.from_numpy(m2))
     x = inputs.activations(name, T).to(DEV).requires_grad_(True)
     gy = inputs.upstream_grad(name, T).to(DEV)
     y, lv = dpb_autograd.dpb_layer(x, plan, True, 2, std)
@@ -184,8 +191,8 @@ def test_standardized_layer_matches_oracle_and_updates(name, T):
     _, rgx = oracle.layer_backward(w.d, m, ii, cc, xd, gy.double().cpu().numpy(), 0.5, 2, True, r_slot=rs)
     compare_dense(x.grad.float().cpu().numpy(), rgx, TOL_F32 if w.dtype == "f32" else TOL_BF16)
     # the training backward applied the EMA update of this batch
-    rmu, rvar = oracle.std_update(w.d, m, nb, K, dl, gens, xd, ii, mu.astype(np.float64), var.astype(np.float64),
+    rmu, rm2 = oracle.std_update(w.d, m, nb, K, dl, gens, xd, ii, mu.astype(np.float64), m2.astype(np.float64),
                                   0.1)
     gs = std.stats.cpu().numpy()
     assert np.allclose(gs[:, 0], rmu, rtol=1e-5, atol=1e-5)
-    assert np.allclose(std.var.cpu().numpy(), rvar, rtol=1e-5, atol=1e-5)
+    assert np.allclose(std.m2.cpu().numpy(), rm2, rtol=1e-5, atol=1e-5)

@@ -13,7 +13,8 @@ import torch
 import oracle
 from paper_2607_20652_amd import binding as dpb
 from paper_2607_20652_amd import inputs
-from parity_util import TOL_BF16, TOL_F32, compare_dense, compare_encode
+from paper_2607_20652_amd import autograd as dpb_autograd
+from parity_util import TOL_BF16, TOL_F32, compare_dense, compare_encode, random_std_state, EncodeCheck
 
 pytestmark = pytest.mark.gpu
 
@@ -64,7 +65,8 @@ def test_encode_matches_oracle(name, T):
     idx, coef = dpb.encode(plan, x.to(DEV))
     torch.cuda.synchronize()
     oi, oc, om, oo = oracle.encode(w.d, m, nb, K, dl, gens, x.double().numpy())
-    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32)
+    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32,
+                        ctx=EncodeCheck(w.d, m, gens, x.double().numpy()))
     say(f"  {st}")
     assert st["exempt_tokens"] <= max(2, 0.02 * T)
 
@@ -81,7 +83,8 @@ def test_encode_full_size_sampled(name):
     rows = np.unique(np.concatenate([np.arange(16), rng.choice(w.tokens, 32, replace=False),
                                      np.arange(w.tokens - 16, w.tokens)]))
     oi, oc, om, oo = oracle.encode(w.d, m, nb, K, dl, gens, x[rows].double().numpy())
-    st = compare_encode(K, idx.cpu().numpy()[rows], coef.cpu().numpy()[rows], oi, oc, om, oo, TOL_F32)
+    st = compare_encode(K, idx.cpu().numpy()[rows], coef.cpu().numpy()[rows], oi, oc, om, oo, TOL_F32,
+                        ctx=EncodeCheck(w.d, m, gens, x[rows].double().numpy()))
     say(f"  {st}")
     assert st["exempt_tokens"] <= max(2, 0.02 * len(rows))
     # every emitted index is unique within its token and lies in its level
@@ -125,18 +128,82 @@ def test_encode_std_matches_oracle(name, T):
     plan = plan_for(name)
     w, nb, dl, K, m, gens = setup(name)
     N = 1 << nb[-1]
-    rng = np.random.default_rng(77 + w.index)
-    mu = (0.3 * rng.standard_normal(N)).astype(np.float32)
-    var = rng.uniform(0.3, 3.0, N).astype(np.float32)
-    r = (1.0 / np.sqrt(var.astype(np.float64) + 1e-6)).astype(np.float32)
+    mu, _, r = random_std_state(N, 77 + w.index)
     stats = torch.from_numpy(np.stack([mu, r], axis=1)).contiguous().to(DEV)
     x = inputs.activations(name, T)
     idx, coef = dpb.encode_std(plan, x.to(DEV), stats)
     torch.cuda.synchronize()
     oi, oc, om, oo = oracle.encode_std(w.d, m, nb, K, dl, gens, x.double().numpy(), mu, r)
-    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32)
+    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32,
+                        ctx=EncodeCheck(w.d, m, gens, x.double().numpy(), mu, r))
     say(f"  {st}")
     assert st["exempt_tokens"] <= max(2, 0.02 * T)
+
+
+@pytest.mark.parametrize("name,T,beta", [("pt_small_2l", 300, 0.1), ("pt_small_3l", 160, 0.05)])
+def test_std_update_matches_oracle(name, T, beta):
+    """The EMA update of the statistics at the paper's own shapes (K_{l-1}
+    Delta_l = 4096 and 8192 candidates per sampled token)."""
+    say(f"[t6 std update] {name} T={T} beta={beta}")
+    plan = plan_for(name)
+    w, nb, dl, K, m, gens = setup(name)
+    N = 1 << nb[-1]
+    mu, m2, r = random_std_state(N, 61 + w.index)
+    stats = torch.from_numpy(np.stack([mu, r], axis=1)).contiguous().to(DEV)
+    m2d = torch.from_numpy(m2).to(DEV)
+    x = inputs.activations(name, T)
+    idx, _ = dpb.encode_std(plan, x.to(DEV), stats)
+    before = stats.clone()
+    dpb.std_update(plan, x.to(DEV), idx, stats, m2d, beta, 1e-6)
+    torch.cuda.synchronize()
+    rmu, rm2 = oracle.std_update(w.d, m, nb, K, dl, gens, x.double().numpy(), idx.cpu().numpy(),
+                                 mu.astype(np.float64), m2.astype(np.float64), beta)
+    gs, gv = stats.cpu().numpy(), m2d.cpu().numpy()
+    touched = (rmu != mu.astype(np.float64)) | (rm2 != m2.astype(np.float64))
+    say(f"  touched {int(touched.sum())} of {N}")
+    assert touched[w.d:].sum() > 4 * K[0] * dl[1]   # level >= 1 features of the sampled tokens
+    assert np.array_equal(gs[~touched], before.cpu().numpy()[~touched])
+    assert np.array_equal(gv[~touched], m2[~touched])
+    assert np.allclose(gs[touched, 0], rmu[touched], rtol=1e-5, atol=1e-5)
+    assert np.allclose(gv[touched], rm2[touched], rtol=1e-5, atol=1e-5)
+    rr = oracle.std_r(gs[touched, 0].astype(np.float64), gv[touched].astype(np.float64), 1e-6)
+    assert np.allclose(gs[touched, 1], rr, rtol=2e-6, atol=0)
+
+
+@pytest.mark.parametrize("name,T", [("pt_small_2l", 128), ("pt_small_3l", 96)])
+def test_standardized_layer_step(name, T):
+    """One training step of the DPB layer on standardized scores at the
+    paper's own shapes: forward and input gradient against the oracle, and
+    the statistics update the backward applies."""
+    say(f"[t6 std layer] {name} T={T}")
+    plan = plan_for(name)
+    w, nb, dl, K, m, gens = setup(name)
+    N = 1 << nb[-1]
+    std = dpb_autograd.Standardizer(plan, momentum=0.1, eps=1e-6)
+    mu, m2, r = random_std_state(N, 71 + w.index)
+    std.stats.copy_(torch.from_numpy(np.stack([mu, r], axis=1)))
+    std.m2.copy_(torch.from_numpy(m2))
+    x = inputs.activations(name, T).to(DEV).requires_grad_(True)
+    gy = inputs.upstream_grad(name, T).to(DEV)
+    y, lv = dpb_autograd.dpb_layer(x, plan, True, 2, std)
+    stats0 = torch.from_numpy(np.stack([mu, r], axis=1)).contiguous().to(DEV)
+    idx, coef = dpb.encode_std(plan, x.detach(), stats0)
+    torch.autograd.backward([y, lv], [gy, torch.tensor(0.5, device=DEV)])
+    torch.cuda.synchronize()
+    ii, cc = idx.cpu().numpy(), coef.cpu().numpy().astype(np.float64)
+    oi, oc, om, oo = oracle.encode_std(w.d, m, nb, K, dl, gens, x.detach().double().cpu().numpy(), mu, r)
+    st = compare_encode(K, ii, cc, oi, oc, om, oo, TOL_F32,
+                        ctx=EncodeCheck(w.d, m, gens, x.detach().double().cpu().numpy(), mu, r))
+    say(f"  {st}")
+    xd = x.detach().double().cpu().numpy()
+    ry, _ = oracle.normalize(oracle.decode(w.d, m, ii, cc), xd)
+    compare_dense(y.detach().float().cpu().numpy(), ry, TOL_BF16)
+    rs = np.where(ii >= 0, r[np.maximum(ii, 0)], 0.0)
+    _, rgx = oracle.layer_backward(w.d, m, ii, cc, xd, gy.double().cpu().numpy(), 0.5, 2, True, r_slot=rs)
+    compare_dense(x.grad.float().cpu().numpy(), rgx, TOL_BF16)
+    rmu, rm2 = oracle.std_update(w.d, m, nb, K, dl, gens, xd, ii, mu.astype(np.float64), m2.astype(np.float64), 0.1)
+    assert np.allclose(std.stats.cpu().numpy()[:, 0], rmu, rtol=1e-5, atol=1e-5)
+    assert np.allclose(std.m2.cpu().numpy(), rm2, rtol=1e-5, atol=1e-5)
 
 
 def test_encode_zero_and_constant_rows():
@@ -154,7 +221,8 @@ def test_encode_zero_and_constant_rows():
     idx, coef = dpb.encode(plan, x.to(DEV))
     torch.cuda.synchronize()
     oi, oc, om, oo = oracle.encode(w.d, m, nb, K, dl, gens, x.double().numpy())
-    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32)
+    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32,
+                        ctx=EncodeCheck(w.d, m, gens, x.double().numpy()))
     say(f"  {st}")
     assert np.array_equal(idx.cpu().numpy()[0], oi[0])
     assert st["exempt_tokens"] <= 2
@@ -170,7 +238,8 @@ def test_encode_f32_input_matches_oracle(name, T):
     idx, coef = dpb.encode(plan, x.to(DEV))
     torch.cuda.synchronize()
     oi, oc, om, oo = oracle.encode(w.d, m, nb, K, dl, gens, x.double().numpy())
-    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32)
+    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32,
+                        ctx=EncodeCheck(w.d, m, gens, x.double().numpy()))
     say(f"  {st}")
     assert st["exempt_tokens"] <= max(2, 0.02 * T)
 
@@ -208,7 +277,8 @@ def test_encode_chunk_boundary_and_full_chunks():
     rows = np.array([0, 1, CHUNK - 2, CHUNK - 1, CHUNK, CHUNK + 1, 2 * CHUNK - 2, 2 * CHUNK - 1, 2 * CHUNK,
                      2 * CHUNK + 1, T - 2, T - 1])
     oi, oc, om, oo = oracle.encode(w.d, m, nb, K, dl, gens, x[rows].double().numpy())
-    st = compare_encode(K, idx.cpu().numpy()[rows], coef.cpu().numpy()[rows], oi, oc, om, oo, TOL_F32)
+    st = compare_encode(K, idx.cpu().numpy()[rows], coef.cpu().numpy()[rows], oi, oc, om, oo, TOL_F32,
+                        ctx=EncodeCheck(w.d, m, gens, x[rows].double().numpy()))
     say(f"  {st}")
     assert st["exempt_tokens"] <= 2
 
@@ -234,7 +304,8 @@ def test_custom_wide_hierarchies(hname, T):
     idx, coef = dpb.encode(plan, x.to(DEV))
     torch.cuda.synchronize()
     oi, oc, om, oo = oracle.encode(d, m, nb, K, dl, gens, x.double().numpy())
-    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32)
+    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32,
+                        ctx=EncodeCheck(d, m, gens, x.double().numpy()))
     say(f"  {st}")
     assert st["exempt_tokens"] <= max(2, 0.02 * T)
     g = inputs.normal((T, d), 800 + len(hname), "bf16")
@@ -248,21 +319,27 @@ def test_custom_wide_hierarchies(hname, T):
     compare_dense(y.cpu().numpy(), oracle.decode(d, m, oi, oc.astype(np.float32).astype(np.float64)), TOL_F32)
 
 
-def test_encode_without_workspace_uses_general_kernel():
-    """With a workspace that is too small the library runs the general
-    encoder instead of the wide one: the same codes (to the parity rules)."""
+def test_encode_rejects_missing_or_small_workspace():
+    """A plan that needs a workspace (many children per parent) and is given
+    none, or too little, is refused on the host before anything is enqueued."""
+    import ctypes
     name, T = "pt_small_3l", 24
     say(f"[t6 encode small workspace] {name} T={T}")
     plan = plan_for(name)
-    w, nb, dl, K, m, gens = setup(name)
-    x = inputs.activations(name, T)
+    x = inputs.activations(name, T).to(DEV)
+    assert dpb.load().dpb_encode_workspace_bytes(plan._handle, T) > 0
+    idx = torch.full((T, plan.k_tot), 7, dtype=torch.int32, device=DEV)
+    coef = torch.zeros((T, plan.k_tot), dtype=torch.float32, device=DEV)
     tiny = torch.empty(4, dtype=torch.float32, device=DEV)
-    idx, coef = dpb.encode(plan, x.to(DEV), workspace=tiny)
+    with pytest.raises(dpb.DPBError) as e:
+        dpb.encode(plan, x, idx, coef, workspace=tiny)
+    assert e.value.status == -1
+    P = ctypes.c_void_p
+    st = dpb.load().dpb_encode(plan._handle, P(x.data_ptr()), 1, T, P(idx.data_ptr()), P(coef.data_ptr()), None, 0,
+                               None)
+    assert st == -1
     torch.cuda.synchronize()
-    oi, oc, om, oo = oracle.encode(w.d, m, nb, K, dl, gens, x.double().numpy())
-    st = compare_encode(K, idx.cpu().numpy(), coef.cpu().numpy(), oi, oc, om, oo, TOL_F32)
-    say(f"  {st}")
-    assert st["exempt_tokens"] <= 2
+    assert (idx == 7).all().item()
 
 
 def test_empty_batches():

@@ -122,12 +122,12 @@ def _brute_update(d, Phi, nbits, K, gens, x, idx, mu, var, beta, sample):
             cands = sorted({p ^ int(gg) for p in parents for gg in gens[l]})
             for c in cands:
                 samples.setdefault(c, []).append(float(Phi[c] @ x[t]))
-    mu, var = mu.copy(), var.copy()
+    mu, m2 = mu.copy(), var.copy()
     for c, v in samples.items():
         v = np.array(v)
         mu[c] = (1 - beta) * mu[c] + beta * v.mean()
-        var[c] = (1 - beta) * var[c] + beta * v.var()
-    return mu, var
+        m2[c] = (1 - beta) * m2[c] + beta * np.mean(v * v)
+    return mu, m2
 
 
 @pytest.mark.parametrize("T,sample,beta", [(10, 4, 0.3), (7, 64, 0.05), (12, 5, 1.0)])
@@ -159,15 +159,58 @@ def test_std_update_closed_forms():
     mu0, var0 = np.zeros(N), np.ones(N)
     mu, var = oracle.std_update(w.d, m, nb, K, dl, g, x, idx, mu0, var0, 0.0)
     assert np.array_equal(mu, mu0) and np.array_equal(var, var0)
-    mu, var = oracle.std_update(w.d, m, nb, K, dl, g, x, idx, mu0, var0, 1.0)
+    mu, m2 = oracle.std_update(w.d, m, nb, K, dl, g, x, idx, mu0, var0, 1.0)
     assert np.allclose(mu[: w.d], x.mean(axis=0), rtol=1e-13, atol=1e-15)
-    assert np.allclose(var[: w.d], x.var(axis=0), rtol=1e-13, atol=1e-15)
+    assert np.allclose(m2[: w.d], (x * x).mean(axis=0), rtol=1e-13, atol=1e-15)
+    # with beta = 1 the implied variance is the batch's population variance
+    r = oracle.std_r(mu, m2, 0.0)
+    assert np.allclose(r[: w.d], 1.0 / x.std(axis=0), rtol=1e-10)
     # repeated updates on one batch approach its moments geometrically from (0, 1)
     beta, n = 0.2, 5
-    mu_n, var_n = mu0, var0
+    mu_n, m2_n = mu0, var0
     for _ in range(n):
-        mu_n, var_n = oracle.std_update(w.d, m, nb, K, dl, g, x, idx, mu_n, var_n, beta)
-    touched = var != var0
+        mu_n, m2_n = oracle.std_update(w.d, m, nb, K, dl, g, x, idx, mu_n, m2_n, beta)
+    touched = m2 != var0
     f = 1 - (1 - beta) ** n
     assert np.allclose(mu_n[touched], f * mu[touched], rtol=1e-12, atol=1e-14)
-    assert np.allclose(var_n[touched], (1 - f) + f * var[touched], rtol=1e-12, atol=1e-14)
+    assert np.allclose(m2_n[touched], (1 - f) + f * m2[touched], rtol=1e-12, atol=1e-14)
+
+
+def test_std_r_closed_forms():
+    mu = np.array([0.0, 2.0, -3.0, 1.0, 0.5])
+    m2 = np.array([4.0, 5.0, 9.0, 0.5, 0.25])
+    r = oracle.std_r(mu, m2, 0.0)
+    # sigma^2 = m2 - mu^2: 4, 1, 0 (clamped), -0.5 -> 0 (clamped), 0
+    with np.errstate(divide="ignore"):
+        assert np.allclose(r, 1.0 / np.sqrt([4.0, 1.0, 0.0, 0.0, 0.0]))
+    assert np.allclose(oracle.std_r(mu, m2, 1e-2)[[1, 2]], [1 / np.sqrt(1.01), 10.0])
+
+
+def test_std_statistics_of_unit_gaussian_scores_stay_near_one():
+    """For x ~ N(0, I) every direction has unit norm, so a feature's raw score
+    is N(0, 1) whatever else is selected (up to the small coherence with its
+    parent).  Over many batches the statistics of the level >= 1 features,
+    most of which are sampled once per batch or not at all, must estimate
+    sigma ~ 1, not shrink toward 0 (which a per-batch variance of single
+    samples would do)."""
+    w = inputs.workload("tiny")
+    nb, dl, K = oracle.hierarchy(w.d, w.n, w.levels, w.branching, w.beam, w.k)
+    m, g = oracle.masks(w.d, w.n), oracle.generators(nb, dl, 0)
+    N = 1 << w.n
+    mu, m2 = np.zeros(N), np.ones(N)
+    updates = np.zeros(N, dtype=np.int64)
+    rng = np.random.default_rng(123)
+    beta = 0.05
+    for _ in range(300):
+        x = rng.standard_normal((64, w.d))
+        r32 = oracle.std_r(mu, m2, 1e-6).astype(np.float32)
+        idx, _, _, _ = oracle.encode_std(w.d, m, nb, K, dl, g, x, mu.astype(np.float32), r32)
+        mu1, m21 = oracle.std_update(w.d, m, nb, K, dl, g, x, idx, mu, m2, beta)
+        updates += (mu1 != mu) | (m21 != m2)
+        mu, m2 = mu1, m21
+    r = oracle.std_r(mu, m2, 1e-6)
+    hashed = np.arange(N) >= w.d
+    often = hashed & (updates >= 100)
+    assert often.sum() > 50
+    assert 0.85 < np.median(r[often]) < 1.15
+    assert r[often].min() > 0.5 and r[often].max() < 2.0
