@@ -186,6 +186,25 @@ dpb_status dpb_decode_bwd_ex(const dpb_plan* plan, const int32_t* idx, const voi
                              const void* add_grad_x, const float* stats, float* grad_coef,
                              void* grad_x, dpb_dtype gx_dtype, void* stream);
 
+/* ENCODE WITHOUT ALLOCATION, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the results of dpb_encode (stats NULL) or of dpb_encode_std
+ * (stats given), bit for bit, without a caller workspace.  Plans that need
+ * one (dpb_encode_workspace_bytes > 0) take it from a scratch array the
+ * library holds on each device it runs on, DPB_NOALLOC_SCRATCH_BYTES bytes,
+ * kept until the process ends, and go through the tokens in passes sized to
+ * it, so any T is accepted; a plan for which a pass of 256 tokens would not
+ * fit gets DPB_EUNSUPPORTED (none of the plans the library accepts).  The
+ * array's device address is looked up when a plan is created on the device.
+ * Every call on one GPU uses that GPU's array: calls that may overlap in
+ * time on one GPU (other streams or threads) race and must be serialized by
+ * the caller.  Nothing in the array needs to start cleared.  Allocates and
+ * frees nothing.  Other arguments as dpb_encode / dpb_encode_std. */
+#define DPB_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+dpb_status dpb_encode_noalloc(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T,
+                              const float* stats, int32_t* idx, float* coef, void* stream);
+
 /* SCORE STANDARDIZATION (§2.2 "Score Standardization").  The state is two
  * caller-owned device arrays over all N = 2^n_last features:
  *   stats : fp32 [N][2] = (mu, r): the moving average of the feature's raw

@@ -53,6 +53,7 @@ def load():
         "dpb_decode_bwd": (i32, [P, P, P, i32, i64, P, P, i32, P]),
         "dpb_decode_bwd_ex": (i32, [P, P, P, i32, i64, P, P, P, P, P, i32, P]),
         "dpb_encode_std": (i32, [P, P, i32, i64, P, P, P, P, ctypes.c_size_t, P]),
+        "dpb_encode_noalloc": (i32, [P, P, i32, i64, P, P, P, P]),
         "dpb_encode_workspace_bytes": (ctypes.c_size_t, [P, i64]),
         "dpb_std_init": (i32, [P, P, P, P]),
         "dpb_std_workspace_bytes": (ctypes.c_size_t, [P]),
@@ -209,6 +210,18 @@ def encode(plan: Plan, x: torch.Tensor, idx: torch.Tensor | None = None, coef: t
         _check("dpb_encode_std", load().dpb_encode_std(plan._handle, _dev(x, "x"), _dtype_code(x), T,
                                                        _dev(stats, "stats"), _dev(idx, "idx"), _dev(coef, "coef"),
                                                        _opt(workspace, "workspace"), nbytes, _stream(x)))
+    return idx, coef
+
+
+def encode_noalloc(plan: Plan, x: torch.Tensor, idx: torch.Tensor, coef: torch.Tensor,
+                   stats: torch.Tensor | None = None):
+    """encode (stats None) or encode_std into the given idx, coef [T, k_tot]
+    through the library's allocation-free entry point (no workspace)."""
+    T = x.shape[0]
+    assert x.dim() == 2 and x.shape[1] == plan.d and idx.shape == coef.shape == (T, plan.k_tot)
+    _check("dpb_encode_noalloc", load().dpb_encode_noalloc(plan._handle, _dev(x, "x"), _dtype_code(x), T,
+                                                           _opt(stats, "stats"), _dev(idx, "idx"),
+                                                           _dev(coef, "coef"), _stream(x)))
     return idx, coef
 
 

@@ -12,6 +12,7 @@
 using dpb::DevPlan;
 
 static_assert(dpb::kStdSample == DPB_STD_SAMPLE, "standardization sample size");
+static_assert(dpb::kStaticScratchBytes == DPB_NOALLOC_SCRATCH_BYTES, "allocation-free encoder scratch size");
 using dpb::Hierarchy;
 
 namespace {
@@ -387,6 +388,8 @@ dpb_status create(dpb_plan** out, const Hierarchy& h, const uint32_t* gens, uint
     dpb_status s = fill_plan(plan, h, gens, seed);
     if (s == DPB_OK && (!any_encoder(plan->dev) || !dpb::code_kernels_fit(plan->dev))) s = DPB_EUNSUPPORTED;
     if (s == DPB_OK) s = upload(plan);
+    // set-up of the allocation-free encoder on this device (its scratch address)
+    if (s == DPB_OK) (void)dpb::scratch_setup(plan->device);
     if (s != DPB_OK) {
         dpb_plan_destroy(plan);
         return s;
@@ -420,9 +423,13 @@ dpb_status launched(hipError_t e)
     return DPB_OK;
 }
 
-// dpb_encode and dpb_encode_std: argument checks, then the plan's encoder.
+// dpb_encode, dpb_encode_std and dpb_encode_noalloc: argument checks, then
+// the plan's encoder.  With `own_scratch` the wide encoder's workspace is the
+// library's per-device scratch array (passes sized to it) instead of the
+// caller's buffer, and nothing is allocated.
 dpb_status encode_any(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T, const float* stats,
-                      int32_t* idx, float* coef, void* workspace, size_t ws_bytes, void* stream)
+                      int32_t* idx, float* coef, void* workspace, size_t ws_bytes, void* stream,
+                      bool own_scratch = false)
 {
     dpb_status s = check_call(plan, T);
     if (s) return s;
@@ -431,6 +438,14 @@ dpb_status encode_any(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, in
     const bool bf = x_dtype == DPB_BF16;
     const Enc e = pick_encoder(P, bf, stats != nullptr);
     if (e == Enc::None) return DPB_EUNSUPPORTED;
+    int64_t chunk = 0;
+    if (own_scratch && e == Enc::Wide) {
+        chunk = dpb::static_chunk_tokens(P);
+        if (chunk == 0) return DPB_EUNSUPPORTED;
+        workspace = dpb::scratch_setup(plan->device);
+        if (!workspace) return DPB_EHIP;
+        ws_bytes = dpb::kStaticScratchBytes;
+    }
     if (T == 0) return DPB_OK;
     if (!x || !idx || !coef || !aligned16(x) || !aligned16(idx) || !aligned16(coef) || !aligned16(stats) ||
         !aligned16(workspace))
@@ -439,8 +454,8 @@ dpb_status encode_any(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, in
     switch (e) {
     case Enc::Narrow: return launched(dpb::launch_encode2(P, x, bf, T, stats, idx, coef, st));
     case Enc::Wide:
-        if (!workspace || ws_bytes < dpb::encode_wide_workspace_bytes(P, T)) return DPB_EINVAL;
-        return launched(dpb::launch_encode_wide(P, x, bf, T, stats, idx, coef, workspace, st));
+        if (!own_scratch && (!workspace || ws_bytes < dpb::encode_wide_workspace_bytes(P, T))) return DPB_EINVAL;
+        return launched(dpb::launch_encode_wide(P, x, bf, T, stats, idx, coef, workspace, st, chunk));
     case Enc::General: return launched(dpb::launch_encode(P, x, bf, T, idx, coef, st));
     default: return DPB_EUNSUPPORTED;
     }
@@ -642,6 +657,12 @@ dpb_status dpb_encode_std(const dpb_plan* plan, const void* x, dpb_dtype x_dtype
 {
     if (plan && T > 0 && !stats) return DPB_EINVAL;
     return encode_any(plan, x, x_dtype, T, stats, idx, coef, workspace, ws_bytes, stream);
+}
+
+dpb_status dpb_encode_noalloc(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T,
+                              const float* stats, int32_t* idx, float* coef, void* stream)
+{
+    return encode_any(plan, x, x_dtype, T, stats, idx, coef, nullptr, 0, stream, true);
 }
 
 dpb_status dpb_std_init(const dpb_plan* plan, float* stats, float* m2, void* stream)

@@ -192,8 +192,17 @@ bool encode2_std_supported(const DevPlan& P);
 // Wide encoder (many children per parent): GEMM + selection per level.
 bool encode_wide_supported(const DevPlan& P, bool x_bf16);
 size_t encode_wide_workspace_bytes(const DevPlan& P, int64_t T);
+// chunk: tokens per pass (0: the default, 16384), which sizes the workspace.
 hipError_t launch_encode_wide(const DevPlan& P, const void* x, bool x_bf16, int64_t T, const float* stats,
-                              int32_t* idx, float* coef, void* ws, hipStream_t stream);
+                              int32_t* idx, float* coef, void* ws, hipStream_t stream, int64_t chunk = 0);
+// The allocation-free encoder's scratch (a device array of this size on each
+// device): its address on `device`, which must be current (looked up once per
+// device; nullptr on failure), and the tokens per pass it holds for a plan
+// (0 if not even kStaticMinChunk tokens fit).
+constexpr size_t kStaticScratchBytes = (size_t)64 << 20;
+constexpr int64_t kStaticMinChunk = 256;
+void* scratch_setup(int device);
+int64_t static_chunk_tokens(const DevPlan& P);
 hipError_t launch_encode2(const DevPlan& P, const void* x, bool x_bf16, int64_t T, const float* stats, int32_t* idx,
                           float* coef, hipStream_t stream);
 

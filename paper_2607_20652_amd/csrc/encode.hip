@@ -23,6 +23,7 @@
 //    adjacent duplicates and is kept once; the first K_l survivors are emitted
 //    in order.
 #include <algorithm>
+#include <mutex>
 
 #include "scoring.hpp"
 
@@ -1306,10 +1307,14 @@ static size_t wide_scores_bytes(const DevPlan& P, int64_t ch)
     return ((size_t)ch * wide_max_cands(P) * 4 + 255) & ~(size_t)255;
 }
 
+static size_t wide_chunk_bytes(const DevPlan& P, int64_t ch)
+{
+    return ch > 0 ? wide_scores_bytes(P, ch) + (((size_t)ch * 4 + 255) & ~(size_t)255) : 0;
+}
+
 size_t encode_wide_workspace_bytes(const DevPlan& P, int64_t T)
 {
-    const int64_t ch = std::min<int64_t>(T, kWideChunkTokens);
-    return ch > 0 ? wide_scores_bytes(P, ch) + (((size_t)ch * 4 + 255) & ~(size_t)255) : 0;
+    return wide_chunk_bytes(P, std::min<int64_t>(T, kWideChunkTokens));
 }
 
 // counts != nullptr: the fused epilogue (lists instead of scores).
@@ -1344,7 +1349,7 @@ static void launch_wide_select(const DevPlan& P, int l, int64_t c0, int64_t nc, 
 }
 
 hipError_t launch_encode_wide(const DevPlan& P, const void* x, bool x_bf16, int64_t T, const float* stats,
-                              int32_t* idx, float* coef, void* ws, hipStream_t stream)
+                              int32_t* idx, float* coef, void* ws, hipStream_t stream, int64_t chunk)
 {
     const float2* st = (const float2*)stats;
     {
@@ -1367,9 +1372,10 @@ hipError_t launch_encode_wide(const DevPlan& P, const void* x, bool x_bf16, int6
 #undef DPB_W0
     }
     float* scores = (float*)ws;
-    int* counts = (int*)((char*)ws + wide_scores_bytes(P, std::min<int64_t>(T, kWideChunkTokens)));
-    for (int64_t c0 = 0; c0 < T; c0 += kWideChunkTokens) {
-        const int64_t nc = std::min<int64_t>(kWideChunkTokens, T - c0);
+    if (chunk <= 0) chunk = kWideChunkTokens;
+    int* counts = (int*)((char*)ws + wide_scores_bytes(P, std::min<int64_t>(T, chunk)));
+    for (int64_t c0 = 0; c0 < T; c0 += chunk) {
+        const int64_t nc = std::min<int64_t>(chunk, T - c0);
         for (int l = 1; l < P.levels; ++l) {
             // standardized scores keep the two-pass selection (z needs each candidate's statistics)
             const bool fuse = !st && wide_fused(P, l);
@@ -1382,6 +1388,40 @@ hipError_t launch_encode_wide(const DevPlan& P, const void* x, bool x_bf16, int6
         }
     }
     return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Encoder workspace without allocation: the wide encoder's scratch taken from
+// a file-scope device array instead of a caller's buffer.  Each device holds
+// its own copy; its address is looked up once per device with that device
+// current (scratch_setup) and passed to the kernels like a workspace.  Tokens
+// go through in passes sized to the array.
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxScratchDevices] = {};
+}  // namespace
+
+void* scratch_setup(int device)
+{
+    if (device < 0 || device >= kMaxScratchDevices) return nullptr;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch[device]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) == hipSuccess) g_scratch[device] = ptr;
+        else (void)hipGetLastError();
+    }
+    return g_scratch[device];
+}
+
+int64_t static_chunk_tokens(const DevPlan& P)
+{
+    // the largest pass (a multiple of 256 tokens, at most the usual chunk) whose workspace fits
+    int64_t ch = kWideChunkTokens;
+    while (ch >= kStaticMinChunk && wide_chunk_bytes(P, ch) > kStaticScratchBytes) ch -= 256;
+    return ch >= kStaticMinChunk ? ch : 0;
 }
 
 }  // namespace dpb
