@@ -578,8 +578,9 @@ __global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const v
 //    the narrow encoder.  Its epilogue computes each token's threshold (the
 //    K_l-th largest distinct magnitude among the lanes' maxima; distinct
 //    magnitudes are distinct children) and writes only the (candidate, z)
-//    entries at or above it to the workspace; tokens with too many entries,
-//    shapes it does not cover and standardized scores get the full scores.
+//    entries at or above it to the workspace (with standardization it first
+//    takes z = (s - mu) r with each candidate's gathered statistics); tokens
+//    with too many entries and shapes it does not cover get the full scores.
 //  * wide_select_kernel: one wave per token; AbsTopK with deduplication (a
 //    child reached from several parents has bit-identical keys): the listed
 //    entries, or the candidates above the same threshold found from the full
@@ -684,14 +685,19 @@ __host__ __device__ inline bool wide_fused(const DevPlan& P, int l)
 // z) entries at or above a threshold tau computed here from the lanes'
 // largest magnitude keys (the selection's first pass), and counts[t - t0]
 // their number; a token with more than kWideList entries gets its full scores
-// and its count says so.
-template <bool X_BF16, int MT, bool FUSE>
+// and its count says so.  STD (with FUSE): every score is standardized here,
+// z = (s - mu) r with the candidate's statistics (§2.2 "Score
+// Standardization"), so that the threshold, the lists and any full scores
+// hold z.
+template <bool X_BF16, int MT, bool FUSE, bool STD>
 __global__ __launch_bounds__(kWideThreads) __attribute__((amdgpu_waves_per_eu(2))) void wide_gemm_kernel(DevPlan P, int l, const void* __restrict__ xin,
                                                                  int64_t t0, int64_t ntok,
                                                                  const int32_t* __restrict__ idx,
+                                                                 const float2* __restrict__ stats,
                                                                  float* __restrict__ scores,
                                                                  int* __restrict__ counts)
 {
+    static_assert(FUSE || !STD, "standardized scores only with the fused epilogue");
     extern __shared__ __align__(16) unsigned char smem[];
     const int KP = P.active[l - 1], KC = P.cpt[l], D = P.delta[l], nchunk = P.nchunk, d = P.d, dp = P.dp;
     const int csh = P.cpt_shift[l];   // KC = 2^csh
@@ -844,8 +850,10 @@ __global__ __launch_bounds__(kWideThreads) __attribute__((amdgpu_waves_per_eu(2)
         if (c + 2 < nchunk) fetch(c + 2, w0);
         if (c + 1 < nchunk) compute(c + 1, w1);
     }
-    // scores (times 1/sqrt d) of the live (token, parent) columns and generator rows
+    // scores (times 1/sqrt d) of the live (token, parent) columns and generator
+    // rows; the fused epilogue takes them (standardized with STD) in place first
     const bool all_rows = 32 * MT == D;   // else rows from D on are padding
+    const float osc = FUSE ? 1.f : P.rsd;
     auto store_scores = [&](int n) {
         const int col = wc * 64 + n * 16 + c16, tt = col >> csh, q = col & (KC - 1);
         if (tt >= nt_tok || q >= KP) return;
@@ -854,7 +862,7 @@ __global__ __launch_bounds__(kWideThreads) __attribute__((amdgpu_waves_per_eu(2)
         for (int mt = 0; mt < MT; ++mt) {
             if (all_rows || wr * 16 * MT + 16 * mt + 4 * kq < D) {
                 const f32x4 v = acc[mt][n];
-                *(float4*)(dst + 16 * mt) = make_float4(v[0] * P.rsd, v[1] * P.rsd, v[2] * P.rsd, v[3] * P.rsd);
+                *(float4*)(dst + 16 * mt) = make_float4(v[0] * osc, v[1] * osc, v[2] * osc, v[3] * osc);
             }
         }
     };
@@ -868,13 +876,48 @@ __global__ __launch_bounds__(kWideThreads) __attribute__((amdgpu_waves_per_eu(2)
 #pragma unroll
         for (int n = 0; n < 4; ++n) pid[n] = s_pidx[bcol[n]];
         __syncthreads();   // the staging LDS is free from here on
+        // s = acc / sqrt d in place; with standardization z = (s - mu) r, the
+        // statistics of child p XOR g_row gathered at an index that is always a
+        // feature (generator of a clamped row, parent 0 for padding columns)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int n = 0; n < 4; ++n)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[mt][n][i] *= P.rsd;
+        if constexpr (STD) {
+            const uint32_t* gl = P.gens + P.gens_off[l];
+            uint32_t gv[MT][4];
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) gv[mt][i] = gl[min(wr * 16 * MT + 16 * mt + 4 * kq + i, D - 1)];
+            constexpr int MH = MT > 1 ? MT / 2 : 1;   // row tiles per batch of gathers
+#pragma unroll
+            for (int n = 0; n < 4; ++n) {
+                const uint32_t pu = pid[n] >= 0 ? (uint32_t)pid[n] : 0u;
+#pragma unroll
+                for (int m0 = 0; m0 < MT; m0 += MH) {
+                    float2 st[MH][4];
+#pragma unroll
+                    for (int mt = 0; mt < MH; ++mt)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) st[mt][i] = stats[pu ^ gv[m0 + mt][i]];
+#pragma unroll
+                    for (int mt = 0; mt < MH; ++mt)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+                            acc[m0 + mt][n][i] = (acc[m0 + mt][n][i] - st[mt][i].x) * st[mt][i].y;
+                }
+            }
+        }
         uint32_t* s_top = (uint32_t*)smem;             // [TT][2 row halves][64 lanes]
         uint32_t* s_tau = s_top + TT * 128;           // [TT]
         int* s_cnt = (int*)(s_tau + TT);              // [TT]
         // magnitude key of value i of tile (mt, n): |z| bits + 1, 0 for padding
         auto mk = [&](int mt, int n, int i) -> uint32_t {
             const bool ok = (pid[n] >= 0) & (all_rows | (wr * 16 * MT + 16 * mt + 4 * kq + i < D));
-            const uint32_t m = (__float_as_uint(acc[mt][n][i] * P.rsd) & 0x7FFFFFFFu) + 1u;
+            const uint32_t m = (__float_as_uint(acc[mt][n][i]) & 0x7FFFFFFFu) + 1u;
             return ok ? m : 0u;
         };
         // each lane's largest key per token of this wave
@@ -947,7 +990,7 @@ __global__ __launch_bounds__(kWideThreads) __attribute__((amdgpu_waves_per_eu(2)
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
                 const f32x4 v = acc[mt][n];
-                *(float4*)(zrow + 4 * mt) = make_float4(v[0] * P.rsd, v[1] * P.rsd, v[2] * P.rsd, v[3] * P.rsd);
+                *(float4*)(zrow + 4 * mt) = make_float4(v[0], v[1], v[2], v[3]);
             }
             const uint32_t f0 = (uint32_t)(q * D + wr * 16 * MT + 4 * kq);
             while (hm) {
@@ -1317,10 +1360,11 @@ size_t encode_wide_workspace_bytes(const DevPlan& P, int64_t T)
     return wide_chunk_bytes(P, std::min<int64_t>(T, kWideChunkTokens));
 }
 
-// counts != nullptr: the fused epilogue (lists instead of scores).
-template <bool XB, bool FUSE>
+// counts != nullptr: the fused epilogue (lists instead of scores); STD: it
+// standardizes the scores with `st`.
+template <bool XB, bool FUSE, bool STD>
 static void launch_wide_gemm(const DevPlan& P, int l, const void* x, int64_t c0, int64_t nc, const int32_t* idx,
-                             float* scores, int* counts, hipStream_t stream)
+                             const float2* st, float* scores, int* counts, hipStream_t stream)
 {
     const int TT = kWideCols / P.cpt[l];
     const dim3 grid((unsigned)((nc + TT - 1) / TT));
@@ -1328,9 +1372,9 @@ static void launch_wide_gemm(const DevPlan& P, int l, const void* x, int64_t c0,
     const int MT = std::max(32, P.delta[l]) / 32;
 #define DPB_WG(M)                                                                                             \
     do {                                                                                                      \
-        allow_lds(wide_gemm_kernel<XB, M, FUSE>, lds);                                                        \
-        hipLaunchKernelGGL((wide_gemm_kernel<XB, M, FUSE>), grid, dim3(kWideThreads), lds, stream, P, l, x, c0, nc, \
-                           idx, scores, counts);                                                              \
+        allow_lds(wide_gemm_kernel<XB, M, FUSE, STD>, lds);                                                   \
+        hipLaunchKernelGGL((wide_gemm_kernel<XB, M, FUSE, STD>), grid, dim3(kWideThreads), lds, stream, P, l, x, c0, \
+                           nc, idx, st, scores, counts);                                                      \
     } while (0)
     if (MT == 1) DPB_WG(1);
     else if (MT == 2) DPB_WG(2);
@@ -1377,14 +1421,21 @@ hipError_t launch_encode_wide(const DevPlan& P, const void* x, bool x_bf16, int6
     for (int64_t c0 = 0; c0 < T; c0 += chunk) {
         const int64_t nc = std::min<int64_t>(chunk, T - c0);
         for (int l = 1; l < P.levels; ++l) {
-            // standardized scores keep the two-pass selection (z needs each candidate's statistics)
-            const bool fuse = !st && wide_fused(P, l);
-            if (x_bf16 && fuse) launch_wide_gemm<true, true>(P, l, x, c0, nc, idx, scores, counts, stream);
-            else if (x_bf16) launch_wide_gemm<true, false>(P, l, x, c0, nc, idx, scores, nullptr, stream);
-            else if (fuse) launch_wide_gemm<false, true>(P, l, x, c0, nc, idx, scores, counts, stream);
-            else launch_wide_gemm<false, false>(P, l, x, c0, nc, idx, scores, nullptr, stream);
-            if (st) launch_wide_select<true>(P, l, c0, nc, scores, nullptr, st, idx, coef, stream);
-            else launch_wide_select<false>(P, l, c0, nc, scores, fuse ? counts : nullptr, st, idx, coef, stream);
+            // the fused epilogue standardizes in place (its lists and scores hold z);
+            // otherwise the selection standardizes the full scores
+            const bool fuse = wide_fused(P, l);
+            if (fuse) {
+                if (x_bf16 && st) launch_wide_gemm<true, true, true>(P, l, x, c0, nc, idx, st, scores, counts, stream);
+                else if (x_bf16) launch_wide_gemm<true, true, false>(P, l, x, c0, nc, idx, st, scores, counts, stream);
+                else if (st) launch_wide_gemm<false, true, true>(P, l, x, c0, nc, idx, st, scores, counts, stream);
+                else launch_wide_gemm<false, true, false>(P, l, x, c0, nc, idx, st, scores, counts, stream);
+                launch_wide_select<false>(P, l, c0, nc, scores, counts, nullptr, idx, coef, stream);
+            } else {
+                if (x_bf16) launch_wide_gemm<true, false, false>(P, l, x, c0, nc, idx, st, scores, nullptr, stream);
+                else launch_wide_gemm<false, false, false>(P, l, x, c0, nc, idx, st, scores, nullptr, stream);
+                if (st) launch_wide_select<true>(P, l, c0, nc, scores, nullptr, st, idx, coef, stream);
+                else launch_wide_select<false>(P, l, c0, nc, scores, nullptr, st, idx, coef, stream);
+            }
         }
     }
     return hipGetLastError();

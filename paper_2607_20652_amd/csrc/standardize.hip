@@ -10,8 +10,9 @@
 //    a fixed token range, folded in a fixed order;
 //  * levels l >= 1: on kStdSample evenly spaced tokens, the children
 //    p XOR g_j of the active parents (the level l-1 entries of the token's
-//    code), each child once per token, scored from the definition
-//    <phi_c, x>; one record per (token, child).  Records of one feature are
+//    code), each child once per token, scored on the matrix cores
+//    (<phi_c, x> by the child-scoring contraction); one record per
+//    (token, child).  Records of one feature are
 //    combined with fp64 atomics in a per-feature accumulator that only the
 //    records themselves clear, and the record with the lowest position
 //    applies the update.
@@ -22,8 +23,7 @@
 //    r = 1 / sqrt(max(m2 - mu^2, 0) + eps).
 #include <algorithm>
 
-#include "dpb_internal.hpp"
-#include "device_common.hpp"
+#include "scoring.hpp"
 
 namespace dpb {
 namespace {
@@ -179,55 +179,129 @@ __global__ void std_col_update_kernel(int d, int64_t T, StdWs W, float2* stats, 
     ema(stats, m2, c, (double)T, s1, s2, beta, eps);
 }
 
-// kStdSlices workgroups per (sample token, level l >= 1): the token's
-// candidates at level l, each child once, scored <phi_c, x_t> from the
-// definition.  The candidate list and the row of x are staged in LDS in each
-// workgroup; a candidate is a duplicate when an earlier entry of the list
-// holds the same child; each wave scores one candidate at a time, lanes over
-// the coordinates, and the slices of a list take turns (more waves in flight
-// for the few sampled tokens).
+// One workgroup per (sampled token, level l >= 1, block of 16 parent slots
+// of level l - 1): the scores <phi_c, x_t> of the children c = p XOR g_j of
+// its parents, on the matrix cores (the encoder's child-scoring contraction
+// of §2.2: generator tiles of Gamma_l against the sign-flipped row of x), one
+// record per candidate.  A child reached from several parents is sampled once
+// per token: every workgroup of the (token, level) inserts all of the level's
+// candidates into an LDS hash set (linear probing, compare-and-swap; a
+// child's slot ends up holding its lowest candidate position, so every
+// workgroup of the token and level agrees on it), and a candidate is recorded
+// only when it is that copy.
 constexpr int kStdMaxCand = 8192;   // K_{l-1} Delta_l of the paper's 3-level hierarchy (32 x 256)
-constexpr int kStdSlices = 8;   // workgroups sharing one sampled token's candidates of a level
+
+__host__ __device__ inline int std_hash_bits(const DevPlan& P)
+{
+    int n = 1;
+    for (int l = 1; l < P.levels; ++l) n = std::max(n, P.active[l - 1] * P.delta[l]);
+    int b = 8;
+    while ((1 << b) < 2 * n) ++b;
+    return b;
+}
+
+__host__ __device__ inline unsigned std_sample_lds(const DevPlan& P, bool x_bf16)
+{
+    return align16u(4u << std_hash_bits(P)) + align16u(x_bf16 ? P.prow * 4 : P.dp * 4) + align16u(16 * P.cws * 4);
+}
+
+__host__ __device__ inline int std_parent_blocks(const DevPlan& P)
+{
+    int nb = 1;
+    for (int l = 1; l < P.levels; ++l) nb = std::max(nb, (P.active[l - 1] + 15) / 16);
+    return nb;
+}
+
+__device__ __forceinline__ uint32_t std_slot(uint32_t c, int hb) { return (c * 0x9E3779B1u) >> (32 - hb); }
 
 template <bool BF16>
 __global__ __launch_bounds__(kStdThreads) void std_sample_kernel(DevPlan P, const void* x, int64_t T, int m,
                                                                  const int32_t* idx, StdWs W)
 {
-    __shared__ int32_t cand[kStdMaxCand];
-    extern __shared__ __align__(16) float xrow[];
-    const int j = blockIdx.x, l = blockIdx.y + 1, z = blockIdx.z;
-    const int64_t t = ((int64_t)j * T) / m;
-    const int Kp = P.active[l - 1], Dl = P.delta[l], d = P.d, n = Kp * Dl;
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int js = blockIdx.x, l = blockIdx.y + 1, nb = blockIdx.z;
+    const int Kp = P.active[l - 1], Dl = P.delta[l], n = Kp * Dl, d = P.d;
+    if (16 * nb >= Kp) return;   // the level has fewer parent blocks (uniform per workgroup)
+    const int64_t t = ((int64_t)js * T) / m;
     const int32_t* par = idx + t * P.k_tot + P.slot_base[l - 1];
     const uint32_t* g = P.gens + P.gens_off[l];
     int cbase = 0;
     for (int ll = 1; ll < l; ++ll) cbase += P.active[ll - 1] * P.delta[ll];
-    StdRec* rec = W.rec + (int64_t)j * std_cands(P) + cbase;
-    for (int e = threadIdx.x; e < n; e += kStdThreads) {
-        const int q = e / Dl;
-        const int32_t p = par[q];
-        cand[e] = p >= 0 ? (int32_t)((uint32_t)p ^ g[e - q * Dl]) : -1;
-    }
-    for (int iota = threadIdx.x; iota < d; iota += kStdThreads) xrow[iota] = load_act<BF16>(x, t * d + iota);
-    __syncthreads();
-    // candidates e = z * waves + wave, step waves * slices: one wave each; a
-    // later copy of a child (found by a ballot over the earlier entries) is
-    // recorded as absent
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, nw = kStdThreads / 64;
-    for (int e = z * nw + wave; e < n; e += nw * kStdSlices) {
-        int32_t c = cand[e];
-        bool dup = false;
-        for (int e0 = 0; e0 < e && c >= 0; e0 += 64)
-            dup = dup || __ballot(e0 + lane < e && cand[min(e0 + lane, e)] == c) != 0ull;
-        if (dup) c = -1;
-        float s = 0.f;
-        if (c >= 0) {
-            float part = 0.f;
-            for (int iota = lane; iota < d; iota += 64)
-                part += signed_by_parity(xrow[iota], P.masks[iota] & (uint32_t)c);
-            s = wave_sum(part) * P.rsd;
+    StdRec* rec = W.rec + (int64_t)js * std_cands(P) + cbase;
+
+    const int hb = std_hash_bits(P);
+    const uint32_t hmask = (1u << hb) - 1u;
+    int32_t* tab = (int32_t*)smem;   // candidate position e of the copy holding the slot, or -1
+    unsigned char* rb = smem + align16u(4u << hb);
+    uint32_t* pairs = (uint32_t*)rb;
+    float* xf = (float*)rb;
+    uint32_t* cw = (uint32_t*)(rb + align16u(BF16 ? P.prow * 4 : P.dp * 4));
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+
+    for (int i = threadIdx.x; i < (1 << hb); i += kStdThreads) tab[i] = -1;
+    if (wave == 0) {
+        if constexpr (BF16) {
+            load_pairs(P, lane, 1, 1, (const uint16_t*)x, t, pairs);
+        } else {
+            const float* xs = (const float*)x;
+            for (int iota = lane; iota < P.dp; iota += 64) xf[iota] = iota < d ? xs[t * d + iota] : 0.f;
         }
-        if (lane == 0) rec[e] = StdRec{c, s};
+    }
+    {   // sign bitmaps of parents 16 nb .. 16 nb + 15: one nibble-table word per 4-bit group of the index
+        const int col = threadIdx.x & 15, q = 16 * nb + col;
+        const int32_t p = q < Kp ? par[q] : -1;
+        const uint32_t pu = p >= 0 ? (uint32_t)p : 0u;
+        for (int w = threadIdx.x >> 4; w < P.nchunk; w += kStdThreads / 16) {
+            uint32_t word = 0;
+            for (int gg = 0; gg < P.nt_groups; ++gg) word ^= P.nt[(gg * P.nchunk + w) * 16 + ((pu >> (4 * gg)) & 15u)];
+            cw[col * P.cws + w] = p >= 0 ? word : 0u;
+        }
+    }
+    __syncthreads();
+    auto child = [&](int e) -> uint32_t {
+        const int q = e / Dl;
+        return (uint32_t)par[q] ^ g[e - q * Dl];
+    };
+    // every candidate of the level into the set (padding parents have none)
+    for (int e = threadIdx.x; e < n; e += kStdThreads) {
+        if (par[e / Dl] < 0) continue;
+        const uint32_t c = child(e);
+        uint32_t h = std_slot(c, hb);
+        for (;;) {
+            const int prev = atomicCAS(&tab[h], -1, e);
+            if (prev == -1) break;   // inserted
+            if (child(prev) == c) {  // the slot holds a copy: it keeps the lowest position
+                atomicMin(&tab[h], e);
+                break;
+            }
+            h = (h + 1u) & hmask;
+        }
+    }
+    __syncthreads();
+
+    const ActTile A{pairs, xf};
+    const int col = lane & 15, kq = lane >> 4, q = 16 * nb + col;
+    const int32_t p = q < Kp ? par[q] : -1;
+    for (int mb = wave; mb < P.mblocks[l]; mb += kStdThreads / 64) {
+        const f32x4 acc = mfma_scores<BF16>(P, lane, l, mb, 0, A, cw);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int jj = 16 * mb + 4 * kq + i;
+            if (q >= Kp || jj >= Dl) continue;
+            const int e = q * Dl + jj;
+            StdRec r{-1, 0.f};
+            if (p >= 0) {
+                const uint32_t c = (uint32_t)p ^ g[jj];
+                uint32_t h = std_slot(c, hb);
+                int v = tab[h];
+                while (v != e && v >= 0 && child(v) != c) {   // the child is in the set: the walk ends at its slot
+                    h = (h + 1u) & hmask;
+                    v = tab[h];
+                }
+                if (v == e) r = StdRec{(int32_t)c, acc[i] * P.rsd};
+            }
+            rec[e] = r;
+        }
     }
 }
 
@@ -274,7 +348,7 @@ bool std_supported(const DevPlan& P)
 {
     for (int l = 1; l < P.levels; ++l)
         if (P.active[l - 1] * P.delta[l] > kStdMaxCand) return false;
-    return P.d <= 16384;
+    return P.d <= 16384 && std_sample_lds(P, false) <= (unsigned)kLdsBudget;
 }
 
 size_t std_workspace_bytes(const DevPlan& P)
@@ -304,12 +378,15 @@ hipError_t launch_std_update(const DevPlan& P, const void* x, bool x_bf16, int64
                        eps);
     const int m = (int)std::min<int64_t>(T, kStdSample);
     if (P.levels > 1 && m > 0) {
-        const dim3 g2(m, P.levels - 1, kStdSlices);
-        const size_t xl = (size_t)P.d * 4;
-        allow_lds(std_sample_kernel<true>, xl);
-        allow_lds(std_sample_kernel<false>, xl);
-        if (x_bf16) hipLaunchKernelGGL(std_sample_kernel<true>, g2, dim3(kStdThreads), xl, stream, P, x, T, m, idx, W);
-        else hipLaunchKernelGGL(std_sample_kernel<false>, g2, dim3(kStdThreads), xl, stream, P, x, T, m, idx, W);
+        const dim3 g2(m, P.levels - 1, std_parent_blocks(P));
+        const size_t xl = std_sample_lds(P, x_bf16);
+        if (x_bf16) {
+            allow_lds(std_sample_kernel<true>, xl);
+            hipLaunchKernelGGL(std_sample_kernel<true>, g2, dim3(kStdThreads), xl, stream, P, x, T, m, idx, W);
+        } else {
+            allow_lds(std_sample_kernel<false>, xl);
+            hipLaunchKernelGGL(std_sample_kernel<false>, g2, dim3(kStdThreads), xl, stream, P, x, T, m, idx, W);
+        }
         const int64_t nrec = (int64_t)m * std_cands(P);
         hipLaunchKernelGGL(std_rec_clear_kernel, std_grid(nrec, 256), dim3(256), 0, stream, nrec, W);
         hipLaunchKernelGGL(std_rec_accum_kernel, std_grid(nrec, 256), dim3(256), 0, stream, nrec, W);
