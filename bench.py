@@ -4,9 +4,11 @@
 
 A step is one pass of the whole path over one batch: encode x -> (idx, coef),
 decode -> y, and decode-backward of an upstream gradient g -> (grad_coef,
-grad_x).  Inputs are seeded synthetic activations resident in HBM before the
-timed region; three input sets rotate so that their total (>600 MB at the
-default workload) exceeds the 256 MB Infinity Cache.
+grad_x).  The three kernels are timed separately with HIP events between
+them (dpb_forward, the encode + decode call, enqueues the same two kernels).
+Inputs are seeded synthetic activations resident in HBM before the timed
+region; three input sets rotate so that their total (>600 MB at the default
+workload) exceeds the 256 MB Infinity Cache.
 
 Prints ONE JSON line.  `roofline` describes the kernel with the largest average
 launch time, timed with HIP events on the stream the kernels run on;
@@ -54,7 +56,7 @@ def kernel_source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-KERNEL_SYMBOLS = {"encode": "encode", "decode": "decode2_kernel", "decode_bwd": "decode_bwd2_kernel"}
+KERNEL_SYMBOLS = {"encode": "encode3_kernel", "decode": "decode2_kernel", "decode_bwd": "decode_bwd2_kernel"}
 
 
 def ingest_counters(fetch_csv: str, write_csv: str, workload: str) -> dict:
@@ -71,7 +73,7 @@ def ingest_counters(fetch_csv: str, write_csv: str, workload: str) -> dict:
             name = r["Kernel_Name"]
             key = "copy"  # runtime copies and fills
             for k, sym in KERNEL_SYMBOLS.items():
-                if sym in name and not (k == "encode" and "decode" in name):
+                if sym in name:
                     key = k
             acc.setdefault(key, []).append(float(r["Counter_Value"]) * 1024.0)
         if not acc.get("copy"):
@@ -98,6 +100,7 @@ def algorithmic_bytes_per_token(w, k_tot: int) -> dict:
     """HBM bytes each kernel must move per token (inputs read once, outputs written once)."""
     xb = 2 if w.dtype == "bf16" else 4
     return {
+        "forward": w.d * xb + k_tot * 8 + w.d * xb,        # read x, write (idx, coef), write y
         "encode": w.d * xb + k_tot * 8,                    # read x, write (idx, coef)
         "decode": k_tot * 8 + w.d * xb,                    # read (idx, coef), write y
         "decode_bwd": k_tot * 4 + w.d * xb + k_tot * 4 + w.d * xb,  # read idx, g; write grad_coef, grad_x
@@ -114,7 +117,8 @@ def algorithmic_flops_per_token(w, plan_k_tot: int, hier) -> dict:
     nbits, delta, active = hier
     hashed = plan_k_tot - active[0]
     score = sum(active[l - 1] * delta[l] for l in range(1, len(active))) * w.d
-    return {"encode": 2 * score, "decode": 2 * hashed * w.d, "decode_bwd": 4 * hashed * w.d}
+    return {"forward": 2 * score + 2 * hashed * w.d, "encode": 2 * score, "decode": 2 * hashed * w.d,
+            "decode_bwd": 4 * hashed * w.d}
 
 
 def load_traffic(kernel: str, tokens: int):
@@ -235,13 +239,59 @@ def cpu_baseline(name: str, target_s: float = 12.0) -> dict:
     t_probe = run(probe)
     T = int(min(w.tokens, max(probe, probe * target_s / max(t_probe, 1e-3))))
     t = run(T)
-    return {
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    out = {
         "value": T / t,
         "unit": "tokens/s",
         "cores": oracle.num_threads(),
         "kind": "oracle",
         "sample": f"first {T} of {w.tokens} tokens of '{name}' (encode+decode+decode_bwd), {t:.1f} s",
+        "cpu_model": model,
+        "logical_cpus": os.cpu_count(),
     }
+    # the same oracle on one thread, on the first 1,024 tokens: the OpenMP
+    # runtime the oracle runs on is set to one thread and back
+    import ctypes
+    try:
+        gomp = ctypes.CDLL("libgomp.so.1")
+        before = gomp.omp_get_max_threads()
+        gomp.omp_set_num_threads(1)
+        try:
+            used = oracle.num_threads()
+            t1 = cpu_oracle_seconds(name, 1024)
+        finally:
+            gomp.omp_set_num_threads(before)
+        out["single_thread"] = {"value": 1024 / t1, "unit": "tokens/s", "tokens": 1024, "seconds": round(t1, 2),
+                                "threads": used}
+    except OSError:
+        out["single_thread"] = None
+    return out
+
+
+def cpu_oracle_seconds(name: str, T: int) -> float:
+    """Seconds the oracle takes for encode + decode + decode_bwd of the first T
+    tokens of the workload (the threads OpenMP gives it)."""
+    import oracle
+
+    w = inputs.workload(name)
+    h = w.hierarchy()
+    nb, dl, K = h if h is not None else oracle.hierarchy(w.d, w.n, w.levels, w.branching, w.beam, w.k)
+    m = oracle.masks(w.d, w.n)
+    gens = oracle.generators(nb, dl, 0)
+    x = inputs.activations(name, T).double().numpy()
+    g = inputs.upstream_grad(name, T).double().numpy()
+    t = time.perf_counter()
+    idx, coef, _, _ = oracle.encode(w.d, m, nb, K, dl, gens, x)
+    oracle.decode(w.d, m, idx, coef)
+    oracle.decode_bwd(w.d, m, idx, g)
+    return time.perf_counter() - t
 
 
 def main() -> int:
@@ -304,20 +354,19 @@ def main() -> int:
 
     def step(i, ev=None):
         x, g = sets[i % 3]
+        for j, n in enumerate(names):
+            if ev is not None:
+                ev[j].record()
+            if not run[n]:
+                continue
+            if n == "encode":
+                dpb.encode(plan, x, idx, coef)
+            elif n == "decode":
+                dpb.decode(plan, idx, coef, act, y)
+            else:
+                dpb.decode_bwd(plan, idx, g, act, gc, gx)
         if ev is not None:
-            ev[0].record()
-        if run["encode"]:
-            dpb.encode(plan, x, idx, coef)
-        if ev is not None:
-            ev[1].record()
-        if run["decode"]:
-            dpb.decode(plan, idx, coef, act, y)
-        if ev is not None:
-            ev[2].record()
-        if run["decode_bwd"]:
-            dpb.decode_bwd(plan, idx, g, act, gc, gx)
-        if ev is not None:
-            ev[3].record()
+            ev[len(names)].record()
 
     if args.only in ("decode", "decode_bwd"):
         dpb.encode(plan, sets[0][0], idx, coef)  # codes for the kernels under test
@@ -332,7 +381,8 @@ def main() -> int:
         step(i)
     torch.cuda.synchronize()
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    nev = len(names) + 1
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
@@ -342,6 +392,7 @@ def main() -> int:
     torch.cuda.synchronize()
     ms_total = start.elapsed_time(end)
     ms_step = ms_total / args.steps
+    step_ms = [evs[i][0].elapsed_time(evs[i][nev - 1]) for i in range(args.steps)]
     launch_ms = {n: [evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(args.steps)] for j, n in enumerate(names)}
     per_kernel_ms = {n: float(np.mean(v)) for n, v in launch_ms.items()}
 
@@ -381,14 +432,18 @@ def main() -> int:
     out = {
         "metric": METRIC if args.workload == "train" else f"DPB fwd+bwd tokens/sec ({w.name})",
         "value": T / (ms_step * 1e-3),
-        # forward alone (encode + decode), from the per-launch means
+        "value_median": T / (float(np.median(step_ms)) * 1e-3),
+        # forward alone (encode + decode), from the per-launch means, and the
+        # forward's HBM ceiling (read x, write the code and y once)
         "fwd_tokens_per_s": (T / ((per_kernel_ms["encode"] + per_kernel_ms["decode"]) * 1e-3)
                              if run["encode"] and run["decode"] else None),
+        "fwd_hbm_ceiling_tokens_per_s": HBM_PEAK_GBS * 1e9 / bpt["forward"],
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_step,
+        "ms_per_step_median": float(np.median(step_ms)),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -400,6 +455,7 @@ def main() -> int:
                          if w.hierarchy() is None else
                          f"{w.name}: DPB d={w.d}, levels n={plan.level_bits}, K={plan.active}, "
                          f"{w.branching} children per parent, {T} tokens {w.dtype}; encode+decode+decode_bwd per step"),
+            "step_calls": "dpb_encode + dpb_decode + dpb_decode_bwd",
             "tokens_per_step": T, "d": w.d, "n_bits": w.n, "levels": w.levels, "branching": w.branching,
             "beam": w.beam, "k": w.k, "k_tot": k, "only": args.only,
         },

@@ -151,6 +151,19 @@ dpb_status dpb_encode(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, in
 dpb_status dpb_decode(const dpb_plan* plan, const int32_t* idx, const float* coef, int64_t T,
                       void* y, dpb_dtype y_dtype, void* stream);
 
+/* FORWARD: dpb_encode (stats NULL) or dpb_encode_std (stats given) followed
+ * by dpb_decode of the code just written (§2.2 beam search, then §2.1 Eq. 1),
+ * in one call; idx, coef and y are those calls' results bit for bit:
+ *   x, stats, idx, coef, workspace, ws_bytes : as in dpb_encode / dpb_encode_std
+ *                                              (the same workspace rule)
+ *   y         : device [T, d], fp32 or bf16 (y_dtype; written), 16-B aligned
+ * The encoder and the decode kernel are enqueued in turn on `stream`.  Errors
+ * as dpb_encode's, plus DPB_EINVAL for a NULL or misaligned y or an unknown
+ * y_dtype, found before anything is enqueued. */
+dpb_status dpb_forward(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T, const float* stats,
+                       int32_t* idx, float* coef, void* y, dpb_dtype y_dtype, void* workspace, size_t ws_bytes,
+                       void* stream);
+
 /* DECODE BACKWARD: for upstream gradient g of y,
  *   grad_coef[s] = <phi_{idx_s}, g>                (the VJP of decode in coef)
  *   grad_x       = sum_s grad_coef[s] * phi_{idx_s} (through coef = Phi_S x,

@@ -50,6 +50,7 @@ def load():
         "dpb_plan_tables": (i32, [P, P, P]),
         "dpb_encode": (i32, [P, P, i32, i64, P, P, P, ctypes.c_size_t, P]),
         "dpb_decode": (i32, [P, P, P, i64, P, i32, P]),
+        "dpb_forward": (i32, [P, P, i32, i64, P, P, P, P, i32, P, ctypes.c_size_t, P]),
         "dpb_decode_bwd": (i32, [P, P, P, i32, i64, P, P, i32, P]),
         "dpb_decode_bwd_ex": (i32, [P, P, P, i32, i64, P, P, P, P, P, i32, P]),
         "dpb_encode_std": (i32, [P, P, i32, i64, P, P, P, P, ctypes.c_size_t, P]),
@@ -225,6 +226,29 @@ def encode_noalloc(plan: Plan, x: torch.Tensor, idx: torch.Tensor, coef: torch.T
     return idx, coef
 
 
+def forward(plan: Plan, x: torch.Tensor, idx: torch.Tensor | None = None, coef: torch.Tensor | None = None,
+            y: torch.Tensor | None = None, stats: torch.Tensor | None = None, out_dtype: torch.dtype | None = None,
+            workspace: torch.Tensor | None = None):
+    """x [T, d] -> (idx, coef, y): encode (on standardized scores when stats is
+    given) and decode in one library call (dpb_forward); y [T, d] in out_dtype
+    (default: the type of x)."""
+    T = x.shape[0]
+    assert x.dim() == 2 and x.shape[1] == plan.d
+    if idx is None:
+        idx = torch.empty((T, plan.k_tot), dtype=torch.int32, device=x.device)
+    if coef is None:
+        coef = torch.empty((T, plan.k_tot), dtype=torch.float32, device=x.device)
+    if y is None:
+        y = torch.empty((T, plan.d), dtype=out_dtype or x.dtype, device=x.device)
+    if workspace is None:
+        workspace = encode_workspace(plan, T, x.device)
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check("dpb_forward", load().dpb_forward(plan._handle, _dev(x, "x"), _dtype_code(x), T, _opt(stats, "stats"),
+                                             _dev(idx, "idx"), _dev(coef, "coef"), _dev(y, "y"), _dtype_code(y),
+                                             _opt(workspace, "workspace"), nbytes, _stream(x)))
+    return idx, coef, y
+
+
 def decode(plan: Plan, idx: torch.Tensor, coef: torch.Tensor, out_dtype: torch.dtype = torch.float32,
            y: torch.Tensor | None = None):
     """(idx, coef) [T, k_tot] -> y [T, d] in out_dtype (fp32 or bf16)."""
@@ -251,12 +275,6 @@ def decode_bwd(plan: Plan, idx: torch.Tensor, grad_y: torch.Tensor, gx_dtype: to
                                                    _dtype_code(grad_y), T, _dev(grad_coef, "grad_coef"),
                                                    _dev(grad_x, "grad_x"), _dtype_code(grad_x), _stream(idx)))
     return grad_coef, grad_x
-
-
-def forward(plan: Plan, x: torch.Tensor, out_dtype: torch.dtype | None = None):
-    """encode then decode: x -> (idx, coef, y)."""
-    idx, coef = encode(plan, x)
-    return idx, coef, decode(plan, idx, coef, out_dtype or x.dtype)
 
 
 def _opt(t: torch.Tensor | None, name: str):

@@ -599,6 +599,23 @@ dpb_status dpb_encode(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, in
     return encode_any(plan, x, x_dtype, T, nullptr, idx, coef, workspace, ws_bytes, stream);
 }
 
+dpb_status dpb_forward(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T, const float* stats,
+                       int32_t* idx, float* coef, void* y, dpb_dtype y_dtype, void* workspace, size_t ws_bytes,
+                       void* stream)
+{
+    dpb_status s = check_call(plan, T);
+    if (s) return s;
+    if (!dtype_ok(x_dtype) || !dtype_ok(y_dtype)) return DPB_EINVAL;
+    const DevPlan& P = plan->dev;
+    if (T > 0 && (!x || !idx || !coef || !y || !aligned16(x) || !aligned16(idx) || !aligned16(coef) || !aligned16(y) ||
+                  !aligned16(stats)))
+        return DPB_EINVAL;
+    // the encoder, then the decode kernel on the code it wrote, on one stream
+    s = encode_any(plan, x, x_dtype, T, stats, idx, coef, workspace, ws_bytes, stream);
+    if (s || T == 0) return s;
+    return launched(dpb::launch_decode2(P, idx, coef, T, y, y_dtype == DPB_BF16, (hipStream_t)stream));
+}
+
 dpb_status dpb_decode(const dpb_plan* plan, const int32_t* idx, const float* coef, int64_t T, void* y,
                       dpb_dtype y_dtype, void* stream)
 {

@@ -461,9 +461,12 @@ __device__ void decode_tokens(const DevPlan& P, const Wave& W, const float* cf)
         // parents) all lanes write.
         const int CPT = P.cpt[L1];
         const bool all = TPW * CPT == 16 && W.ntok == TPW;
-        // (one compile-time layout only: more of them inlined here cost the
-        // kernels registers, and with them a wave per SIMD)
-        if (CPT == 8 && all) leaf_columns<8, EXACT3, PB16, LCB>(P, W, ahi, amid, alo);
+        // (one compile-time layout per kernel variant: more of them inlined here
+        // cost the kernels registers, and with them a wave per SIMD.  Eight
+        // parents per token take one byte of sign bits (PB16 false), sixteen
+        // take two: one token per wave, all sixteen columns its own)
+        if (!PB16 && CPT == 8 && all) leaf_columns<8, EXACT3, PB16, LCB>(P, W, ahi, amid, alo);
+        else if (PB16 && CPT == 16 && all) leaf_columns<16, EXACT3, PB16, LCB>(P, W, ahi, amid, alo);
         else leaf_columns_any<EXACT3, PB16>(P, W, ahi, amid, alo);
         wave_sync();
     }
