@@ -256,7 +256,7 @@ def cpu_baseline(name: str, target_s: float = 12.0) -> dict:
         "cpu_model": model,
         "logical_cpus": os.cpu_count(),
     }
-    # the same oracle on one thread, on the first 1,024 tokens: the OpenMP
+    # the same oracle on one thread, on the first tokens: the OpenMP
     # runtime the oracle runs on is set to one thread and back
     import ctypes
     try:
@@ -265,10 +265,12 @@ def cpu_baseline(name: str, target_s: float = 12.0) -> dict:
         gomp.omp_set_num_threads(1)
         try:
             used = oracle.num_threads()
-            t1 = cpu_oracle_seconds(name, 1024)
+            # up to 1,024 tokens, fewer where one thread would take more than ~10 s
+            T1 = int(max(64, min(1024, 10.0 * out["value"] / max(out["cores"], 1))))
+            t1 = cpu_oracle_seconds(name, T1)
         finally:
             gomp.omp_set_num_threads(before)
-        out["single_thread"] = {"value": 1024 / t1, "unit": "tokens/s", "tokens": 1024, "seconds": round(t1, 2),
+        out["single_thread"] = {"value": T1 / t1, "unit": "tokens/s", "tokens": T1, "seconds": round(t1, 2),
                                 "threads": used}
     except OSError:
         out["single_thread"] = None
