@@ -72,36 +72,46 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p)
 __device__ __forceinline__ uint32_t lds_ld(uint32_t a) { return *(const lds_u32*)(size_t)a; }
 __device__ __forceinline__ float lds_ldf(uint32_t a) { return *(const lds_f32*)(size_t)a; }
 
-// Routes every hashed slot of levels >= lmin: finds the first parent slot q
+// Routes every hashed slot of the last level: finds the first parent slot q
 // of the previous level (in slot order) and the generator j with
 // c = parent_q XOR g_j, by looking c XOR parent_q up in the level's
-// collision-free generator hash: one probe per parent, all parents tried.
-// W.route[tt][s] = (q << 16) | j, or -1 when no pair exists.
-__device__ void route_slots(const DevPlan& P, const Wave& W, int lmin)
+// collision-free generator hash: one probe per parent, all parents tried,
+// four probes at a time (the reads of a batch are in flight together; the
+// parents' reads, then the table's).  W.route[tt][s] = (q << 16) | j, or -1
+// when no pair exists.
+__device__ void route_slots(const DevPlan& P, const Wave& W)
 {
-    const int k = P.k_tot, kmax = P.kmax;
-    if (P.gtab_total <= 0 || P.levels < 2) return;
-    for (int tt = 0; tt < W.ntok; ++tt)
-        for (int s = P.slot_base[lmin] + W.lane; s < k; s += 64) {
+    const int k = P.k_tot, l = P.levels - 1;
+    if (P.gtab_total <= 0 || l < 1) return;
+    const int Kp = P.active[l - 1], r = P.gtab_shift[l], sb = P.slot_base[l], sbp = P.slot_base[l - 1], d = P.d;
+    const uint32_t hmask = (1u << P.gtab_bits[l]) - 1u;
+    const u32x2* tab = (const u32x2*)W.gtab + P.gtab_off[l];
+    for (int tt = 0; tt < W.ntok; ++tt) {
+        const int32_t* parents = W.idx + tt * k + sbp;
+        for (int s = sb + W.lane; s < k; s += 64) {
             int rt = -1;
             const int32_t c = W.idx[tt * k + s];
-            if (c >= P.d) {
-                int l = lmin;
-                while (l + 1 < P.levels && s >= P.slot_base[l + 1]) ++l;
-                const int Kp = P.active[l - 1], r = P.gtab_shift[l];
-                const uint32_t hmask = (1u << P.gtab_bits[l]) - 1u;
-                const u32x2* tab = (const u32x2*)W.gtab + P.gtab_off[l];
-                const int32_t* parents = W.idx + tt * k + P.slot_base[l - 1];
-                for (int q = Kp - 1; q >= 0; --q) {
-                    const int32_t p = parents[q];
-                    const uint32_t x = (uint32_t)c ^ (uint32_t)p;
-                    const u32x2 e = tab[(x ^ (x >> r)) & hmask];
-                    if (p >= 0 && x != 0u && e.x == x) rt = (q << 16) | (int)e.y;
+            if (c >= d) {
+                for (int q0 = Kp - 1; q0 >= 0; q0 -= 4) {
+                    int32_t pq[4];
+                    uint32_t x[4];
+                    u32x2 e[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) pq[u] = parents[max(q0 - u, 0)];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        x[u] = (uint32_t)c ^ (uint32_t)pq[u];
+                        e[u] = tab[(x[u] ^ (x[u] >> r)) & hmask];
+                    }
+                    // descending q: the lowest matching parent slot is kept
+#pragma unroll
+                    for (int u = 0; u < 4; ++u)
+                        if (q0 - u >= 0 && pq[u] >= 0 && x[u] != 0u && e[u].x == x[u]) rt = ((q0 - u) << 16) | (int)e[u].y;
                 }
             }
             W.route[tt * k + s] = rt;
         }
-    (void)kmax;
+    }
 }
 
 // Bit transpose inside each 32-lane half: lane s of a half holds x_s on
@@ -683,7 +693,7 @@ __global__ __launch_bounds__(kThreads) void decode2_kernel(DevPlan P, const int3
         }
         wave_sync();
         if (P.leaf_columns) {
-            route_slots(P, W, P.levels - 1);
+            route_slots(P, W);
             wave_sync();
         }
         decode_tokens<!OUT_BF16, NG, PB16, kBatch, kDecodeUnroll>(P, W, W.coef);
@@ -896,7 +906,7 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
         // route the last level's slots to a parent slot of the previous level
         // (its scoring and the decode's leaf columns use the routes; plans with
         // many children per parent take every slot directly below)
-        if (!P.bwd_direct) route_slots(P, W, P.levels - 1);
+        if (!P.bwd_direct) route_slots(P, W);
         // coefficients for basis slots and padding
         for (int tt = 0; tt < TPW; ++tt)
             for (int s = lane; s < k; s += 64) {
