@@ -377,3 +377,24 @@ def test_decode_and_bwd_full_size_sampled(name):
     rgc, rgx = oracle.decode_bwd(w.d, m, ii, g.double().cpu().numpy()[rows])
     compare_dense(gc.cpu().numpy()[rows], rgc, TOL_F32)
     compare_dense(gx.float().cpu().numpy()[rows], rgx, TOL_BF16)
+
+
+@pytest.mark.parametrize("name", ["pt_small_2l", "pt_small_3l"])
+def test_wide_encode_deterministic(name):
+    """The GEMM epilogue reserves each wave's list space with an LDS atomic, so
+    the order of a token's listed candidates can differ from run to run; the
+    selection sorts them, so the code may not.  Plain and standardized scores,
+    three runs each, 3,000 tokens (a partial last tile of the level GEMMs)."""
+    say(f"[t6 determinism] {name}")
+    plan = plan_for(name)
+    w = inputs.workload(name)
+    x = inputs.activations(name, 3000).to(DEV)
+    N = 1 << plan.level_bits[-1]
+    mu, _, r = random_std_state(N, 55 + w.index)
+    stats = torch.from_numpy(np.stack([mu, r], axis=1)).contiguous().to(DEV)
+    for st in (None, stats):
+        runs = [dpb.encode(plan, x, stats=st) for _ in range(3)]
+        torch.cuda.synchronize()
+        for idx, coef in runs[1:]:
+            assert torch.equal(idx, runs[0][0])
+            assert torch.equal(coef.view(torch.int32), runs[0][1].view(torch.int32))
