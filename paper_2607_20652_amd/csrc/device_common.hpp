@@ -90,15 +90,15 @@ __device__ __forceinline__ uint32_t lane_xor(uint32_t v)
 {
     static_assert(J == 1 || J == 2 || J == 4 || J == 8 || J == 16 || J == 32, "power of two up to 32");
     if constexpr (J == 1) {
-        return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);   // quad_perm 1,0,3,2
+        return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false);   // quad_perm 1,0,3,2
     } else if constexpr (J == 2) {
-        return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);   // quad_perm 2,3,0,1
+        return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, false);   // quad_perm 2,3,0,1
     } else if constexpr (J == 4) {
-        const uint32_t r4 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x124, 0xF, 0xF, false);    // row_ror 4
-        const uint32_t r12 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x12C, 0xF, 0xF, false);   // row_ror 12
+        const uint32_t r4 = (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x124, 0xF, 0xF, false);    // row_ror 4
+        const uint32_t r12 = (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x12C, 0xF, 0xF, false);   // row_ror 12
         return (__lane_id() & 4) ? r4 : r12;
     } else if constexpr (J == 8) {
-        return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x128, 0xF, 0xF, false);   // row_ror 8
+        return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x128, 0xF, 0xF, false);   // row_ror 8
     } else if constexpr (J == 16) {
         const auto p = __builtin_amdgcn_permlane16_swap(v, v, false, false);
         return (__lane_id() & 16) ? p[0] : p[1];

@@ -86,8 +86,8 @@ __host__ __device__ inline unsigned enc_shared_bytes(const DevPlan& P, bool std)
 __device__ __forceinline__ uint32_t xlane(uint32_t v, int m, int x32addr)
 {
     switch (m) {
-    case 1: return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);
-    case 2: return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);
+    case 1: return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false);
+    case 2: return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, false);
     case 4: return swz_xor<4>(v);
     case 8: return swz_xor<8>(v);
     case 16: return swz_xor<16>(v);
@@ -370,8 +370,12 @@ __device__ void level0_std(const DevPlan& P, int lane, int64_t t0, int ntok, con
     }
 }
 
+// The variant for bf16 input, one token per wave, one block of sixteen parents
+// per level and plain scores is held to 128 registers, four waves per SIMD: it
+// fits without spilling.  The two-token variant fits too but measured slower
+// under that bound, so it keeps the compiler's own choice.
 template <bool X_BF16, int CPT, int R, bool STD>
-__global__ __launch_bounds__(kEncThreads) void encode3_kernel(DevPlan P, const void* __restrict__ xin, int64_t T,
+__global__ __launch_bounds__(kEncThreads, (X_BF16 && CPT == 16 && R == 4 && !STD) ? 4 : 1) void encode3_kernel(DevPlan P, const void* __restrict__ xin, int64_t T,
                                                               const float2* __restrict__ stats,
                                                               int32_t* __restrict__ out_idx,
                                                               float* __restrict__ out_coef)
