@@ -516,21 +516,25 @@ __global__ __launch_bounds__(kEncThreads, (X_BF16 && CPT == 16 && R == 4 && !STD
             const int Kl = P.active[l];
             bool done = false;
             if (Kl <= 2 * CPT && EL.listn >= 4 * CPT) {
-                uint64_t mx[1] = {keys[0]};
+                // the lane maxima are sorted by their magnitude word alone:
+                // K_l distinct magnitudes at or above tau are K_l distinct
+                // children, so tau = (that magnitude, lowest low word) still
+                // admits the K_l largest keys (a valid key of magnitude 0
+                // counts as none: then tau = 1)
+                uint64_t m64 = keys[0];
 #pragma unroll
-                for (int r = 1; r < R; ++r) mx[0] = keys[r] > mx[0] ? keys[r] : mx[0];
+                for (int r = 1; r < R; ++r) m64 = keys[r] > m64 ? keys[r] : m64;
+                uint32_t mx[1] = {(uint32_t)(m64 >> 32)};
                 sort_desc<1, NB, true>(mx, lanepos, x32);
-                const uint32_t ph = (uint32_t)__builtin_amdgcn_ds_bpermute(prev_addr, (int)(uint32_t)(mx[0] >> 32));
-                const uint32_t pl = (uint32_t)__builtin_amdgcn_ds_bpermute(prev_addr, (int)(uint32_t)mx[0]);
-                const uint64_t prev = lanepos > 0 ? (((uint64_t)ph << 32) | pl) : 0ull;
-                const bool kept = mx[0] != 0ull && mx[0] != prev;
+                const uint32_t ph = (uint32_t)__builtin_amdgcn_ds_bpermute(prev_addr, (int)mx[0]);
+                const uint32_t prev = lanepos > 0 ? ph : 0u;
+                const bool kept = mx[0] != 0u && mx[0] != prev;
                 const int rank = (int)__popcll(__ballot(kept) & before_mask);
                 const uint64_t owner = __ballot(kept && rank == Kl - 1) & token_mask;
                 uint64_t tau = 1ull;   // fewer than K_l distinct maxima: every key
                 if (owner) {
                     const int oa = (int)__builtin_ctzll(owner) << 2;
-                    tau = ((uint64_t)(uint32_t)__builtin_amdgcn_ds_bpermute(oa, (int)(uint32_t)(mx[0] >> 32)) << 32) |
-                          (uint32_t)__builtin_amdgcn_ds_bpermute(oa, (int)(uint32_t)mx[0]);
+                    tau = (uint64_t)(uint32_t)__builtin_amdgcn_ds_bpermute(oa, (int)mx[0]) << 32;
                 }
                 int c = 0;
 #pragma unroll
