@@ -321,7 +321,7 @@ def main() -> int:
         return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build runs on one GPU only; the DPB shards by tokens with no "
+        print("bench.py: measures one GPU only; the DPB shards by tokens with no "
               "communication, so a multi-GPU figure is N times the one-GPU value (not measured).",
               file=sys.stderr)
         return 2

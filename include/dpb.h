@@ -49,7 +49,7 @@ typedef enum { DPB_F32 = 0, DPB_BF16 = 1 } dpb_dtype;
 typedef enum {
     DPB_OK = 0,
     DPB_EINVAL = -1,       /* bad argument (shape, pointer, alignment, dtype) */
-    DPB_EUNSUPPORTED = -2, /* valid per the paper but outside what this build supports */
+    DPB_EUNSUPPORTED = -2, /* valid per the paper but outside what this library supports */
     DPB_EHIP = -3,         /* a HIP runtime call or kernel launch failed */
     DPB_ENOMEM = -4        /* device or host allocation failed (plan creation only) */
 } dpb_status;

@@ -8,7 +8,7 @@
  * HIP library; only tests, the smoke check and the benchmark's CPU-baseline leg
  * may load it.  The product path never calls it.
  *
- * Readings taken where the paper is silent (each also listed in the design doc):
+ * Readings taken where the paper is silent:
  *   R1  indices are 0-based: phi_i = e_i for 0 <= i < d  (Eq. 2 writes i <= d).
  *   R2  bit p of an index (LSB = 0) pairs with column p of M; columns 0..t-1
  *       hold coord(xi), columns t..2t-1 hold coord(xi^-1)  (App. A.4).

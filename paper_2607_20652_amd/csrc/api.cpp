@@ -470,7 +470,7 @@ const char* dpb_status_string(dpb_status s)
     switch (s) {
     case DPB_OK: return "DPB_OK";
     case DPB_EINVAL: return "DPB_EINVAL: invalid argument";
-    case DPB_EUNSUPPORTED: return "DPB_EUNSUPPORTED: configuration not supported by this build";
+    case DPB_EUNSUPPORTED: return "DPB_EUNSUPPORTED: configuration not supported by this library";
     case DPB_EHIP: return "DPB_EHIP: HIP runtime or launch failure";
     case DPB_ENOMEM: return "DPB_ENOMEM: allocation failed";
     }

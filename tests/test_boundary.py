@@ -76,7 +76,7 @@ def _create(lib, *args):
     ((64, 12, 3, 0, 4, 8, 0), -1),        # no children
     ((64, 7, 3, 16, 4, 8, 0), -1),        # level bits not increasing
     ((64, 12, 3, 500, 4, 8, 0), -1),      # more generators than level 1 holds (448)
-    ((8192, 26, 2, 16, 4, 8, 0), -2),     # wider than this build supports
+    ((8192, 26, 2, 16, 4, 8, 0), -2),     # wider than the library supports
 ])
 def test_plan_create_rejects_bad_arguments_before_touching_the_gpu(lib, args, status):
     assert _create(lib, *args) == status
