@@ -114,3 +114,52 @@ def test_plan_sweep(case):
     e1 = compare_dense(gc.cpu().numpy(), rgc, TOL_F32)
     e2 = compare_dense(gx.float().cpu().numpy(), rgx, tol)
     say(f"  y err {ey:.3g}  grad_coef err {e1:.3g}  grad_x err {e2:.3g}")
+
+
+@pytest.mark.parametrize("case", range(0, len(CASES), 2))
+def test_plan_sweep_forward_and_std_update(case):
+    """The forward call equals encode followed by decode bit for bit, and the
+    statistics update on the standardized code matches the oracle's."""
+    d, nb, dl, K, dt, T = CASES[case]
+    say(f"[sweep fwd/update {case}] d={d} n={nb} delta={dl} K={K} {dt} T={T}")
+    try:
+        plan = dpb.Plan(d, seed=0, level_bits=nb, branchings=dl, active=K)
+    except dpb.DPBError as e:
+        pytest.skip(f"unsupported plan: {e}")
+    x = inputs.normal((T, d), 7300 + case, dt).to(DEV)
+    idx, coef, y = dpb.forward(plan, x)
+    ri, rc = dpb.encode(plan, x)
+    ry = dpb.decode(plan, ri, rc, x.dtype)
+    torch.cuda.synchronize()
+    assert torch.equal(idx, ri) and torch.equal(coef.view(torch.int32), rc.view(torch.int32))
+    assert torch.equal(y.view(torch.int16) if y.dtype == torch.bfloat16 else y.view(torch.int32),
+                       ry.view(torch.int16) if ry.dtype == torch.bfloat16 else ry.view(torch.int32))
+
+    N = 1 << nb[-1]
+    mu, m2, r = random_std_state(N, 7400 + case)
+    stats = torch.from_numpy(np.stack([mu, r], axis=1)).contiguous().to(DEV)
+    m2d = torch.from_numpy(m2).to(DEV)
+    try:
+        sidx, _ = dpb.encode(plan, x, stats=stats)
+    except dpb.DPBError as e:   # plans only the general encoder takes have no standardized encoder
+        pytest.skip(f"forward checked; standardized encode unsupported: {e}")
+    before = stats.clone()
+    beta = 0.3
+    try:
+        dpb.std_update(plan, x, sidx, stats, m2d, beta, 1e-6)
+    except dpb.DPBError as e:
+        pytest.skip(f"statistics update unsupported: {e}")
+    torch.cuda.synchronize()
+    m = oracle.masks(d, nb[-1])
+    gens = oracle.generators(nb, dl, 0)
+    rmu, rm2 = oracle.std_update(d, m, nb, K, dl, gens, x.double().cpu().numpy(), sidx.cpu().numpy(),
+                                 mu.astype(np.float64), m2.astype(np.float64), beta)
+    gs, gv = stats.cpu().numpy(), m2d.cpu().numpy()
+    touched = (rmu != mu.astype(np.float64)) | (rm2 != m2.astype(np.float64))
+    say(f"  touched {int(touched.sum())} of {N}")
+    assert np.array_equal(gs[~touched], before.cpu().numpy()[~touched])
+    assert np.array_equal(gv[~touched], m2[~touched])
+    assert np.allclose(gs[touched, 0], rmu[touched], rtol=1e-5, atol=1e-5)
+    assert np.allclose(gv[touched], rm2[touched], rtol=1e-5, atol=1e-5)
+    rr = oracle.std_r(gs[touched, 0].astype(np.float64), gv[touched].astype(np.float64), 1e-6)
+    assert np.allclose(gs[touched, 1], rr, rtol=2e-6, atol=0)
