@@ -440,6 +440,10 @@ def main() -> int:
         "fwd_tokens_per_s": (T / ((per_kernel_ms["encode"] + per_kernel_ms["decode"]) * 1e-3)
                              if run["encode"] and run["decode"] else None),
         "fwd_hbm_ceiling_tokens_per_s": HBM_PEAK_GBS * 1e9 / bpt["forward"],
+        # backward alone (decode-backward), and its HBM ceiling (read the code
+        # indices and g, write grad_coef and grad_x once)
+        "bwd_tokens_per_s": T / (per_kernel_ms["decode_bwd"] * 1e-3) if run["decode_bwd"] else None,
+        "bwd_hbm_ceiling_tokens_per_s": HBM_PEAK_GBS * 1e9 / bpt["decode_bwd"],
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
