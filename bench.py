@@ -185,7 +185,7 @@ def time_extras(plan, w, sets, act, steps: int) -> dict:
     for name, (fn, bpt) in cases.items():
         try:
             fn()
-        except dpb.DPBError as e:        # e.g. no standardized encoder for this hierarchy
+        except dpb.DPBError as e:        # a call outside the library's limits for this hierarchy
             res[name] = {"unsupported": str(e)}
             continue
         for _ in range(2):

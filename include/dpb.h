@@ -234,7 +234,8 @@ dpb_status dpb_std_init(const dpb_plan* plan, float* stats, float* m2, void* str
  * z is the coefficient written to the code.  Level-0 z is computed in fp32
  * as (x - mu) * r.  Arguments as dpb_encode (the same workspace rule), plus
  *   stats : device fp32 [N][2] (read; required).
- * DPB_EUNSUPPORTED for plans only the general encoder covers. */
+ * Every plan the library accepts is supported (each encoder has a
+ * standardized form). */
 dpb_status dpb_encode_std(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, int64_t T, const float* stats,
                           int32_t* idx, float* coef, void* workspace, size_t ws_bytes, void* stream);
 

@@ -358,16 +358,14 @@ dpb_status upload(dpb_plan* plan)
 
 // The encoder that runs a plan: the narrow one (a level's candidates in one
 // wave's registers), the wide one (a GEMM per level and a workspace), or the
-// general one; None when no encoder covers the plan for this activation type
-// (or, with statistics, on standardized scores, which the general encoder
-// does not take).
+// general one; None when no encoder covers the plan for this activation type.
 enum class Enc { Narrow, Wide, General, None };
 
 Enc pick_encoder(const DevPlan& P, bool x_bf16, bool std)
 {
     if (dpb::encode2_supported(P) && (!std || dpb::encode2_std_supported(P))) return Enc::Narrow;
     if (dpb::encode_wide_supported(P, x_bf16)) return Enc::Wide;
-    if (!std && dpb::general_encoder_fits(P)) return Enc::General;
+    if (dpb::general_encoder_fits(P)) return Enc::General;
     return Enc::None;
 }
 
@@ -456,7 +454,7 @@ dpb_status encode_any(const dpb_plan* plan, const void* x, dpb_dtype x_dtype, in
     case Enc::Wide:
         if (!own_scratch && (!workspace || ws_bytes < dpb::encode_wide_workspace_bytes(P, T))) return DPB_EINVAL;
         return launched(dpb::launch_encode_wide(P, x, bf, T, stats, idx, coef, workspace, st, chunk));
-    case Enc::General: return launched(dpb::launch_encode(P, x, bf, T, idx, coef, st));
+    case Enc::General: return launched(dpb::launch_encode(P, x, bf, T, stats, idx, coef, st));
     default: return DPB_EUNSUPPORTED;
     }
 }

@@ -235,7 +235,7 @@ hipError_t launch_variance_grad(int64_t T, int k, int64_t nfeat, int S, void* ws
                                 const float* grad_scale, hipStream_t stream);
 
 // General encoder (encode_general.hip) for plans outside the narrow and wide encoders.
-hipError_t launch_encode(const DevPlan& P, const void* x, bool x_bf16, int64_t T, int32_t* idx,
+hipError_t launch_encode(const DevPlan& P, const void* x, bool x_bf16, int64_t T, const float* stats, int32_t* idx,
                          float* coef, hipStream_t stream);
 
 }  // namespace dpb

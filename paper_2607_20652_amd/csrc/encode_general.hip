@@ -13,7 +13,9 @@
 // (App. A.4, packed-parity equation).  Products of +-1 with bf16 are exact
 // and accumulate in fp32; fp32 inputs are split exactly into three bf16
 // terms.  The keys of a token's candidates are sorted in LDS by a bitonic
-// network over the workgroup.
+// network over the workgroup.  With statistics (STD) every score is first
+// standardized, z = (s - mu) r with the candidate's (mu, r) (§2.2 "Score
+// Standardization"), in the same fp32 arithmetic as the other encoders.
 #include "device_common.hpp"
 
 namespace dpb {
@@ -51,8 +53,9 @@ __device__ __forceinline__ uint32_t flip_bits8(const uint32_t* s_mask, int base,
            (parity(m1.x & p) << 4) | (parity(m1.y & p) << 5) | (parity(m1.z & p) << 6) | (parity(m1.w & p) << 7);
 }
 
-template <bool X_BF16>
+template <bool X_BF16, bool STD>
 __global__ __launch_bounds__(kBlock) void encode_kernel(DevPlan P, const void* __restrict__ xin, int64_t T,
+                                                        const float2* __restrict__ stats,
                                                         int32_t* __restrict__ out_idx,
                                                         float* __restrict__ out_coef, int tile_tokens)
 {
@@ -98,6 +101,10 @@ __global__ __launch_bounds__(kBlock) void encode_kernel(DevPlan P, const void* _
                     float v;
                     if constexpr (X_BF16) v = bf16_bits_to_f32(((const uint16_t*)s_x)[tt * dp + iota]);
                     else v = ((const float*)s_x)[tt * dp + iota];
+                    if constexpr (STD) {
+                        const float2 st = stats[iota];
+                        v = (v - st.x) * st.y;
+                    }
                     const uint64_t key = make_key(v, (uint32_t)iota);
                     best = key > best ? key : best;
                 }
@@ -181,7 +188,13 @@ __global__ __launch_bounds__(kBlock) void encode_kernel(DevPlan P, const void* _
                 for (int i = 0; i < 4; ++i) {
                     const int j = mb * 16 + kq * 4 + i;
                     if (j < Dl) {
-                        const uint64_t key = cv ? make_key(acc[i] * P.rsd, up ^ gens[j]) : 0ull;
+                        float sc = acc[i] * P.rsd;
+                        if constexpr (STD)
+                            if (cv) {
+                                const float2 st = stats[up ^ gens[j]];
+                                sc = (sc - st.x) * st.y;
+                            }
+                        const uint64_t key = cv ? make_key(sc, up ^ gens[j]) : 0ull;
                         s_key[tt * cpm + kk * Dl + j] = key;
                     }
                 }
@@ -253,8 +266,8 @@ int pick_tile_tokens(const DevPlan& P, int x_bytes)
 
 bool general_encoder_fits(const DevPlan& P) { return encode_layout(P, 4, 1).bytes <= (unsigned)kLdsBudget; }
 
-hipError_t launch_encode(const DevPlan& P, const void* x, bool x_bf16, int64_t T, int32_t* idx, float* coef,
-                         hipStream_t stream)
+hipError_t launch_encode(const DevPlan& P, const void* x, bool x_bf16, int64_t T, const float* stats, int32_t* idx,
+                         float* coef, hipStream_t stream)
 {
     const int xb = x_bf16 ? 2 : 4;
     const int tt = pick_tile_tokens(P, xb);
@@ -262,14 +275,18 @@ hipError_t launch_encode(const DevPlan& P, const void* x, bool x_bf16, int64_t T
     if (L.bytes > (unsigned)kLdsBudget) return hipErrorInvalidValue;
     const int64_t blocks = (T + tt - 1) / tt;
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
-    allow_lds(encode_kernel<true>, L.bytes);
-    allow_lds(encode_kernel<false>, L.bytes);
-    if (x_bf16)
-        hipLaunchKernelGGL(encode_kernel<true>, dim3((unsigned)blocks), dim3(kBlock), L.bytes, stream, P, x, T, idx,
-                           coef, tt);
-    else
-        hipLaunchKernelGGL(encode_kernel<false>, dim3((unsigned)blocks), dim3(kBlock), L.bytes, stream, P, x, T,
-                           idx, coef, tt);
+    const float2* st = (const float2*)stats;
+#define DPB_GEN(XB, SD)                                                                                           \
+    do {                                                                                                          \
+        allow_lds(encode_kernel<XB, SD>, L.bytes);                                                                \
+        hipLaunchKernelGGL((encode_kernel<XB, SD>), dim3((unsigned)blocks), dim3(kBlock), L.bytes, stream, P, x, T, \
+                           st, idx, coef, tt);                                                                    \
+    } while (0)
+    if (x_bf16 && st) DPB_GEN(true, true);
+    else if (x_bf16) DPB_GEN(true, false);
+    else if (st) DPB_GEN(false, true);
+    else DPB_GEN(false, false);
+#undef DPB_GEN
     return hipGetLastError();
 }
 

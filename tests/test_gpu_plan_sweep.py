@@ -89,17 +89,13 @@ def test_plan_sweep(case):
     # standardized scores (§2.2 "Score Standardization") with random statistics
     mu, _, r = random_std_state(1 << nb[-1], 7200 + case)
     stats = torch.from_numpy(np.stack([mu, r], axis=1)).contiguous().to(DEV)
-    try:
-        sidx, scoef = dpb.encode(plan, x.to(DEV), stats=stats)
-    except dpb.DPBError as e:
-        say(f"  standardized encode unsupported: {e}")
-    else:
-        torch.cuda.synchronize()
-        si, sc, sm, so = oracle.encode_std(d, m, nb, K, dl, gens, xd, mu, r)
-        st2 = compare_encode(K, sidx.cpu().numpy(), scoef.cpu().numpy(), si, sc, sm, so, TOL_F32,
-                             ctx=EncodeCheck(d, m, gens, xd, mu, r))
-        say(f"  encode std {st2}")
-        assert st2["exempt_tokens"] <= max(2, 0.05 * T)
+    sidx, scoef = dpb.encode(plan, x.to(DEV), stats=stats)   # every accepted plan has a standardized encoder
+    torch.cuda.synchronize()
+    si, sc, sm, so = oracle.encode_std(d, m, nb, K, dl, gens, xd, mu, r)
+    st2 = compare_encode(K, sidx.cpu().numpy(), scoef.cpu().numpy(), si, sc, sm, so, TOL_F32,
+                         ctx=EncodeCheck(d, m, gens, xd, mu, r))
+    say(f"  encode std {st2}")
+    assert st2["exempt_tokens"] <= max(2, 0.05 * T)
 
     tdt = torch.float32 if dt == "f32" else torch.bfloat16
     tol = TOL_F32 if dt == "f32" else TOL_BF16
@@ -139,10 +135,7 @@ def test_plan_sweep_forward_and_std_update(case):
     mu, m2, r = random_std_state(N, 7400 + case)
     stats = torch.from_numpy(np.stack([mu, r], axis=1)).contiguous().to(DEV)
     m2d = torch.from_numpy(m2).to(DEV)
-    try:
-        sidx, _ = dpb.encode(plan, x, stats=stats)
-    except dpb.DPBError as e:   # plans only the general encoder takes have no standardized encoder
-        pytest.skip(f"forward checked; standardized encode unsupported: {e}")
+    sidx, _ = dpb.encode(plan, x, stats=stats)
     before = stats.clone()
     beta = 0.3
     try:
