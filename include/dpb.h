@@ -86,7 +86,13 @@ dpb_status dpb_plan_create(dpb_plan** out, int d, int n_bits, int levels, int br
  * branching[l] = Delta_l (index 0 ignored), active[l] = K_l with
  * 1 <= K_0 <= d and 1 <= K_l <= K_{l-1} * Delta_l.  `generators` (host
  * pointer, may be NULL) supplies sum_{l>=1} Delta_l distinct generators, level
- * by level, each in [2^{n_{l-1}}, 2^{n_l}); NULL draws them from `seed`. */
+ * by level, each in [2^{n_{l-1}}, 2^{n_l}); NULL draws them from `seed`.
+ * DPB_EINVAL for arrays that break these rules.  DPB_EUNSUPPORTED for valid
+ * plans outside the library's limits: d > 4096; n_last > 3t or 2t > 31 with
+ * t = ceil(log2 d) (the mask construction of App. A.4 over GF(2^t)); any
+ * K_l > 256; any Delta_l > 4096 or K_{l-1} Delta_l > 8192 candidates per
+ * token and level; sum_l K_l > 1024; and plans whose one-token encoder or
+ * one-token decode rows exceed the 160 KB of LDS of a compute unit. */
 dpb_status dpb_plan_create_ex(dpb_plan** out, int d, int levels, const int* level_bits,
                               const int* branching, const int* active,
                               const uint32_t* generators, uint64_t seed);

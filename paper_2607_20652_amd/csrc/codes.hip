@@ -979,9 +979,27 @@ dim3 code_grid(const DevPlan& P, int64_t T, size_t lds, int rounds)
 
 }  // namespace
 
-bool code_kernels_fit(const DevPlan& P)
+static bool code_rows_fit(const DevPlan& P)
 {
     return code_lds_bytes(P, true, true) <= (size_t)kLdsBudget && code_lds_bytes(P, true, false) <= (size_t)kLdsBudget;
+}
+
+// The plan as the code kernels take it: a wave keeps the encoder's
+// wave_tokens tokens (16 parent columns) where their rows fit the LDS budget;
+// wide rows with few parents per token (d in the thousands, K_0 of 2 or 4)
+// get fewer tokens per wave, halved until they fit.  Every kernel here sizes
+// its LDS regions and bounds its token and column loops by this count, so a
+// wave simply leaves some of the 16 columns empty.
+static DevPlan code_plan(const DevPlan& P)
+{
+    DevPlan C = P;
+    while (C.wave_tokens > 1 && !code_rows_fit(C)) C.wave_tokens >>= 1;
+    return C;
+}
+
+bool code_kernels_fit(const DevPlan& P)
+{
+    return code_rows_fit(code_plan(P));
 }
 
 // Kernel variants: index groups NG in {3, 4, 5, 6, 8} (a larger NG than the
@@ -1013,9 +1031,10 @@ static void launch_decode_ng(const DevPlan& P, dim3 grid, size_t lds, hipStream_
     }
 }
 
-hipError_t launch_decode2(const DevPlan& P, const int32_t* idx, const float* coef, int64_t T, void* y, bool y_bf16,
+hipError_t launch_decode2(const DevPlan& Pp, const int32_t* idx, const float* coef, int64_t T, void* y, bool y_bf16,
                           hipStream_t stream)
 {
+    const DevPlan P = code_plan(Pp);
     const size_t lds = code_lds_bytes(P, false, true);
     if (lds > (size_t)kLdsBudget) return hipErrorInvalidValue;
     const dim3 grid = code_grid(P, T, lds, 1);
@@ -1063,10 +1082,11 @@ static void launch_bwd_ub(const DevPlan& P, dim3 grid, size_t lds, hipStream_t s
     else launch_bwd_ng<GB, XB, false>(P, grid, lds, stream, idx, g, T, gc, gx, ex);
 }
 
-hipError_t launch_decode_bwd2(const DevPlan& P, const int32_t* idx, const void* g, bool g_bf16, int64_t T,
+hipError_t launch_decode_bwd2(const DevPlan& Pp, const int32_t* idx, const void* g, bool g_bf16, int64_t T,
                               float* grad_coef, void* grad_x, bool gx_bf16, hipStream_t stream,
                               const float* add_grad_coef, const void* add_grad_x, const float* stats)
 {
+    const DevPlan P = code_plan(Pp);
     const size_t lds = code_lds_bytes(P, true, g_bf16);
     if (lds > (size_t)kLdsBudget) return hipErrorInvalidValue;
     const dim3 grid = code_grid(P, T, lds, 4);

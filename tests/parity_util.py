@@ -38,11 +38,17 @@ def rel_err(got: np.ndarray, ref: np.ndarray) -> np.ndarray:
 
 
 def coef_err(got: np.ndarray, ref: np.ndarray) -> np.ndarray:
-    """|got - ref| / |ref| element by element (0 where both are 0)."""
+    """|got - ref| / max(|ref|, rms of ref along the last axis), element by
+    element (0 where got equals ref): the relative bar taken against the
+    row's scale, as for decoded rows, with one token's coefficients of one
+    level as the row.  A level that keeps every child also keeps scores near
+    zero, whose fp32 sums cannot meet 1e-5 of their own magnitude."""
     got = np.asarray(got, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
     diff = np.abs(got - ref)
-    return np.where(diff == 0, 0.0, diff / np.where(ref == 0, 1e-300, np.abs(ref)))
+    rms = np.sqrt(np.mean(ref * ref, axis=-1, keepdims=True)) if ref.size else ref
+    den = np.maximum(np.abs(ref), rms)
+    return np.where(diff == 0, 0.0, diff / np.where(den == 0, 1e-300, den))
 
 
 class EncodeCheck:

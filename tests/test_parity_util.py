@@ -41,7 +41,8 @@ def _mutated(case, fn):
 
 
 @pytest.mark.parametrize("all_near_ties", [False, True])
-@pytest.mark.parametrize("mistake", ["foreign_index", "weak_candidate", "coef", "order", "repeat", "padding"])
+@pytest.mark.parametrize("mistake", ["foreign_index", "weak_candidate", "coef", "coef_row_scale", "order", "repeat",
+                                     "padding"])
 def test_planted_mistakes_are_caught(case, all_near_ties, mistake):
     K, _, _, _, _, ctx = case
     s1 = K[0]                     # first slot of level 1
@@ -60,6 +61,10 @@ def test_planted_mistakes_are_caught(case, all_near_ties, mistake):
             oc[t, sL + K[-1] - 1] = s[np.argmin(np.abs(s))]
         elif mistake == "coef":
             oc[t, s1 + 2] *= 1.0 + 1e-4
+        elif mistake == "coef_row_scale":   # the weakest slot moved by 1e-4 of its level row's rms, toward 0
+            row = oc[t, sL:sL + K[-1]]
+            shift = 1e-4 * np.sqrt(np.mean(row * row))
+            oc[t, sL + K[-1] - 1] -= np.sign(oc[t, sL + K[-1] - 1]) * shift
         elif mistake == "order":
             oi[t, [s1, s1 + 1]] = oi[t, [s1 + 1, s1]]
             oc[t, [s1, s1 + 1]] = oc[t, [s1 + 1, s1]]
