@@ -53,13 +53,16 @@ __host__ __device__ inline int enc_r(const DevPlan& P)
     return 4 * pow2_ceil(mb);
 }
 
-__host__ __device__ inline EncLayout enc_layout(const DevPlan& P, bool act_bf16)
+__host__ __device__ inline EncLayout enc_layout(const DevPlan& P, bool act_bf16, bool std = false)
 {
     EncLayout L;
     const int TPW = P.wave_tokens, LPT = 64 / TPW;
     const int ND = (P.dp / 2 + LPT - 1) / LPT;  // activation dwords per lane at level 0
-    // level-0 candidates: the K_0 lanes whose maximum reaches tau, each with all its keys
-    int listn = P.active[0] * (act_bf16 ? 2 * ND : (P.d + LPT - 1) / LPT);
+    // level-0 candidates: the K_0 lanes whose maximum reaches tau, each with all
+    // its keys; listn counts 64-bit words per token.  Plain bf16 keys are 32
+    // bits (2 ND per lane, two to a word); standardized and fp32 keys are 64.
+    const int listn = (act_bf16 && !std) ? P.active[0] * ND
+                                         : P.active[0] * (act_bf16 ? 2 * ND : (P.d + LPT - 1) / LPT);
     L.listn = listn;
     L.kmaxp = P.kmax;
     unsigned off = 0;
@@ -370,12 +373,13 @@ __device__ void level0_std(const DevPlan& P, int lane, int64_t t0, int ntok, con
     }
 }
 
-// The variant for bf16 input, one token per wave, one block of sixteen parents
-// per level and plain scores is held to 128 registers, four waves per SIMD: it
-// fits without spilling.  The two-token variant fits too but measured slower
-// under that bound, so it keeps the compiler's own choice.
+// The variants for bf16 input with one block of sixteen parent columns per
+// level and plain scores (one or two tokens per wave) are held to 128
+// registers, four waves per SIMD: both fit without spilling.  The two-token
+// variant gains from it only because its level-0 list holds 32-bit keys at
+// half the 64-bit size, so that four workgroups fit the LDS of a CU.
 template <bool X_BF16, int CPT, int R, bool STD>
-__global__ __launch_bounds__(kEncThreads, (X_BF16 && CPT == 16 && R == 4 && !STD) ? 4 : 1) void encode3_kernel(DevPlan P, const void* __restrict__ xin, int64_t T,
+__global__ __launch_bounds__(kEncThreads, (X_BF16 && (CPT == 16 || CPT == 8) && R == 4 && !STD) ? 4 : 1) void encode3_kernel(DevPlan P, const void* __restrict__ xin, int64_t T,
                                                               const float2* __restrict__ stats,
                                                               int32_t* __restrict__ out_idx,
                                                               float* __restrict__ out_coef)
@@ -397,7 +401,7 @@ __global__ __launch_bounds__(kEncThreads, (X_BF16 && CPT == 16 && R == 4 && !STD
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int d = P.d, dp = P.dp;
     const int x32 = (lane ^ 32) << 2;
-    const EncLayout EL = enc_layout(P, X_BF16);
+    const EncLayout EL = enc_layout(P, X_BF16, STD);
     unsigned char* wb = smem + enc_shared_bytes(P, STD) + (unsigned)wave * EL.bytes;
     uint32_t* pairs = (uint32_t*)(wb + EL.act);
     float* xf = (float*)(wb + EL.act);
@@ -1277,7 +1281,7 @@ hipError_t launch_encode2(const DevPlan& P, const void* x, bool x_bf16, int64_t 
                           float* coef, hipStream_t stream)
 {
     const float2* st = (const float2*)stats;
-    const size_t lds = enc_shared_bytes(P, stats != nullptr) + (size_t)kEncWaves * enc_layout(P, x_bf16).bytes;
+    const size_t lds = enc_shared_bytes(P, stats != nullptr) + (size_t)kEncWaves * enc_layout(P, x_bf16, stats != nullptr).bytes;
     const int64_t groups = (T + P.wave_tokens - 1) / P.wave_tokens;
     const int64_t need = (groups + kEncWaves - 1) / kEncWaves;
     int cus = 256, dev = 0;
