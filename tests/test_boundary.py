@@ -82,6 +82,23 @@ def test_plan_create_rejects_bad_arguments_before_touching_the_gpu(lib, args, st
     assert _create(lib, *args) == status
 
 
+@pytest.mark.parametrize("d,level_bits,branching,active", [
+    (5000, [13, 16], [0, 16], [4, 8]),                                    # d > 4096
+    (64, [6, 19], [0, 16], [4, 8]),                                       # n_last > 3t (t = 6)
+    (1024, [10, 14], [0, 64], [8, 300]),                                  # K_1 > 256
+    (1024, [10, 14], [0, 5000], [1, 8]),                                  # Delta_1 > 4096
+    (1024, [10, 15], [0, 256], [64, 32]),                                 # K_0 Delta_1 = 16384 candidates
+    (1024, [10, 13, 16, 19, 22], [0, 32, 32, 32, 32], [256] * 5),        # k_tot = 1280 > 1024
+])
+def test_plans_outside_the_library_limits_are_unsupported(lib, d, level_bits, branching, active):
+    """Valid hierarchies beyond the documented limits of dpb_plan_create_ex
+    get DPB_EUNSUPPORTED, found on the host before any device call."""
+    h = ctypes.c_void_p()
+    st = lib.dpb_plan_create_ex(ctypes.byref(h), d, len(level_bits), binding._ints(level_bits),
+                                binding._ints(branching), binding._ints(active), None, 0)
+    assert st == -2
+
+
 def test_compute_calls_reject_null_plan(lib):
     P = ctypes.c_void_p
     assert lib.dpb_encode(None, P(16), 0, 4, P(16), P(16), None, 0, None) == -1
