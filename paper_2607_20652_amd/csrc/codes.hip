@@ -599,10 +599,10 @@ __device__ void write_rows(const DevPlan& P, const Wave& W, void* out, const voi
             if (vec) {
                 if constexpr (OUT_BF16) {
                     u32x4 v;
-                    v.x = f32_to_bf16_rne(a.x) | (f32_to_bf16_rne(a.y) << 16);
-                    v.y = f32_to_bf16_rne(a.z) | (f32_to_bf16_rne(a.w) << 16);
-                    v.z = f32_to_bf16_rne(b.x) | (f32_to_bf16_rne(b.y) << 16);
-                    v.w = f32_to_bf16_rne(b.z) | (f32_to_bf16_rne(b.w) << 16);
+                    v.x = pack_bf16x2(a.x, a.y);
+                    v.y = pack_bf16x2(a.z, a.w);
+                    v.z = pack_bf16x2(b.x, b.y);
+                    v.w = pack_bf16x2(b.z, b.w);
                     *(u32x4*)((uint16_t*)out + r0 + o) = v;
                 } else {
                     *(float4*)((float*)out + r0 + o) = a;

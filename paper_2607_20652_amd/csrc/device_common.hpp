@@ -29,6 +29,16 @@ __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f)
     return u >> 16;
 }
 
+// Two fp32 values rounded to nearest even as one word of bf16 (lo in bits
+// 0-15): a single hardware conversion on gfx950, equal to f32_to_bf16_rne of
+// each half for every non-NaN input.
+typedef float dpb_f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 dpb_bf16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi)
+{
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((dpb_f32x2){lo, hi}, dpb_bf16x2));
+}
+
 __device__ __forceinline__ uint32_t parity(uint32_t v) { return __popc(v) & 1u; }
 
 // +-a where the sign flips when popcount(m) is odd: the entry of a hashed

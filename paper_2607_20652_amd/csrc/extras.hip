@@ -53,10 +53,10 @@ __device__ __forceinline__ void store8(void* p, bool bf16, int64_t i, int64_t n,
     if (vec) {
         if (bf16) {
             u32x4 q;
-            q.x = f32_to_bf16_rne(v[0]) | (f32_to_bf16_rne(v[1]) << 16);
-            q.y = f32_to_bf16_rne(v[2]) | (f32_to_bf16_rne(v[3]) << 16);
-            q.z = f32_to_bf16_rne(v[4]) | (f32_to_bf16_rne(v[5]) << 16);
-            q.w = f32_to_bf16_rne(v[6]) | (f32_to_bf16_rne(v[7]) << 16);
+            q.x = pack_bf16x2(v[0], v[1]);
+            q.y = pack_bf16x2(v[2], v[3]);
+            q.z = pack_bf16x2(v[4], v[5]);
+            q.w = pack_bf16x2(v[6], v[7]);
             *(u32x4*)((uint16_t*)p + i) = q;
         } else {
             *(float4*)((float*)p + i) = make_float4(v[0], v[1], v[2], v[3]);
