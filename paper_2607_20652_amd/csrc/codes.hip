@@ -202,7 +202,8 @@ __device__ void fr_chunk(const DevPlan& P, const Wave& W, int tt, int n, bool fi
 }
 
 // Coordinate loop of the table decode over Wn words; LG (even, <= 8) groups
-// of each word are summed (the others hold no slot).
+// of each word are summed (the others hold no slot).  Two coordinates at a
+// time, all their table reads ahead of their writes.
 template <int NG, int LG, bool PB16>
 __device__ __forceinline__ void fr_coords(const DevPlan& P, const Wave& W, int tt, int Wn, bool first, int pbpos, int pbn)
 {
@@ -211,13 +212,13 @@ __device__ __forceinline__ void fr_coords(const DevPlan& P, const Wave& W, int t
     float* yt = W.y + tt * dp;
     const int w0 = pbpos >> 5, sh = pbpos & 31;
     const uint32_t pmask = pbn >= 32 ? ~0u : ((1u << pbn) - 1u);
-#pragma unroll 2
-    for (int iota = lane; iota < dp; iota += 64) {
+    auto eval = [&](int iota, float& acc, uint32_t& lo, uint32_t& hi) {
         // 4 x nibble g of the row mask: even groups in s0, odd groups in s1, byte g / 2
         const uint32_t M = W.mask[iota];
         const uint32_t s0 = (M << 2) & 0x3C3C3C3Cu, s1 = (M >> 2) & 0x3C3C3C3Cu;
-        float acc = 0.f;
-        uint32_t lo = 0, hi = 0;
+        acc = 0.f;
+        lo = 0;
+        hi = 0;
         for (int w = 0; w < Wn; ++w) {
             const uint32_t vb = vbase + (uint32_t)(w * 512), tb = tbase + (uint32_t)(w * 512);
             uint32_t U = 0;
@@ -232,6 +233,8 @@ __device__ __forceinline__ void fr_coords(const DevPlan& P, const Wave& W, int t
             lo = w == w0 ? U : lo;
             hi = w == w0 + 1 ? U : hi;
         }
+    };
+    auto store = [&](int iota, float acc, uint32_t lo, uint32_t hi) {
         if (first) yt[iota] = acc;
         else yt[iota] += acc;
         if (pbn > 0) {
@@ -239,12 +242,29 @@ __device__ __forceinline__ void fr_coords(const DevPlan& P, const Wave& W, int t
             if constexpr (PB16) ((uint16_t*)W.pb)[tt * dp + iota] = (uint16_t)bits;
             else ((uint8_t*)W.pb)[tt * dp + iota] = (uint8_t)bits;
         }
+    };
+    int iota = lane;
+    for (; iota + 64 < dp; iota += 128) {
+        float a0, a1;
+        uint32_t l0, h0, l1, h1;
+        eval(iota, a0, l0, h0);
+        eval(iota + 64, a1, l1, h1);
+        store(iota, a0, l0, h0);
+        store(iota + 64, a1, l1, h1);
+    }
+    if (iota < dp) {
+        float a;
+        uint32_t l, h;
+        eval(iota, a, l, h);
+        store(iota, a, l, h);
     }
 }
 
 // The common case of the coordinate loop: one word, the first write of y,
-// the leaf parents' sign bits inside the word.  The body has no branches,
-// so the compiler overlaps the table reads of consecutive coordinates.
+// the leaf parents' sign bits inside the word.  FRU coordinates at a time:
+// every table read of the group is issued before any of its writes (the
+// compiler cannot reorder reads past stores to the same LDS), so their
+// latencies overlap.
 template <int NG, int LG, bool PB16, int FRU>
 __device__ __forceinline__ void fr_coords1(const DevPlan& P, const Wave& W, int tt, int pbpos, int pbn)
 {
@@ -252,23 +272,43 @@ __device__ __forceinline__ void fr_coords1(const DevPlan& P, const Wave& W, int 
     const uint32_t vb = lds_addr(W.frv), tb = lds_addr(W.frt);
     float* yt = W.y + tt * dp;
     const uint32_t pmask = (1u << pbn) - 1u;   // pbpos + pbn <= 32
-#pragma unroll FRU
-    for (int iota = lane; iota < dp; iota += 64) {
+    auto word = [&](int iota) {
         const uint32_t M = W.mask[iota];
         const uint32_t s0 = (M << 2) & 0x3C3C3C3Cu, s1 = (M >> 2) & 0x3C3C3C3Cu;
         uint32_t U = 0;
 #pragma unroll
         for (int g = 0; g < NG; ++g)
             U ^= lds_ld(__builtin_amdgcn_perm(vb, (g & 1) ? s1 : s0, 0x07060500u | (uint32_t)(g >> 1)) + (uint32_t)(g * 64));
+        return U;
+    };
+    auto sum = [&](uint32_t U) {
         const uint32_t e4 = (U << 2) & 0x3C3C3C3Cu, o4 = (U >> 2) & 0x3C3C3C3Cu;
-        float acc = 0.f;
+        float acc = lds_ldf(__builtin_amdgcn_perm(tb, e4, 0x07060500u));
 #pragma unroll
-        for (int i8 = 0; i8 < LG; ++i8)
+        for (int i8 = 1; i8 < LG; ++i8)
             acc += lds_ldf(__builtin_amdgcn_perm(tb, (i8 & 1) ? o4 : e4, 0x07060500u | (uint32_t)(i8 >> 1)) + (uint32_t)(i8 * 64));
+        return acc;
+    };
+    auto store = [&](int iota, uint32_t U, float acc) {
         yt[iota] = acc;
         const uint32_t bits = (U >> pbpos) & pmask;
         if constexpr (PB16) ((uint16_t*)W.pb)[tt * dp + iota] = (uint16_t)bits;
         else ((uint8_t*)W.pb)[tt * dp + iota] = (uint8_t)bits;
+    };
+    int iota = lane;
+    for (; iota + 64 * (FRU - 1) < dp; iota += 64 * FRU) {
+        uint32_t U[FRU];
+        float acc[FRU];
+#pragma unroll
+        for (int u = 0; u < FRU; ++u) U[u] = word(iota + 64 * u);
+#pragma unroll
+        for (int u = 0; u < FRU; ++u) acc[u] = sum(U[u]);
+#pragma unroll
+        for (int u = 0; u < FRU; ++u) store(iota + 64 * u, U[u], acc[u]);
+    }
+    for (; iota < dp; iota += 64) {
+        const uint32_t U = word(iota);
+        store(iota, U, sum(U));
     }
 }
 
