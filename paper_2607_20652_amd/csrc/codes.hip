@@ -319,17 +319,28 @@ __device__ __forceinline__ void fr_coords1(const DevPlan& P, const Wave& W, int 
 // summed by a swizzle (and a permute), after which they hold bit-identical
 // sums (each addition is commutative).
 template <bool EXACT3>
-__device__ __forceinline__ float column_sum(bf16x4 ahi, bf16x4 amid, bf16x4 alo, u32x2 bfe, uint32_t pv)
+__device__ __forceinline__ f32x4 column_acc(bf16x4 ahi, bf16x4 amid, bf16x4 alo, u32x2 bfe)
 {
     const bf16x4 b = __builtin_bit_cast(bf16x4, bfe);
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ahi, b, acc, 0, 0, 0);
     if constexpr (EXACT3) acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(amid, b, acc, 0, 0, 0);
     acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(alo, b, acc, 0, 0, 0);
+    return acc;
+}
+
+__device__ __forceinline__ float column_signs(f32x4 acc, uint32_t pv)
+{
     return (__uint_as_float(__float_as_uint(acc[0]) ^ (pv << 31)) +
             __uint_as_float(__float_as_uint(acc[1]) ^ ((pv >> 1) << 31))) +
            (__uint_as_float(__float_as_uint(acc[2]) ^ ((pv >> 2) << 31)) +
             __uint_as_float(__float_as_uint(acc[3]) ^ ((pv >> 3) << 31)));
+}
+
+template <bool EXACT3>
+__device__ __forceinline__ float column_sum(bf16x4 ahi, bf16x4 amid, bf16x4 alo, u32x2 bfe, uint32_t pv)
+{
+    return column_signs(column_acc<EXACT3>(ahi, amid, alo, bfe), pv);
 }
 
 // Leaf columns when every lane's column belongs to a live token (CPT
@@ -366,9 +377,16 @@ __device__ __forceinline__ void leaf_columns(const DevPlan& P, const Wave& W, bf
             bf[e] = bfr[(int64_t)(cb0 + e) * 64];
             pbv[e] = pb_at(cb0 + e);
         }
+        // four columns' products in flight at once, in accumulators of their own
         float v[NB];
 #pragma unroll
-        for (int e = 0; e < NB; ++e) v[e] = token_sum(column_sum<EXACT3>(ahi, amid, alo, bf[e], pbv[e]));
+        for (int e0 = 0; e0 < NB; e0 += 4) {
+            f32x4 acc[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) acc[u] = column_acc<EXACT3>(ahi, amid, alo, bf[e0 + u]);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) v[e0 + u] = token_sum(column_signs(acc[u], pbv[e0 + u]));
+        }
 #pragma unroll
         for (int e = 0; e < NB; ++e) yt[16 * (cb0 + e)] += P.rsd * v[e];
     }
