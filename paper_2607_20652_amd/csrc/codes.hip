@@ -820,8 +820,10 @@ __device__ __forceinline__ uint32_t unit_pair(uint32_t R)
 
 // grad_coef of the hashed slots that route nowhere: the scaled sum over the
 // coordinates of g(iota) (-1)^{parity(M_iota & c)} for slot index c, with
-// one lane per slot (2, 4 or 8 lanes per slot on the last, partial round,
-// each taking every 2nd, 4th or 8th chunk).  The slot's signs over the 32
+// one lane per slot while 64 or more remain, then 2, 4 or 8 lanes per slot
+// (each taking every 2nd, 4th or 8th chunk) in rounds of 32, 16 and 8 slots,
+// so that the lanes stay busy (48 slots: 32 at two lanes, then 16 at four,
+// 18 chunk steps instead of 24).  The slot's signs over the 32
 // coordinates of chunk w form one word, the XOR of one nibble-table word per
 // 4-bit group of c (parity is linear in the index bits).  bf16 g: dword o of
 // the chunk holds coordinates o and o + 16, which meet the +-1 pair made from
@@ -843,9 +845,10 @@ __device__ void direct_scores(const DevPlan& P, const Wave& W)
             m += __popcll(bal);
         }
         wave_sync();
-        for (int r0 = 0; r0 < m; r0 += 64) {
-            const int mr = min(64, m - r0);
-            const int sh = mr > 32 ? 0 : mr > 16 ? 1 : mr > 8 ? 2 : 3;   // 2^sh lanes per slot
+        for (int r0 = 0; r0 < m;) {
+            const int rem = m - r0;
+            const int sh = rem >= 64 ? 0 : rem >= 32 ? 1 : rem >= 16 ? 2 : 3;   // 2^sh lanes per slot
+            const int mr = min(64 >> sh, rem);
             const int r = lane & ((64 >> sh) - 1), part = lane >> (6 - sh);
             const bool valid = r < mr;
             const int item = list[r0 + (valid ? r : 0)];
@@ -898,6 +901,7 @@ __device__ void direct_scores(const DevPlan& P, const Wave& W)
             float acc = acc0 + acc1;
             for (int off = 64 >> sh; off < 64; off <<= 1) acc += __shfl_xor(acc, off, 64);
             if (valid && part == 0) W.coef[item] = P.rsd * acc;
+            r0 += mr;
         }
         wave_sync();   // the list is rewritten by the next window
     }
