@@ -34,7 +34,7 @@ namespace {
 constexpr int kThreads = 64 * kCodeWaves;
 constexpr int kBatch = 16;    // leaf columns decoded per batch
 constexpr int kBwdBatch = 4;
-constexpr int kDecodeUnroll = 4;  // coordinates of the table decode overlapped (2 in the backward, for registers)  // the same in the backward, whose scoring leaves fewer registers
+constexpr int kDecodeUnroll = 4;  // coordinates of the table decode whose reads are issued together
 
 struct Wave {
     int lane;
@@ -1004,7 +1004,7 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
         }
 
         // grad_x = decode(idx, grad_coef) (+ add_gx); the scoring buffers are dead now
-        decode_tokens<!GX_BF16, NG, PB16, kBwdBatch, 2>(P, W, W.coef);
+        decode_tokens<!GX_BF16, NG, PB16, kBwdBatch, kDecodeUnroll>(P, W, W.coef);
         write_rows<GX_BF16>(P, W, grad_x, add_gx);
         wave_sync();
     }
