@@ -715,15 +715,16 @@ __global__ __launch_bounds__(kThreads) void decode2_kernel(DevPlan P, const int3
     const int64_t ngroups = (T + TPW - 1) / TPW;
     const int64_t gstride = (int64_t)gridDim.x * kCodeWaves;
     // the next group's code is requested while this group is decoded (two
-    // tokens of at most 128 slots: four words of each array per lane)
+    // tokens of at most 128 slots or one of at most 256: four words of each
+    // array per lane)
     constexpr int kPrefetch = 4;
-    const bool pf = TPW == 2 && k <= 128;
+    const bool pf = (TPW == 2 && k <= 128) || (TPW == 1 && k <= 256);
     int32_t nidx[kPrefetch];
     float ncoef[kPrefetch];
     auto fetch = [&](int64_t grp) {
 #pragma unroll
         for (int e = 0; e < kPrefetch; ++e) {
-            const int tt = e >> 1, s = (e & 1) * 64 + lane;
+            const int tt = TPW == 2 ? e >> 1 : 0, s = (TPW == 2 ? (e & 1) : e) * 64 + lane;
             const int64_t t = grp * TPW + tt;
             const bool ok = s < k && t < T;
             nidx[e] = ok ? idx[t * k + s] : -1;
@@ -738,7 +739,7 @@ __global__ __launch_bounds__(kThreads) void decode2_kernel(DevPlan P, const int3
         if (pf) {
 #pragma unroll
             for (int e = 0; e < kPrefetch; ++e) {
-                const int tt = e >> 1, s = (e & 1) * 64 + lane;
+                const int tt = TPW == 2 ? e >> 1 : 0, s = (TPW == 2 ? (e & 1) : e) * 64 + lane;
                 if (s < k) {
                     W.idx[tt * k + s] = nidx[e];
                     W.coef[tt * k + s] = ncoef[e];
@@ -923,7 +924,8 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
     const int64_t ngroups = (T + TPW - 1) / TPW;
     const int64_t gstride = (int64_t)gridDim.x * kCodeWaves;
     // the next group's code is requested while this group is processed
-    // (two tokens of at most 128 slots: four words per lane)
+    // (two tokens of at most 128 slots: four words per lane; the one-token
+    // form costs this kernel a wave per SIMD in registers)
     const bool pf = TPW == 2 && k <= 128;
     int32_t nidx[4];
     auto fetch = [&](int64_t gp) {
