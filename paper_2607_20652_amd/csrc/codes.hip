@@ -908,7 +908,10 @@ __device__ void direct_scores(const DevPlan& P, const Wave& W)
     }
 }
 
-template <bool G_BF16, bool GX_BF16, int NG, bool PB16>
+// PF1: the next group's code is prefetched for waves of one token (a
+// separate instance: selecting the layout at run time costs the two-token
+// form a wave per SIMD in registers).
+template <bool G_BF16, bool GX_BF16, int NG, bool PB16, bool PF1 = false>
 __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const int32_t* __restrict__ idx,
                                                                const void* __restrict__ g, int64_t T,
                                                                float* __restrict__ grad_coef,
@@ -924,14 +927,14 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
     const int64_t ngroups = (T + TPW - 1) / TPW;
     const int64_t gstride = (int64_t)gridDim.x * kCodeWaves;
     // the next group's code is requested while this group is processed
-    // (two tokens of at most 128 slots: four words per lane; the one-token
-    // form costs this kernel a wave per SIMD in registers)
-    const bool pf = TPW == 2 && k <= 128;
+    // (two tokens of at most 128 slots, or with PF1 one of at most 256: four
+    // words per lane)
+    const bool pf = PF1 ? (TPW == 1 && k <= 256) : (TPW == 2 && k <= 128);
     int32_t nidx[4];
     auto fetch = [&](int64_t gp) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const int tt = e >> 1, s = (e & 1) * 64 + lane;
+            const int tt = PF1 ? 0 : e >> 1, s = (PF1 ? e : (e & 1)) * 64 + lane;
             const int64_t t = gp * TPW + tt;
             nidx[e] = (s < k && t < T) ? idx[t * k + s] : -1;
         }
@@ -947,7 +950,7 @@ __global__ __launch_bounds__(kThreads) void decode_bwd2_kernel(DevPlan P, const 
         if (pf) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const int tt = e >> 1, s = (e & 1) * 64 + lane;
+                const int tt = PF1 ? 0 : e >> 1, s = (PF1 ? e : (e & 1)) * 64 + lane;
                 if (s < k) {
                     W.idx[tt * k + s] = nidx[e];
                     W.route[tt * k + s] = -1;
@@ -1120,6 +1123,14 @@ template <bool GB, bool XB, int NG, bool PB>
 static void launch_bwd_v(const DevPlan& P, dim3 grid, size_t lds, hipStream_t stream, const int32_t* idx,
                          const void* g, int64_t T, float* gc, void* gx, BwdExtra ex)
 {
+    if constexpr (GB && XB) {
+        if (P.wave_tokens == 1 && P.k_tot <= 256) {
+            allow_lds(decode_bwd2_kernel<GB, XB, NG, PB, true>, lds);
+            hipLaunchKernelGGL((decode_bwd2_kernel<GB, XB, NG, PB, true>), grid, dim3(kThreads), lds, stream, P, idx, g,
+                               T, gc, gx, ex.gc, ex.gx, ex.stats);
+            return;
+        }
+    }
     allow_lds(decode_bwd2_kernel<GB, XB, NG, PB>, lds);
     hipLaunchKernelGGL((decode_bwd2_kernel<GB, XB, NG, PB>), grid, dim3(kThreads), lds, stream, P, idx, g, T, gc, gx,
                        ex.gc, ex.gx, ex.stats);
