@@ -99,6 +99,24 @@ def test_plans_outside_the_library_limits_are_unsupported(lib, d, level_bits, br
     assert st == -2
 
 
+@pytest.mark.parametrize("d,level_bits,branching,active", [
+    (1536, [11, 16], [0, 64], [2, 64]),
+    (4096, [12, 16], [0, 16], [1, 16]),
+    (2048, [11, 13, 15], [0, 16, 16], [4, 4, 8]),
+])
+def test_wide_rows_with_few_parents_are_within_the_limits(lib, d, level_bits, branching, active):
+    """Hierarchies whose 16-column decode groups would not fit in LDS (d in
+    the thousands, K_0 of 1 to 4) pass validation: the code kernels take
+    fewer tokens per wave.  Without a GPU the call ends at the device upload
+    (DPB_EHIP); with one it succeeds."""
+    h = ctypes.c_void_p()
+    st = lib.dpb_plan_create_ex(ctypes.byref(h), d, len(level_bits), binding._ints(level_bits),
+                                binding._ints(branching), binding._ints(active), None, 0)
+    if st == 0:
+        lib.dpb_plan_destroy(h)
+    assert st in (0, -3)
+
+
 def test_compute_calls_reject_null_plan(lib):
     P = ctypes.c_void_p
     assert lib.dpb_encode(None, P(16), 0, 4, P(16), P(16), None, 0, None) == -1
